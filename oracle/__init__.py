@@ -1,0 +1,214 @@
+"""CPU oracle for the M+Adam optimizer step -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its binding in ``paper_2607_10611_amd``) never imports, links or runs it, and
+the two share no code.
+
+The arithmetic lives in ``madd_oracle.c`` (plain scalar C, FP32 step in one
+fixed operation order, codecs by grid search).  This module compiles it with
+gcc (``build()``) and exposes it through ctypes with numpy arrays.
+
+What each function follows in the paper:
+  * ``step``        -- Algorithm 1 (additive and multiplicative branches,
+                       combine), the optional clamps of Algorithm 2
+                       (Appendix A), rounded into the storage format as in the
+                       FP32-step / BF16-storage round trip of Appendix B.
+  * ``step_block``  -- the same step on FP8 payloads with FP16 block scales
+                       (Section 4.2, FP8 master-weight setting).
+  * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
+                       storage formats' value grids.
+  * ``philox`` / ``draw16`` -- the counter-based generator that keys
+                       stochastic rounding (not defined by the paper).
+
+Parity pins live in ``tests/test_oracle_*.py``.  Function-level status:
+``philox`` is pinned to published known-answer vectors and to rocRAND's
+implementation; everything else is pinned by closed forms, limits,
+invariants, library conversions and brute force (see the tests).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "madd_oracle.c")
+_LIB = os.path.join(_HERE, "libmadd_oracle.so")
+
+# format / rounding numbering of the oracle's C interface
+FMT = {"bf16": 0, "e4m3": 1, "e5m2": 2, "fp32": 3, "fp16": 4}
+GFMT = {"fp32": 0, "bf16": 1}
+ROUND = {"rne": 0, "sr": 1}
+
+_CODE_DTYPE = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,
+               "fp16": np.uint16}
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no fast-math, no FP contraction)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+           "-Wall", "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        path = os.environ.get("MADD_ORACLE_LIB")  # a deliberately mutated copy (mutation tests)
+        if path is None:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+        L = ctypes.CDLL(path)
+        P = ctypes.c_void_p
+        D = ctypes.c_double
+        I = ctypes.c_int
+        I64 = ctypes.c_int64
+        U64 = ctypes.c_uint64
+        U32 = ctypes.c_uint32
+        hp_args = [D] * 11 + [I, I, U64, I64]
+        L.oracle_step.argtypes = [I, P, I, P, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step.restype = I
+        L.oracle_step_block.argtypes = [I, P, P, I, P, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_block.restype = I
+        L.oracle_encode_array.argtypes = [I, P, P, I64]
+        L.oracle_encode_array.restype = I
+        L.oracle_encode_block.argtypes = [I, P, P, P, I64]
+        L.oracle_encode_block.restype = I
+        L.oracle_decode.argtypes = [I, U32]
+        L.oracle_decode.restype = D
+        L.oracle_encode.argtypes = [I, ctypes.c_float, I, U32]
+        L.oracle_encode.restype = U32
+        L.oracle_philox4x32_10.argtypes = [P, P, P]
+        L.oracle_philox4x32_10.restype = None
+        L.oracle_draw16.argtypes = [U64, I64, U32, I64]
+        L.oracle_draw16.restype = U32
+        L.oracle_scalars.argtypes = [D] * 11 + [I, I64, P]
+        L.oracle_scalars.restype = I
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _hp_args(hp: dict):
+    return [float(hp["lr_add"]), float(hp["lr_mul"]), float(hp["beta1"]), float(hp["beta2"]),
+            float(hp["eps"]), float(hp["tau"]), float(hp["r_max"]), float(hp["eps0"]),
+            float(hp["g_max"]), float(hp["d_mult_max"]), float(hp["w_max"]),
+            int(hp["bias_correction"]), ROUND[hp["rounding"]], int(hp["seed"]) & (2**64 - 1),
+            int(hp["step"])]
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check_state(n, g, m, v, ve, gfmt):
+    gd = np.float32 if gfmt == "fp32" else np.uint16
+    for name, a, dt in (("g", g, gd), ("m", m, np.float32), ("v", v, np.float32),
+                        ("ve", ve, np.float32)):
+        if a.dtype != dt or a.size != n:
+            raise OracleError(f"{name}: expected {n} x {np.dtype(dt)}, got {a.size} x {a.dtype}")
+
+
+def step(wfmt: str, w: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, ve: np.ndarray,
+         hp: dict, gfmt: str = "fp32", index_base: int = 0, gidx: np.ndarray | None = None):
+    """One M+Adam step in place on host arrays (w codes, g, m, v, ve).
+
+    ``gidx`` (int64, one per element) gives each element's global index for the
+    stochastic-rounding draw; without it element i has index ``index_base + i``.
+    """
+    n = w.size
+    if w.dtype != _CODE_DTYPE[wfmt]:
+        raise OracleError(f"w: expected {np.dtype(_CODE_DTYPE[wfmt])} codes, got {w.dtype}")
+    _check_state(n, g, m, v, ve, gfmt)
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+        assert gidx.size == n
+    rc = lib().oracle_step(FMT[wfmt], _ptr(w), GFMT[gfmt], _ptr(g), _ptr(m), _ptr(v), _ptr(ve),
+                           n, _ptr(gidx), int(index_base), *_hp_args(hp))
+    if rc != 0:
+        raise OracleError(f"oracle_step returned {rc}")
+
+
+def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray,
+               v: np.ndarray, ve: np.ndarray, hp: dict, gfmt: str = "fp32", index_base: int = 0,
+               gidx: np.ndarray | None = None):
+    """Block-scaled FP8 step (blocks of 128 contiguous elements, FP16 scales)."""
+    n = q.size
+    if q.dtype != np.uint8 or scales.dtype != np.uint16 or scales.size * 128 != n:
+        raise OracleError("q must be uint8 codes and scales uint16, one per 128 elements")
+    _check_state(n, g, m, v, ve, gfmt)
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+        assert gidx.size == n
+    rc = lib().oracle_step_block(FMT[wfmt], _ptr(q), _ptr(scales), GFMT[gfmt], _ptr(g), _ptr(m),
+                                 _ptr(v), _ptr(ve), n, _ptr(gidx), int(index_base),
+                                 *_hp_args(hp))
+    if rc != 0:
+        raise OracleError(f"oracle_step_block returned {rc}")
+
+
+def encode_array(fmt: str, x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.size, dtype=_CODE_DTYPE[fmt])
+    if lib().oracle_encode_array(FMT[fmt], _ptr(x), _ptr(out), x.size) != 0:
+        raise OracleError("oracle_encode_array failed")
+    return out
+
+
+def encode_block(fmt: str, x: np.ndarray):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.empty(x.size, dtype=np.uint8)
+    s = np.empty(x.size // 128, dtype=np.uint16)
+    if lib().oracle_encode_block(FMT[fmt], _ptr(x), _ptr(q), _ptr(s), x.size) != 0:
+        raise OracleError("oracle_encode_block failed")
+    return q, s
+
+
+def decode(fmt: str, code: int) -> float:
+    return lib().oracle_decode(FMT[fmt], int(code))
+
+
+def decode_array(fmt: str, codes: np.ndarray) -> np.ndarray:
+    return np.array([decode(fmt, int(c)) for c in codes.ravel()], dtype=np.float64)
+
+
+def encode(fmt: str, x: float, rounding: str = "rne", r16: int = 0) -> int:
+    return int(lib().oracle_encode(FMT[fmt], float(np.float32(x)), ROUND[rounding], int(r16)))
+
+
+def philox(ctr, key):
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def draw16(seed: int, step_: int, stream: int, idx: int) -> int:
+    return int(lib().oracle_draw16(int(seed) & (2**64 - 1), int(step_), int(stream), int(idx)))
+
+
+def scalars(hp: dict) -> dict:
+    out = np.zeros(13, dtype=np.float32)
+    a = _hp_args(hp)
+    rc = lib().oracle_scalars(*a[:11], a[11], a[14], _ptr(out))
+    if rc != 0:
+        raise OracleError("oracle_scalars failed")
+    names = ["B1", "B2", "OMB1", "OMB2", "SA", "IBC2", "LRM", "EPS", "TAU", "GMAX", "ULO", "UHI",
+             "WMAX"]
+    return dict(zip(names, out.tolist()))

@@ -1,0 +1,580 @@
+/*
+ * CPU oracle for the M+Adam optimizer step.  TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, scalar C.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this library; the product path (the HIP
+ * library) never does, and the two share no source, header or table.
+ *
+ * What it computes, by the paper's section / algorithm / equation:
+ *
+ *   Algorithm 1 (M+Adam: additive-multiplicative update), restated in
+ *   Section 3.1 (Additive-Multiplicative Updates):
+ *     additive branch        u <- b1 u + (1-b1) g ;  v <- b2 v + (1-b2) g^2
+ *                            u^ = u/(1-b1^t), v^ = v/(1-b2^t)
+ *                            u_a = -eta_a u^/(sqrt(v^)+eps)
+ *     multiplicative branch  g_e = ln2 * w * g        (gradient w.r.t. the exponent)
+ *                            v_e <- b2 v_e + (1-b2) g_e^2 ;  v_e^ = v_e/(1-b2^t)
+ *                            ut_m = -eta_m g_e/(sqrt(v_e^)+eps)
+ *                            rho = max(|w|, tau) ;  u_m = clip(ut_m/rho)
+ *     combine                w <- w + w u_m + u_a
+ *
+ *   Algorithm 2 (Appendix A, detailed algorithm) adds the optional clamps used
+ *   here as options: clamp_{g_max} of the normalised multiplicative direction,
+ *   the clip of u_m to [-(0.75-eps0), 0.75], the exponent-step cap
+ *   clamp_{d_mult,max}(log2(1+u_m)) followed by u_m = 2^de - 1, and the final
+ *   weight clamp clamp_{w_max}(w).  Algorithm 2 is printed without bias
+ *   correction; bias_correction = 0 reproduces it, 1 gives Algorithm 1.
+ *
+ *   Appendix B (BF16-stored matrix fitting) fixes the precision: the step is
+ *   computed in FP32 and the weight is rounded into the storage format before
+ *   the next step.  This oracle generalises that round trip from BF16 to the
+ *   FP8 storage of Section 4.2 (FP8 payload with FP16 block scales).
+ *
+ * Readings where the paper is silent (each is listed in the design notes):
+ *   - FP32 operation order: one fixed sequence (oracle_step_elem below); every
+ *     line is one IEEE binary32 operation with round-to-nearest-even, fmaf is
+ *     one rounding, division and square root are correctly rounded.
+ *   - The hyper-parameter scalars are evaluated in double and rounded once to
+ *     float: B1, B2, 1-B1, 1-B2, SA = eta_a/(1-b1^t), IBC2 = 1/(1-b2^t), and
+ *     the u_m clip bounds.
+ *   - The exponent-step cap is applied as the equivalent clamp of u_m to
+ *     [2^-d - 1, 2^d - 1] (log2 is monotone), so no transcendental is
+ *     evaluated per element.
+ *   - Stochastic rounding (cited, not defined, in the paper): on the
+ *     magnitude a = |x| with grid neighbours lo <= a < hi,
+ *     k = floor((a-lo)/(hi-lo) * 2^16), round up iff k + r16 >= 2^16, where
+ *     r16 is a 16-bit draw.  For BF16 this is exact: P(up) = (a-lo)/(hi-lo).
+ *   - The 16-bit draw for global element index i at step t is a 16-bit lane
+ *     of Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11) with key
+ *     (seed lo32, seed hi32) and counter (j lo32, j hi32, t, stream), j = i>>3:
+ *     lane (i & 7) = bits 16*(i&1) .. +15 of output word (i&7)>>1.
+ *   - FP8 formats: OCP E4M3 (bias 7, no Inf, NaN = S.1111.111, max 448) and
+ *     E5M2 (bias 15, IEEE specials, max 57344), both saturating finite
+ *     overflow (and Inf) to +-max; NaN encodes as the positive code 0x7F
+ *     (0.1111.111 / 0.11111.11) in both.
+ *   - BF16 / FP16 follow IEEE: overflow under RNE rounds to Inf, NaN encodes
+ *     as the positive quiet NaN 0x7FC0 / 0x7E00 (a NaN's sign is not
+ *     meaningful, so it is dropped).
+ *   - FP32 "storage" (test passthrough) keeps the float bits; a NaN is stored
+ *     as 0x7FC00000.
+ *   - Block-scaled FP8: contiguous blocks of 128 elements, one FP16 scale s
+ *     per block, weight = q * s (fp32 product).  After the update,
+ *     amax = max|w'| over the block; s' = RNE_fp16(amax / FMAX) with
+ *     s' = 1 when amax = 0, the smallest FP16 subnormal when it underflows to
+ *     0, the largest finite FP16 when it overflows, and FP16 NaN when any w'
+ *     of the block is not finite; q' = encode(w'/s') with the block's
+ *     rounding mode.
+ *
+ * Codec implementation: values are decoded from the (sign, exponent,
+ * mantissa) definition of each format; encoding searches the sorted table of
+ * decoded grid values for the neighbours of |x| and decides with exact double
+ * arithmetic (no bit manipulation of the float representation).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OF_BF16 = 0, OF_E4M3 = 1, OF_E5M2 = 2, OF_FP32 = 3, OF_FP16 = 4, OF_NFMT = 5 };
+enum { OG_FP32 = 0, OG_BF16 = 1 };
+enum { OR_RNE = 0, OR_SR = 1 };
+
+enum {
+  ORACLE_OK = 0,
+  ORACLE_EINVAL = -1,
+};
+
+/* ------------------------------------------------------------------------ */
+/* Storage formats, from their definitions                                   */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int ebits, mbits, bias;
+  int ieee_special; /* all-ones exponent field: Inf (mantissa 0) or NaN        */
+  int satfinite;    /* finite overflow and Inf saturate to +-max                */
+  uint32_t nan_code;
+  uint32_t inf_code;
+  /* sorted non-negative finite grid */
+  int nval;
+  double *val;
+  uint32_t *code;
+  double max;
+  uint32_t max_code;
+  double beyond; /* next grid point above max if the exponent were unbounded */
+} ofmt;
+
+static ofmt g_fmt[OF_NFMT];
+static int g_ready = 0;
+
+static double decode_def(const ofmt *f, uint32_t c) {
+  const int nb = f->ebits + f->mbits;
+  const uint32_t s = (c >> nb) & 1u;
+  const uint32_t e = (c >> f->mbits) & ((1u << f->ebits) - 1u);
+  const uint32_t m = c & ((1u << f->mbits) - 1u);
+  const uint32_t eall = (1u << f->ebits) - 1u, mall = (1u << f->mbits) - 1u;
+  double mag;
+  if (f->ieee_special && e == eall) {
+    mag = m ? NAN : INFINITY;
+  } else if (!f->ieee_special && e == eall && m == mall) {
+    mag = NAN; /* E4M3: only S.1111.111 is special */
+  } else if (e == 0) {
+    mag = ldexp((double)m, 1 - f->bias - f->mbits); /* subnormal */
+  } else {
+    mag = ldexp((double)((1u << f->mbits) + m), (int)e - f->bias - f->mbits);
+  }
+  return s ? -mag : mag;
+}
+
+typedef struct {
+  double v;
+  uint32_t c;
+} vc_pair;
+
+static int cmp_vc(const void *a, const void *b) {
+  const double x = ((const vc_pair *)a)->v, y = ((const vc_pair *)b)->v;
+  return (x > y) - (x < y);
+}
+
+static void fmt_init(ofmt *f, int ebits, int mbits, int bias, int ieee, int sat) {
+  f->ebits = ebits;
+  f->mbits = mbits;
+  f->bias = bias;
+  f->ieee_special = ieee;
+  f->satfinite = sat;
+  const int nb = ebits + mbits;
+  const uint32_t ncodes = 1u << nb; /* codes with the sign bit clear */
+  vc_pair *tmp = (vc_pair *)malloc(sizeof(vc_pair) * ncodes);
+  int n = 0;
+  for (uint32_t c = 0; c < ncodes; ++c) {
+    const double x = decode_def(f, c);
+    if (isfinite(x)) {
+      tmp[n].v = x;
+      tmp[n].c = c;
+      ++n;
+    } else if (isinf(x)) {
+      f->inf_code = c;
+    }
+  }
+  qsort(tmp, (size_t)n, sizeof(vc_pair), cmp_vc);
+  f->nval = n;
+  f->val = (double *)malloc(sizeof(double) * (size_t)n);
+  f->code = (uint32_t *)malloc(sizeof(uint32_t) * (size_t)n);
+  for (int i = 0; i < n; ++i) {
+    f->val[i] = tmp[i].v;
+    f->code[i] = tmp[i].c;
+  }
+  free(tmp);
+  f->max = f->val[n - 1];
+  f->max_code = f->code[n - 1];
+  /* spacing at the top binade, continued one more step */
+  f->beyond = f->max + (f->val[n - 1] - f->val[n - 2]);
+}
+
+static void init_formats(void) {
+  if (g_ready) return;
+  fmt_init(&g_fmt[OF_BF16], 8, 7, 127, 1, 0);
+  fmt_init(&g_fmt[OF_E4M3], 4, 3, 7, 0, 1);
+  fmt_init(&g_fmt[OF_E5M2], 5, 2, 15, 1, 1);
+  fmt_init(&g_fmt[OF_FP16], 5, 10, 15, 1, 0);
+  /* canonical NaN codes (positive) */
+  g_fmt[OF_BF16].nan_code = 0x7FC0u;
+  g_fmt[OF_FP16].nan_code = 0x7E00u;
+  g_fmt[OF_E4M3].nan_code = 0x7Fu;
+  g_fmt[OF_E5M2].nan_code = 0x7Fu;
+  /* OF_FP32 is a passthrough and has no grid */
+  g_ready = 1;
+}
+
+static int fmt_bits(int fmt) {
+  switch (fmt) {
+  case OF_BF16: return 16;
+  case OF_FP16: return 16;
+  case OF_E4M3: return 8;
+  case OF_E5M2: return 8;
+  case OF_FP32: return 32;
+  default: return 0;
+  }
+}
+
+static uint32_t f32_bits(float x) {
+  uint32_t u;
+  memcpy(&u, &x, 4);
+  return u;
+}
+
+static float f32_from_bits(uint32_t u) {
+  float x;
+  memcpy(&x, &u, 4);
+  return x;
+}
+
+/* Value of a stored code, as a double (exact). */
+static double decode(int fmt, uint32_t code) {
+  if (fmt == OF_FP32) return (double)f32_from_bits(code);
+  return decode_def(&g_fmt[fmt], code);
+}
+
+/* Round the fp32 value x into format fmt.  mode = OR_RNE (nearest, ties to the
+ * code with an even last mantissa bit) or OR_SR (stochastic, draw r16). */
+static uint32_t encode(int fmt, float xf, int mode, uint32_t r16) {
+  if (fmt == OF_FP32) return isnan(xf) ? 0x7FC00000u : f32_bits(xf);
+  const ofmt *f = &g_fmt[fmt];
+  const int nb = f->ebits + f->mbits;
+  const uint32_t sign = signbit(xf) ? (1u << nb) : 0u;
+  if (isnan(xf)) return f->nan_code; /* the sign of a NaN carries no meaning */
+  const double a = fabs((double)xf);
+  if (f->satfinite && a >= f->max) return sign | f->max_code;
+  if (!f->satfinite && isinf(a)) return sign | f->inf_code;
+
+  /* largest grid index i with val[i] <= a */
+  int lo_i = 0, hi_i = f->nval - 1;
+  while (lo_i < hi_i) {
+    const int mid = (lo_i + hi_i + 1) / 2;
+    if (f->val[mid] <= a) lo_i = mid;
+    else hi_i = mid - 1;
+  }
+  const double lo = f->val[lo_i];
+  if (lo == a) return sign | f->code[lo_i];
+  double hi;
+  uint32_t hi_code;
+  if (lo_i + 1 < f->nval) {
+    hi = f->val[lo_i + 1];
+    hi_code = f->code[lo_i + 1];
+  } else {
+    /* above the largest finite value of an IEEE format: the next point of
+     * the unbounded grid stands for Inf */
+    hi = f->beyond;
+    hi_code = f->inf_code;
+  }
+  const uint32_t lo_code = f->code[lo_i];
+  uint32_t out;
+  if (mode == OR_RNE) {
+    const double dlo = a - lo, dhi = hi - a; /* exact */
+    if (dlo < dhi) out = lo_code;
+    else if (dhi < dlo) out = hi_code;
+    else out = (lo_code & 1u) ? hi_code : lo_code;
+  } else {
+    const double frac = (a - lo) / (hi - lo); /* exact: spacing is a power of two */
+    const double k = floor(frac * 65536.0);
+    out = (k + (double)r16 >= 65536.0) ? hi_code : lo_code;
+  }
+  return sign | out;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw; SC'11)                         */
+/* ------------------------------------------------------------------------ */
+
+static void philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4]) {
+  uint32_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+  uint32_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += 0x9E3779B9u; /* golden ratio */
+      k1 += 0xBB67AE85u; /* sqrt(3) - 1 */
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
+    const uint32_t n1 = (uint32_t)p1;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    const uint32_t n3 = (uint32_t)p0;
+    c[0] = n0;
+    c[1] = n1;
+    c[2] = n2;
+    c[3] = n3;
+  }
+  out[0] = c[0];
+  out[1] = c[1];
+  out[2] = c[2];
+  out[3] = c[3];
+}
+
+/* 16-bit draw for global element index idx at step t on stream `stream`. */
+static uint32_t draw16(uint64_t seed, int64_t t, uint32_t stream, int64_t idx) {
+  const uint64_t j = (uint64_t)idx >> 3;
+  const uint32_t ctr[4] = {(uint32_t)j, (uint32_t)(j >> 32), (uint32_t)t, stream};
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t out[4];
+  philox4x32_10(ctr, key, out);
+  const uint32_t lane = (uint32_t)((uint64_t)idx & 7u);
+  const uint32_t word = out[lane >> 1];
+  return (lane & 1u) ? (word >> 16) : (word & 0xFFFFu);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The step                                                                  */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  double lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max, w_max;
+  int bias_correction, rounding;
+  uint64_t seed;
+  int64_t step;
+} ohp;
+
+typedef struct {
+  float B1, B2, OMB1, OMB2, SA, IBC2, LRM, EPS, TAU, GMAX, ULO, UHI, WMAX;
+} oscal;
+
+static int check_hp(const ohp *h) {
+  if (!(h->beta1 >= 0.0 && h->beta1 < 1.0)) return ORACLE_EINVAL;
+  if (!(h->beta2 >= 0.0 && h->beta2 < 1.0)) return ORACLE_EINVAL;
+  if (!(h->eps >= 0.0)) return ORACLE_EINVAL;
+  if (!(h->tau > 0.0)) return ORACLE_EINVAL;
+  if (!(h->r_max > 0.0 && h->r_max < 1.0)) return ORACLE_EINVAL;
+  if (!(h->eps0 >= 0.0 && h->eps0 < h->r_max)) return ORACLE_EINVAL;
+  if (!(h->g_max > 0.0) || !(h->d_mult_max > 0.0) || !(h->w_max > 0.0)) return ORACLE_EINVAL;
+  if (h->step < 1 || h->step > 0xFFFFFFFFll) return ORACLE_EINVAL;
+  if (h->rounding != OR_RNE && h->rounding != OR_SR) return ORACLE_EINVAL;
+  if (h->bias_correction != 0 && h->bias_correction != 1) return ORACLE_EINVAL;
+  return ORACLE_OK;
+}
+
+static void make_scalars(const ohp *h, oscal *s) {
+  const double t = (double)h->step;
+  s->B1 = (float)h->beta1;
+  s->B2 = (float)h->beta2;
+  s->OMB1 = (float)(1.0 - h->beta1);
+  s->OMB2 = (float)(1.0 - h->beta2);
+  if (h->bias_correction) {
+    s->SA = (float)(h->lr_add / (1.0 - pow(h->beta1, t)));
+    s->IBC2 = (float)(1.0 / (1.0 - pow(h->beta2, t)));
+  } else {
+    s->SA = (float)h->lr_add;
+    s->IBC2 = 1.0f;
+  }
+  s->LRM = (float)h->lr_mul;
+  s->EPS = (float)h->eps;
+  s->TAU = (float)h->tau;
+  s->GMAX = (float)h->g_max;
+  double ulo = -(h->r_max - h->eps0), uhi = h->r_max;
+  if (isfinite(h->d_mult_max)) {
+    /* |log2(1+u)| <= d  <=>  2^-d - 1 <= u <= 2^d - 1 */
+    const double lo_cap = exp2(-h->d_mult_max) - 1.0, hi_cap = exp2(h->d_mult_max) - 1.0;
+    if (lo_cap > ulo) ulo = lo_cap;
+    if (hi_cap < uhi) uhi = hi_cap;
+  }
+  s->ULO = (float)ulo;
+  s->UHI = (float)uhi;
+  s->WMAX = (float)h->w_max;
+}
+
+/* NaN passes through: both comparisons are false. */
+static float clampf(float x, float lo, float hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+/* One element of the step in the fixed FP32 order; returns the unrounded new
+ * weight and updates the three moments in place. */
+static float oracle_step_elem(float w, float g, float *pm, float *pv, float *pve, const oscal *s) {
+  const float LN2 = (float)0.69314718055994530942; /* fp32(ln 2) */
+  /* additive branch (Algorithm 1; Algorithm 2 without bias correction) */
+  const float m = fmaf(s->B1, *pm, s->OMB1 * g);
+  const float v = fmaf(s->B2, *pv, s->OMB2 * (g * g));
+  const float den_a = sqrtf(v * s->IBC2) + s->EPS;
+  const float ua = -((s->SA * m) / den_a);
+  /* multiplicative branch: gradient w.r.t. the exponent, second moment */
+  const float ge = (LN2 * w) * g;
+  const float ve = fmaf(s->B2, *pve, s->OMB2 * (ge * ge));
+  const float den_m = sqrtf(ve * s->IBC2) + s->EPS;
+  const float r = clampf(ge / den_m, -s->GMAX, s->GMAX);
+  const float ut = -(s->LRM * r);
+  /* relative conversion: rho = max(|w|, tau), then the u_m clip and cap */
+  const float aw = fabsf(w);
+  const float rho = aw > s->TAU ? aw : s->TAU;
+  const float um = clampf(ut / rho, s->ULO, s->UHI);
+  /* combine: w + w u_m + u_a, then the optional final weight clamp */
+  float wn = fmaf(w, um, w) + ua;
+  wn = clampf(wn, -s->WMAX, s->WMAX);
+  *pm = m;
+  *pv = v;
+  *pve = ve;
+  return wn;
+}
+
+static float load_grad(int gfmt, const void *g, int64_t i) {
+  if (gfmt == OG_FP32) return ((const float *)g)[i];
+  return (float)decode(OF_BF16, ((const uint16_t *)g)[i]);
+}
+
+static uint32_t load_code(int fmt, const void *w, int64_t i) {
+  switch (fmt_bits(fmt)) {
+  case 8: return ((const uint8_t *)w)[i];
+  case 16: return ((const uint16_t *)w)[i];
+  default: return ((const uint32_t *)w)[i];
+  }
+}
+
+static void store_code(int fmt, void *w, int64_t i, uint32_t c) {
+  switch (fmt_bits(fmt)) {
+  case 8: ((uint8_t *)w)[i] = (uint8_t)c; break;
+  case 16: ((uint16_t *)w)[i] = (uint16_t)c; break;
+  default: ((uint32_t *)w)[i] = c; break;
+  }
+}
+
+static int fill_hp(ohp *h, double lr_add, double lr_mul, double beta1, double beta2, double eps,
+                   double tau, double r_max, double eps0, double g_max, double d_mult_max,
+                   double w_max, int bias_correction, int rounding, uint64_t seed, int64_t step) {
+  h->lr_add = lr_add;
+  h->lr_mul = lr_mul;
+  h->beta1 = beta1;
+  h->beta2 = beta2;
+  h->eps = eps;
+  h->tau = tau;
+  h->r_max = r_max;
+  h->eps0 = eps0;
+  h->g_max = g_max;
+  h->d_mult_max = d_mult_max;
+  h->w_max = w_max;
+  h->bias_correction = bias_correction;
+  h->rounding = rounding;
+  h->seed = seed;
+  h->step = step;
+  return check_hp(h);
+}
+
+/* Per-element M+Adam step on an unscaled storage format.
+ * Element i has global index gidx[i] (or index_base + i when gidx is NULL),
+ * which keys its stochastic-rounding draw. */
+int oracle_step(int wfmt, void *w, int gfmt, const void *g, float *m, float *v, float *ve,
+                int64_t n, const int64_t *gidx, int64_t index_base, double lr_add, double lr_mul,
+                double beta1, double beta2, double eps, double tau, double r_max, double eps0,
+                double g_max, double d_mult_max, double w_max, int bias_correction, int rounding,
+                uint64_t seed, int64_t step) {
+  init_formats();
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
+              w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (wfmt != OF_BF16 && wfmt != OF_E4M3 && wfmt != OF_E5M2 && wfmt != OF_FP32) return ORACLE_EINVAL;
+  if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (n < 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  for (int64_t i = 0; i < n; ++i) {
+    const float wv = (float)decode(wfmt, load_code(wfmt, w, i));
+    const float gv = load_grad(gfmt, g, i);
+    const float wn = oracle_step_elem(wv, gv, &m[i], &v[i], &ve[i], &s);
+    const int64_t idx = gidx ? gidx[i] : index_base + i;
+    const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+    store_code(wfmt, w, i, encode(wfmt, wn, h.rounding, r16));
+  }
+  return ORACLE_OK;
+}
+
+#define BLOCK 128
+
+static float fp8_max(int fmt) { return (float)g_fmt[fmt].max; }
+
+/* FP16 scale for one block of updated weights (rule in the file header). */
+static uint16_t block_scale(int fmt, const float *wn) {
+  double amax = 0.0;
+  int nonfinite = 0;
+  for (int i = 0; i < BLOCK; ++i) {
+    if (!isfinite(wn[i])) nonfinite = 1;
+    else if (fabs((double)wn[i]) > amax) amax = fabs((double)wn[i]);
+  }
+  if (nonfinite) return 0x7E00u;
+  if (amax == 0.0) return 0x3C00u; /* 1.0 */
+  const float ratio = (float)amax / fp8_max(fmt);
+  uint32_t sc = encode(OF_FP16, ratio, OR_RNE, 0u);
+  if (sc == 0u) sc = 0x0001u;       /* underflow: smallest subnormal */
+  if (sc == 0x7C00u) sc = 0x7BFFu;  /* overflow: largest finite */
+  return (uint16_t)sc;
+}
+
+/* Block-scaled FP8 M+Adam step.  n must be a multiple of 128; elements
+ * [128 b, 128 b + 128) form block b with scale scales[b]. */
+int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const void *g, float *m,
+                      float *v, float *ve, int64_t n, const int64_t *gidx, int64_t index_base,
+                      double lr_add, double lr_mul, double beta1, double beta2, double eps,
+                      double tau, double r_max, double eps0, double g_max, double d_mult_max,
+                      double w_max, int bias_correction, int rounding, uint64_t seed,
+                      int64_t step) {
+  init_formats();
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
+              w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (wfmt != OF_E4M3 && wfmt != OF_E5M2) return ORACLE_EINVAL;
+  if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (n < 0 || n % BLOCK != 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  float wn[BLOCK];
+  for (int64_t b = 0; b < n / BLOCK; ++b) {
+    const float sold = (float)decode(OF_FP16, scales[b]);
+    for (int k = 0; k < BLOCK; ++k) {
+      const int64_t i = b * BLOCK + k;
+      const float wv = (float)decode(wfmt, q[i]) * sold;
+      const float gv = load_grad(gfmt, g, i);
+      wn[k] = oracle_step_elem(wv, gv, &m[i], &v[i], &ve[i], &s);
+    }
+    const uint16_t snew = block_scale(wfmt, wn);
+    const float sf = (float)decode(OF_FP16, snew);
+    for (int k = 0; k < BLOCK; ++k) {
+      const int64_t i = b * BLOCK + k;
+      const int64_t idx = gidx ? gidx[i] : index_base + i;
+      const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+      q[i] = (uint8_t)encode(wfmt, wn[k] / sf, h.rounding, r16);
+    }
+    scales[b] = snew;
+  }
+  return ORACLE_OK;
+}
+
+/* Round fp32 values into a storage format with round-to-nearest-even. */
+int oracle_encode_array(int fmt, const float *x, void *codes, int64_t n) {
+  init_formats();
+  if (fmt < 0 || fmt >= OF_NFMT || n < 0) return ORACLE_EINVAL;
+  for (int64_t i = 0; i < n; ++i) store_code(fmt, codes, i, encode(fmt, x[i], OR_RNE, 0u));
+  return ORACLE_OK;
+}
+
+/* Block-scaled FP8 encoding of fp32 values with round-to-nearest-even. */
+int oracle_encode_block(int fmt, const float *x, uint8_t *q, uint16_t *scales, int64_t n) {
+  init_formats();
+  if ((fmt != OF_E4M3 && fmt != OF_E5M2) || n < 0 || n % BLOCK != 0) return ORACLE_EINVAL;
+  for (int64_t b = 0; b < n / BLOCK; ++b) {
+    const uint16_t sc = block_scale(fmt, x + b * BLOCK);
+    const float sf = (float)decode(OF_FP16, sc);
+    for (int k = 0; k < BLOCK; ++k)
+      q[b * BLOCK + k] = (uint8_t)encode(fmt, x[b * BLOCK + k] / sf, OR_RNE, 0u);
+    scales[b] = sc;
+  }
+  return ORACLE_OK;
+}
+
+/* --- small exports used by the tests ------------------------------------ */
+
+double oracle_decode(int fmt, uint32_t code) {
+  init_formats();
+  return decode(fmt, code);
+}
+
+uint32_t oracle_encode(int fmt, float x, int rounding, uint32_t r16) {
+  init_formats();
+  return encode(fmt, x, rounding, r16 & 0xFFFFu);
+}
+
+void oracle_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out) {
+  philox4x32_10(ctr, key, out);
+}
+
+uint32_t oracle_draw16(uint64_t seed, int64_t step, uint32_t stream, int64_t idx) {
+  return draw16(seed, step, stream, idx);
+}
+
+/* The fp32 scalars of one step, in the order of oscal. */
+int oracle_scalars(double lr_add, double lr_mul, double beta1, double beta2, double eps,
+                   double tau, double r_max, double eps0, double g_max, double d_mult_max,
+                   double w_max, int bias_correction, int64_t step, float *out13) {
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max, w_max,
+              bias_correction, OR_RNE, 0u, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  memcpy(out13, &s, sizeof(oscal));
+  return ORACLE_OK;
+}
