@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the M+Adam optimizer step on one MI355X.
+
+A step is one madd_multi_tensor_step call over the whole parameter list (one
+kernel launch for a single-format list): read weight codes, gradients and the
+three fp32 moments, update, round the weights back with stochastic rounding,
+write back.  Default workload: the Llama-7B-shaped list (291 tensors,
+6,738,415,616 parameters, bf16 weights, fp32 gradients and m / v / v_e),
+all resident in HBM before timing starts.  Gradients are synthetic (two
+pre-generated sets, alternating between steps).
+
+Prints one JSON line with optimizer-step throughput (Gparam/s), the achieved
+HBM bandwidth of the step kernel against the 8 TB/s peak, and the CPU oracle
+timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "optimizer-step Gparams/s + achieved HBM GB/s (% of peak), 7B-shaped set"
+HBM_PEAK_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
+
+# algorithmic bytes per parameter: read w + g + m + v + v_e, write w + m + v + v_e
+BYTES_PER_PARAM = {"bf16": 2 + 4 + 12 + 2 + 12, "e4m3": 1 + 4 + 12 + 1 + 12,
+                   "e5m2": 1 + 4 + 12 + 1 + 12}
+
+WORKLOAD_NAMES = {
+    "c5": "llama-7b-shaped list (32 layers, d=4096, SwiGLU 11008, vocab 32000)",
+    "c3": "llama-1.1b-shaped list (22 layers, d=2048, GQA 32/4, SwiGLU 5632, vocab 32000)",
+    "c4": "llama-1.1b-shaped list in fp8 e4m3",
+    "c2": "gpt2-small-shaped list (12 layers, d=768, vocab 50257)",
+}
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+
+
+def traffic_from_profile():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when it is missing or was taken on a different kernel source."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    text = open(PMC_SUMMARY).read()
+    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_sha():
+        return None
+    return float(val.group(1))
+
+
+def cpu_baseline(cfg: str, sample: int, steps: int) -> dict:
+    """The CPU oracle (single thread) on a bounded sample of the workload: the
+    first `sample` elements of the list, `steps` steps."""
+    import numpy as np
+
+    import oracle
+    from paper_2607_10611_amd import workloads as W
+
+    specs = W.specs(cfg)
+    wfmt = W.CONFIGS[cfg]["wfmt"]
+    xs, gs, left = [], [], sample
+    for i, s in enumerate(specs):
+        k = min(left, s.numel)
+        xs.append(W.init_fp32(cfg, i, k))
+        gs.append([W.grad_fp32(cfg, i, t, k) for t in range(1, steps + 1)])
+        left -= k
+        if left == 0:
+            break
+    codes = oracle.encode_array(wfmt, np.concatenate(xs))
+    grads = [np.concatenate([g[t] for g in gs]) for t in range(steps)]
+    m, v, ve = (np.zeros(sample, np.float32) for _ in range(3))
+    t0 = time.perf_counter()
+    for t in range(1, steps + 1):
+        oracle.step(wfmt, codes, grads[t - 1], m, v, ve, W.hparams(cfg, step=t))
+    dt = time.perf_counter() - t0
+    return {"value": sample * steps / dt / 1e9, "unit": "Gparam/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {sample:,} parameters of the list, {steps} steps "
+                      f"({dt:.1f} s, single-threaded scalar C)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--cpu-sample", type=int, default=1 << 23)
+    ap.add_argument("--cpu-steps", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the optimizer step on one GPU only; multi-GPU runs are not "
+              "part of this build (the step shards by index range without communication).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_10611_amd import binding as B
+    from paper_2607_10611_amd import workloads as W
+
+    B.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = args.config
+    wfmt = W.CONFIGS[cfg]["wfmt"]
+    specs = W.specs(cfg)
+    nparam = W.total_params(cfg)
+    code_dt = torch.int16 if wfmt == "bf16" else torch.uint8
+
+    log(f"workload {cfg}: {len(specs)} tensors, {nparam:,} params, {wfmt} weights")
+    t0 = time.perf_counter()
+    ws, ms, vs, ves = [], [], [], []
+    for i, s in enumerate(specs):
+        x = W.init_fp32_device(cfg, i, dev)
+        w = torch.empty(s.numel, dtype=code_dt, device=dev)
+        B.madd_encode_weights(x, w, wfmt)
+        del x
+        ws.append(w)
+        m = torch.empty(s.numel, dtype=torch.float32, device=dev)
+        v = torch.empty_like(m)
+        ve = torch.empty_like(m)
+        B.madd_init_state(m, v, ve)
+        ms.append(m)
+        vs.append(v)
+        ves.append(ve)
+    grad_sets = []
+    for k in range(2):
+        gl = []
+        for i, s in enumerate(specs):
+            g = torch.empty(s.numel, dtype=torch.float32, device=dev)
+            W.grad_fp32_device_(cfg, i, k + 1, g)
+            gl.append(g)
+        grad_sets.append(gl)
+    torch.cuda.synchronize()
+    log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
+        f"{time.perf_counter() - t0:.1f} s")
+
+    lists = [B.TensorList(ws, [wfmt] * len(ws), gl, ms, vs, ves) for gl in grad_sets]
+    stream = torch.cuda.current_stream()
+    step_no = 0
+
+    def one_step():
+        nonlocal step_no
+        step_no += 1
+        B.madd_multi_tensor_step(lists[step_no % 2], W.hparams(cfg, step=step_no), stream=stream)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev[0].record(stream)
+    for k in range(args.steps):
+        one_step()
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    per_launch_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
+    total_ms = ev[0].elapsed_time(ev[-1])
+    ms_per_step = total_ms / args.steps
+    avg_launch_ms = sum(per_launch_ms) / len(per_launch_ms)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})"
+        f", launches min {min(per_launch_ms):.3f} max {max(per_launch_ms):.3f} ms")
+
+    alg_bytes = nparam * BYTES_PER_PARAM[wfmt]
+    achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
+    traffic = traffic_from_profile() if cfg == "c5" else None
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "algorithmic_bytes_per_launch": alg_bytes,
+                "kernel": f"madd_step_kernel<{wfmt}, fp32 grad, SR>",
+                "avg_launch_ms": round(avg_launch_ms, 4)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        cpu = cpu_baseline(cfg, args.cpu_sample, args.cpu_steps)
+
+    out = {
+        "metric": METRIC,
+        "value": round(nparam / (ms_per_step / 1e3) / 1e9, 3),
+        "unit": "Gparam/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES[cfg], "params": nparam, "tensors": len(specs),
+                   "weight_format": wfmt, "grad_format": "fp32", "state": "fp32 m, v, v_e",
+                   "rounding": W.CONFIGS[cfg]["rounding"],
+                   "bytes_per_param": BYTES_PER_PARAM[wfmt]},
+        "hbm_gbps": round(alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

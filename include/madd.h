@@ -1,0 +1,179 @@
+/*
+ * madd.h -- C ABI of the M+Adam optimizer-step library for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The library applies one step of M+Adam, the additive-multiplicative
+ * optimizer of arXiv 2607.10611, to weights kept only in a low-precision
+ * storage format (no FP32 master copy):
+ *
+ *   additive branch (Algorithm 1; Section 3.1)
+ *       m  <- b1 m + (1 - b1) g            v <- b2 v + (1 - b2) g^2
+ *       u_a = -eta_a m^ / (sqrt(v^) + eps),  m^ = m/(1-b1^t), v^ = v/(1-b2^t)
+ *   multiplicative branch (Algorithm 1; Section 3.1)
+ *       g_e = ln2 * w * g                  (gradient w.r.t. the exponent)
+ *       ve <- b2 ve + (1 - b2) g_e^2
+ *       ut = -eta_m clamp_{g_max}(g_e / (sqrt(ve^) + eps)),  ve^ = ve/(1-b2^t)
+ *       u_m = clip(ut / max(|w|, tau))     clip: [-(r_max - eps0), r_max] and
+ *                                          |log2(1 + u_m)| <= d_mult_max
+ *                                          (clamps of Algorithm 2, Appendix A)
+ *   combine
+ *       w <- clamp_{w_max}(w + w u_m + u_a), rounded into the storage format
+ *       (the FP32-step / low-precision-storage round trip of Appendix B),
+ *       to nearest-even or stochastically.
+ *
+ * The step is computed in FP32 in one fixed operation order; results are
+ * bit-reproducible across launches, shardings and tensor groupings.
+ *
+ * Conventions common to every entry point
+ *   - Buffer pointers (weights, gradients, moments, scales) are DEVICE
+ *     pointers owned by the caller.  Pointer arrays, numel arrays and the
+ *     hyper-parameter struct are HOST memory, read during the call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued asynchronously on it; no call synchronizes the host
+ *     except madd_multi_tensor_step the first time it sees a given tensor
+ *     list (it uploads a descriptor table; see that function).
+ *   - Updates are in place on w, m, v, ve and scales; g is read-only.
+ *     Buffers must not alias each other.  Concurrent calls that touch the
+ *     same buffers race.
+ *   - Arguments are validated before any device work; on any status other
+ *     than MADD_OK no buffer has been touched.
+ *   - Every status is a madd_status value; madd_status_string() names it.
+ */
+#ifndef MADD_H
+#define MADD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+typedef enum madd_status {
+  MADD_OK = 0,
+  MADD_EINVAL = -1,      /* invalid argument (NULL pointer, size, range, enum) */
+  MADD_EALIGN = -2,      /* block-scaled FP8 buffers not 16-byte aligned      */
+  MADD_EUNSUPPORTED = -3,/* valid request the library does not implement      */
+  MADD_EDEVICE = -4,     /* a HIP runtime call or kernel launch failed         */
+  MADD_ENOMEM = -5       /* device allocation for the descriptor table failed  */
+} madd_status;
+
+/* Weight storage formats.
+ *   BF16     : IEEE-style bfloat16; RNE overflows to Inf; NaN stored as
+ *              0x7FC0.
+ *   FP8_E4M3 : OCP E4M3 (bias 7, max 448, no Inf, NaN = S.1111.111).
+ *   FP8_E5M2 : OCP E5M2 (bias 15, max 57344).
+ *              Both FP8 formats saturate finite overflow and Inf to +-max and
+ *              store NaN as 0x7F.
+ *   FP32     : passthrough (no rounding); for testing the unrounded step.
+ *              NaN stored as 0x7FC00000. */
+typedef enum madd_wfmt {
+  MADD_W_BF16 = 0,
+  MADD_W_FP8_E4M3 = 1,
+  MADD_W_FP8_E5M2 = 2,
+  MADD_W_FP32 = 3
+} madd_wfmt;
+
+/* Gradient formats (decoded exactly to FP32). */
+typedef enum madd_gfmt { MADD_G_FP32 = 0, MADD_G_BF16 = 1 } madd_gfmt;
+
+/* Rounding of the new weight into its storage format.
+ *   RNE : round to nearest, ties to even.
+ *   SR  : stochastic.  For |x| between adjacent grid points lo < |x| < hi,
+ *         rounds up iff floor((|x|-lo)/(hi-lo) * 2^16) + r16 >= 2^16, where
+ *         r16 is the element's 16-bit draw; the sign is restored afterwards.
+ *         For BF16 this gives P(up) = (|x|-lo)/(hi-lo) exactly.
+ *         r16 for global element index i at step t is the 16-bit lane
+ *         (i & 7) -- bits 16*(i&1)..+15 of word (i&7)>>1 -- of
+ *         Philox4x32-10 (Salmon et al., SC'11) with key (seed lo32, seed
+ *         hi32) and counter ((i>>3) lo32, (i>>3) hi32, t, 0).  The paper cites
+ *         stochastic rounding without defining it. */
+typedef enum madd_round { MADD_ROUND_RNE = 0, MADD_ROUND_SR = 1 } madd_round;
+
+/* Hyper-parameters of one step (inputs of Algorithms 1 and 2).
+ * The library evaluates the derived scalars in double and rounds each once
+ * to float: b1, b2, 1-b1, 1-b2, eta_a/(1-b1^t) (or eta_a), 1/(1-b2^t) (or 1),
+ * eta_m, eps, tau, g_max, w_max, and the u_m clip bounds
+ * max(-(r_max-eps0), 2^-d - 1), min(r_max, 2^d - 1) with d = d_mult_max.
+ * Valid ranges (else MADD_EINVAL):
+ *   0 <= beta1 < 1, 0 <= beta2 < 1, eps >= 0, tau > 0, 0 < r_max < 1,
+ *   0 <= eps0 < r_max, g_max > 0, d_mult_max > 0, w_max > 0 (+INFINITY turns
+ *   the clamp off), bias_correction in {0, 1}, rounding a madd_round,
+ *   1 <= step <= 2^32 - 1. */
+typedef struct madd_hparams {
+  double lr_add;          /* eta_a: additive step size                         */
+  double lr_mul;          /* eta_m: multiplicative step size                   */
+  double beta1, beta2;    /* moment decay rates                                */
+  double eps;             /* stabiliser in both denominators                   */
+  double tau;             /* rho = max(|w|, tau)                               */
+  double r_max;           /* u_m clip: [-(r_max - eps0), r_max]; paper: 0.75   */
+  double eps0;            /* asymmetry of the lower clip bound; 0 = symmetric  */
+  double g_max;           /* clamp of the normalised multiplicative direction  */
+  double d_mult_max;      /* cap on |log2(1 + u_m)|                            */
+  double w_max;           /* final weight clamp                                */
+  int32_t bias_correction;/* 1: Algorithm 1 (bias-corrected); 0: Algorithm 2   */
+  int32_t rounding;       /* madd_round                                        */
+  uint64_t seed;          /* stochastic-rounding key                           */
+  int64_t step;           /* t, starting at 1; the caller increments it        */
+} madd_hparams;
+
+/* Zero the optimizer state (Algorithm 1: moments start at 0).
+ * m, v, ve: device float arrays of n elements (n >= 0; may be NULL if n == 0).
+ * Enqueued on `stream`. */
+int32_t madd_init_state(float* m, float* v, float* ve, int64_t n, void* stream);
+
+/* Round n fp32 values x into weight storage w with round-to-nearest-even.
+ * w: device codes of format wfmt (2, 1, 1 or 4 bytes per element).
+ * scales: NULL for unscaled storage; for block-scaled FP8 (wfmt E4M3 or
+ *   E5M2 only) a device array of n/128 FP16 codes, n % 128 == 0: block b is
+ *   elements [128b, 128b+128), its scale is RNE_fp16(max|x| / FMAX) (1.0 when
+ *   the block is all zero, smallest FP16 subnormal on underflow, largest
+ *   finite FP16 on overflow, FP16 NaN when the block holds a non-finite
+ *   value) and its payloads are encode(x / scale). */
+int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* scales, int64_t n,
+                            void* stream);
+
+/* One M+Adam step on one tensor of n elements (Algorithm 1 with the optional
+ * clamps of Algorithm 2).
+ * w       : device weight codes of format wfmt, updated in place.
+ * scales  : NULL, or block-scaled FP8 as in madd_encode_weights: the weight
+ *           is payload * scale (fp32 product); after the update each block's
+ *           scale is recomputed from the new weights by the same rule and the
+ *           payloads re-encoded with hp->rounding.  Requires wfmt FP8,
+ *           n % 128 == 0 and 16-byte-aligned w, g, m, v, ve (else
+ *           MADD_EINVAL / MADD_EALIGN).
+ * g       : device gradient of format gfmt (read only).
+ * m, v, ve: device fp32 moments (first, second, multiplicative second).
+ * index_base: global index of element 0 (keys the stochastic-rounding draw);
+ *           a loop of madd_step calls whose bases are the prefix sums of the
+ *           sizes is bit-identical to one madd_multi_tensor_step call, and to
+ *           any split of the index space (sharding).
+ * Unaligned unscaled buffers are accepted and take a slower path with
+ * identical results. */
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, float* m,
+                  float* v, float* ve, int64_t n, int64_t index_base, const madd_hparams* hp,
+                  void* stream);
+
+/* One M+Adam step on a list of tensors in as few launches as the formats
+ * allow (one per distinct (format, scaled) pair).
+ * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
+ * entries; scales: NULL (no tensor block-scaled) or a host array whose entry
+ * i is NULL or tensor i's scale array.  Tensor i's elements have global
+ * indices index_base + sum_{j<i} numel[j] + local index.
+ * The first call with a given list (same pointers and sizes) uploads a small
+ * device descriptor table with a synchronous copy and caches it; later calls
+ * with the same list enqueue only the kernels. */
+int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                               uint16_t* const* scales, const void* const* g, int32_t gfmt,
+                               float* const* m, float* const* v, float* const* ve,
+                               const int64_t* numel, int64_t index_base, const madd_hparams* hp,
+                               void* stream);
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* madd_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MADD_H */

@@ -1,0 +1,874 @@
+// M+Adam optimizer step for AMD Instinct MI355X (gfx950): HIP kernels and the
+// C ABI declared in include/madd.h.
+//
+// One fused, HBM-bound elementwise pass per step.  Per element it reads the
+// weight code, the gradient and the three fp32 moments, updates the moments,
+// forms the additive update u_a and the multiplicative update u_m
+// (Algorithm 1, with the optional clamps of Algorithm 2), combines
+// w + w u_m + u_a, and rounds the result back into the storage format (the
+// FP32-step / low-precision-storage round trip of Appendix B), to nearest-even
+// or stochastically with a Philox4x32-10 draw keyed by (seed, step, element).
+//
+// Layout of work: a launch covers a list of tensors.  The element space of
+// each tensor is cut into chunks of kChunk elements; one workgroup (256
+// threads, four wave64s) owns one chunk and walks it in tiles of 2048
+// elements, eight consecutive elements per thread, so every thread issues
+// 16-byte loads and stores (bf16 weights: one 16-byte access per 8 weights;
+// fp32 arrays: two).  A workgroup finds its tensor by a binary search over the
+// descriptor table (uniform, scalar loads).  Loads and stores of the streamed
+// arrays are non-temporal: nothing is reused within a step.
+//
+// Arithmetic: FP32, one fixed operation order (step_elem), built with
+// -ffp-contract=off so that only the written fmaf calls fuse; division and
+// square root are the correctly rounded IEEE operations; fp32 denormals are
+// kept.  The result is bit-identical on every launch shape.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include <cmath>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "madd.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kVec = 8;                      // consecutive elements per thread
+constexpr int kTile = kThreads * kVec;       // 2048 elements per workgroup tile
+constexpr int kTilesPerChunk = 4;
+constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
+constexpr int kBlock = 128;                  // block-scaled FP8 block length
+
+// ---------------------------------------------------------------------------
+// Scalars and descriptors
+// ---------------------------------------------------------------------------
+
+struct Scalars {
+  float B1, B2, OMB1, OMB2;  // b1, b2, 1-b1, 1-b2
+  float SA;                  // eta_a / (1 - b1^t)   (eta_a without bias correction)
+  float IBC2;                // 1 / (1 - b2^t)       (1 without bias correction)
+  float LRM, EPS, TAU, GMAX; // eta_m, eps, tau, g_max
+  float ULO, UHI;            // u_m clip bounds
+  float WMAX;                // final weight clamp
+  uint32_t key0, key1;       // Philox key = seed
+  uint32_t t;                // step (Philox counter word 2)
+};
+
+struct TensorDesc {
+  void* w;
+  const void* g;
+  float* m;
+  float* v;
+  float* ve;
+  uint16_t* scales;
+  int64_t n;       // elements
+  int64_t gbase;   // global index of element 0
+  int64_t chunk0;  // first chunk of this tensor within the launch
+  int32_t vec_ok;  // buffers aligned for 16-byte accesses
+  int32_t pad;
+};
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+template <typename T>
+__device__ __forceinline__ T ld_nt(const T* p) {
+  return __builtin_nontemporal_load(p);
+}
+template <typename T>
+__device__ __forceinline__ void st_nt(T* p, T x) {
+  __builtin_nontemporal_store(x, p);
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw; SC'11)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ u4 philox10(u4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = u4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// 128 random bits for the group of eight elements j = idx >> 3.
+__device__ __forceinline__ u4 draw_group(uint64_t j, const Scalars& s) {
+  return philox10(u4{(uint32_t)j, (uint32_t)(j >> 32), s.t, 0u}, s.key0, s.key1);
+}
+
+__device__ __forceinline__ uint32_t lane16(u4 r, uint32_t lane) {
+  const uint32_t word = (lane < 2) ? r.x : (lane < 4) ? r.y : (lane < 6) ? r.z : r.w;
+  return (lane & 1u) ? (word >> 16) : (word & 0xFFFFu);
+}
+
+// 16-bit draw of a single element.
+__device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s) {
+  return lane16(draw_group(idx >> 3, s), (uint32_t)(idx & 7u));
+}
+
+// ---------------------------------------------------------------------------
+// Storage-format codecs (bit level)
+// ---------------------------------------------------------------------------
+
+enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3 };
+enum : int { GF_FP32 = 0, GF_BF16 = 1 };
+
+__device__ __forceinline__ float dec_bf16(uint32_t c) { return __uint_as_float(c << 16); }
+
+__device__ __forceinline__ uint32_t enc_bf16(float x, bool sr, uint32_t r16) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+  // SR: carry into the kept half with probability low16 / 2^16.
+  // RNE: add half an ulp minus one, plus the kept lsb (ties to even).
+  const uint32_t add = sr ? r16 : (0x7FFFu + ((u >> 16) & 1u));
+  return (u + add) >> 16;
+}
+
+// Minifloat description: M mantissa bits, exponent bias, minimum normal
+// exponent, largest finite magnitude and its code, NaN code.
+template <int WF>
+struct Mini;
+template <>
+struct Mini<WF_E4M3> {
+  static constexpr int M = 3, BIAS = 7, EMIN = -6;
+  static constexpr float MAXV = 448.0f;
+  static constexpr uint32_t MAXCODE = 0x7Eu, NANCODE = 0x7Fu;
+};
+template <>
+struct Mini<WF_E5M2> {
+  static constexpr int M = 2, BIAS = 15, EMIN = -14;
+  static constexpr float MAXV = 57344.0f;
+  static constexpr uint32_t MAXCODE = 0x7Bu, NANCODE = 0x7Fu;
+};
+
+template <int WF>
+__device__ __forceinline__ float dec_fp8(uint32_t c) {
+  using F = Mini<WF>;
+  const uint32_t sign = (c & 0x80u) << 24;
+  const uint32_t e = (c >> F::M) & ((0x80u >> F::M) - 1u);
+  const uint32_t mant = c & ((1u << F::M) - 1u);
+  float mag;
+  if (WF == WF_E4M3 && (c & 0x7Fu) == 0x7Fu) {
+    mag = __uint_as_float(0x7FC00000u);
+  } else if (WF == WF_E5M2 && e == 31u) {
+    mag = __uint_as_float(mant ? 0x7FC00000u : 0x7F800000u);
+  } else if (e == 0u) {
+    mag = ldexpf((float)mant, F::EMIN - F::M);
+  } else {
+    mag = __uint_as_float(((e + 127u - F::BIAS) << 23) | (mant << (23 - F::M)));
+  }
+  return __uint_as_float(__float_as_uint(mag) | sign);
+}
+
+// Value-domain rounding onto a minifloat grid: scale |x| so that the grid
+// spacing of its binade is 1, round to an integer k (ties to even, or
+// stochastically), and assemble the code from the spacing exponent and k.
+// A k that reaches the next power of two lands on the next binade's code.
+template <int M, int BIAS, int EMIN>
+__device__ __forceinline__ uint32_t round_mini(float a, bool sr, uint32_t r16) {
+  const int e = (int)((__float_as_uint(a) >> 23) & 0xFFu) - 127;
+  const int se = (e > EMIN ? e : EMIN) - M;  // exponent of the grid spacing
+  const float q = ldexpf(a, -se);            // exact; q < 2^(M+1)
+  float k;
+  if (sr) {
+    k = floorf(q);
+    const uint32_t f16 = (uint32_t)((q - k) * 65536.0f);  // exact
+    if (f16 + r16 >= 65536u) k += 1.0f;
+  } else {
+    k = rintf(q);
+  }
+  return ((uint32_t)(se + M + BIAS - 1) << M) + (uint32_t)k;
+}
+
+template <int WF>
+__device__ __forceinline__ uint32_t enc_fp8(float x, bool sr, uint32_t r16) {
+  using F = Mini<WF>;
+  const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
+  const float a = fabsf(x);
+  if (!(a == a)) return F::NANCODE;
+  if (a >= F::MAXV) return sign | F::MAXCODE;  // saturate (Inf included)
+  uint32_t c = round_mini<F::M, F::BIAS, F::EMIN>(a, sr, r16);
+  c = c > F::MAXCODE ? F::MAXCODE : c;
+  return sign | c;
+}
+
+// FP16 codes of the block scales (IEEE: RNE, overflow to Inf).
+__device__ __forceinline__ float dec_fp16(uint32_t c) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)c);
+}
+
+__device__ __forceinline__ uint32_t enc_fp16_rne(float x) {
+  const uint32_t sign = (__float_as_uint(x) >> 16) & 0x8000u;
+  const float a = fabsf(x);
+  if (!(a == a)) return 0x7E00u;
+  if (a >= 65536.0f) return sign | 0x7C00u;
+  uint32_t c = round_mini<10, 15, -14>(a, false, 0u);
+  c = c > 0x7C00u ? 0x7C00u : c;
+  return sign | c;
+}
+
+template <int WF>
+__device__ __forceinline__ uint32_t encode(float x, bool sr, uint32_t r16) {
+  if constexpr (WF == WF_BF16) return enc_bf16(x, sr, r16);
+  else if constexpr (WF == WF_FP32) return (x == x) ? __float_as_uint(x) : 0x7FC00000u;
+  else return enc_fp8<WF>(x, sr, r16);
+}
+
+template <int WF>
+__device__ __forceinline__ float decode(uint32_t c) {
+  if constexpr (WF == WF_BF16) return dec_bf16(c);
+  else if constexpr (WF == WF_FP32) return __uint_as_float(c);
+  else return dec_fp8<WF>(c);
+}
+
+// Block-scale rule: scale = RNE_fp16(amax / FMAX), with 1.0 for an all-zero
+// block, the smallest subnormal on underflow, the largest finite value on
+// overflow and NaN for a block holding a non-finite value.  `amax_bits` is the
+// largest |w'| as raw bits (unsigned order = magnitude order, NaN above Inf).
+template <int WF>
+__device__ __forceinline__ uint32_t block_scale(uint32_t amax_bits) {
+  if (amax_bits >= 0x7F800000u) return 0x7E00u;
+  if (amax_bits == 0u) return 0x3C00u;
+  uint32_t s = enc_fp16_rne(__uint_as_float(amax_bits) / Mini<WF>::MAXV);
+  if (s == 0u) s = 1u;
+  if (s == 0x7C00u) s = 0x7BFFu;
+  return s;
+}
+
+// ---------------------------------------------------------------------------
+// The per-element step (fixed FP32 operation order)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float clampf(float x, float lo, float hi) {
+  return x < lo ? lo : (x > hi ? hi : x);  // NaN passes through
+}
+
+__device__ __forceinline__ float step_elem(float w, float g, float& m, float& v, float& ve,
+                                           const Scalars& s) {
+  const float LN2 = 0.693147182464599609375f;  // fp32(ln 2)
+  // additive branch
+  m = fmaf(s.B1, m, s.OMB1 * g);
+  v = fmaf(s.B2, v, s.OMB2 * (g * g));
+  const float ua = -((s.SA * m) / (sqrtf(v * s.IBC2) + s.EPS));
+  // multiplicative branch: exponent gradient and its second moment
+  const float ge = (LN2 * w) * g;
+  ve = fmaf(s.B2, ve, s.OMB2 * (ge * ge));
+  const float r = clampf(ge / (sqrtf(ve * s.IBC2) + s.EPS), -s.GMAX, s.GMAX);
+  const float ut = -(s.LRM * r);
+  // relative conversion and clip
+  const float aw = fabsf(w);
+  const float rho = aw > s.TAU ? aw : s.TAU;
+  const float um = clampf(ut / rho, s.ULO, s.UHI);
+  // combine, optional final clamp
+  const float wn = fmaf(w, um, w) + ua;
+  return clampf(wn, -s.WMAX, s.WMAX);
+}
+
+// ---------------------------------------------------------------------------
+// Vector loads / stores of eight consecutive elements
+// ---------------------------------------------------------------------------
+
+template <int WF>
+struct WVec;
+template <>
+struct WVec<WF_BF16> {
+  u4 raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ld_nt((const u4*)((const uint16_t*)p + e)); }
+  __device__ __forceinline__ uint32_t code(int k) const { return (raw[k >> 1] >> (16 * (k & 1))) & 0xFFFFu; }
+  __device__ __forceinline__ void set(int k, uint32_t c) {
+    raw[k >> 1] = (k & 1) ? ((raw[k >> 1] & 0xFFFFu) | (c << 16)) : ((raw[k >> 1] & 0xFFFF0000u) | c);
+  }
+  __device__ __forceinline__ void store(void* p, int64_t e) { st_nt((u4*)((uint16_t*)p + e), raw); }
+};
+template <int WF>
+struct WVec8 {
+  u2 raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ld_nt((const u2*)((const uint8_t*)p + e)); }
+  __device__ __forceinline__ uint32_t code(int k) const { return (raw[k >> 2] >> (8 * (k & 3))) & 0xFFu; }
+  __device__ __forceinline__ void set(int k, uint32_t c) {
+    const int sh = 8 * (k & 3);
+    raw[k >> 2] = (raw[k >> 2] & ~(0xFFu << sh)) | (c << sh);
+  }
+  __device__ __forceinline__ void store(void* p, int64_t e) { st_nt((u2*)((uint8_t*)p + e), raw); }
+};
+template <>
+struct WVec<WF_E4M3> : WVec8<WF_E4M3> {};
+template <>
+struct WVec<WF_E5M2> : WVec8<WF_E5M2> {};
+template <>
+struct WVec<WF_FP32> {
+  u4 a, b;
+  __device__ __forceinline__ void load(const void* p, int64_t e) {
+    a = ld_nt((const u4*)((const uint32_t*)p + e));
+    b = ld_nt((const u4*)((const uint32_t*)p + e + 4));
+  }
+  __device__ __forceinline__ uint32_t code(int k) const { return k < 4 ? a[k] : b[k - 4]; }
+  __device__ __forceinline__ void set(int k, uint32_t c) {
+    if (k < 4) a[k] = c;
+    else b[k - 4] = c;
+  }
+  __device__ __forceinline__ void store(void* p, int64_t e) {
+    st_nt((u4*)((uint32_t*)p + e), a);
+    st_nt((u4*)((uint32_t*)p + e + 4), b);
+  }
+};
+
+__device__ __forceinline__ void ld8f(const float* p, int64_t e, float (&x)[8]) {
+  const f4 a = ld_nt((const f4*)(p + e));
+  const f4 b = ld_nt((const f4*)(p + e + 4));
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void st8f(float* p, int64_t e, const float (&x)[8]) {
+  st_nt((f4*)(p + e), f4{x[0], x[1], x[2], x[3]});
+  st_nt((f4*)(p + e + 4), f4{x[4], x[5], x[6], x[7]});
+}
+
+template <int GF>
+__device__ __forceinline__ void ld8g(const void* p, int64_t e, float (&x)[8]) {
+  if constexpr (GF == GF_FP32) {
+    ld8f((const float*)p, e, x);
+  } else {
+    const u4 r = ld_nt((const u4*)((const uint16_t*)p + e));
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = dec_bf16((r[k >> 1] >> (16 * (k & 1))) & 0xFFFFu);
+  }
+}
+
+template <int GF>
+__device__ __forceinline__ float ld1g(const void* p, int64_t e) {
+  if constexpr (GF == GF_FP32) return ((const float*)p)[e];
+  else return dec_bf16(((const uint16_t*)p)[e]);
+}
+
+template <int WF>
+__device__ __forceinline__ uint32_t ld1w(const void* p, int64_t e) {
+  if constexpr (WF == WF_BF16) return ((const uint16_t*)p)[e];
+  else if constexpr (WF == WF_FP32) return ((const uint32_t*)p)[e];
+  else return ((const uint8_t*)p)[e];
+}
+template <int WF>
+__device__ __forceinline__ void st1w(void* p, int64_t e, uint32_t c) {
+  if constexpr (WF == WF_BF16) ((uint16_t*)p)[e] = (uint16_t)c;
+  else if constexpr (WF == WF_FP32) ((uint32_t*)p)[e] = c;
+  else ((uint8_t*)p)[e] = (uint8_t)c;
+}
+
+// The eight 16-bit draws of elements gidx0 .. gidx0+7.
+template <bool SR>
+__device__ __forceinline__ void draws8(uint64_t gidx0, const Scalars& s, uint32_t (&r)[8]) {
+  if constexpr (!SR) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) r[k] = 0u;
+  } else {
+    const uint32_t off = (uint32_t)(gidx0 & 7u);
+    const u4 a = draw_group(gidx0 >> 3, s);
+    if (off == 0u) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) r[k] = lane16(a, (uint32_t)k);
+    } else {
+      const u4 b = draw_group((gidx0 >> 3) + 1u, s);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const uint32_t l = off + (uint32_t)k;
+        r[k] = l < 8u ? lane16(a, l) : lane16(b, l - 8u);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Step kernel
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ TensorDesc find_tensor(const TensorDesc* __restrict__ table, int ntab,
+                                                  const TensorDesc& single, int64_t chunk) {
+  if (ntab == 0) return single;
+  int lo = 0, hi = ntab - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (table[mid].chunk0 <= chunk) lo = mid;
+    else hi = mid - 1;
+  }
+  return table[lo];
+}
+
+template <int WF, int GF, bool SR>
+__device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b, int64_t e,
+                                                  const Scalars& s) {
+  for (int64_t i = b; i < e; ++i) {
+    float m = d.m[i], v = d.v[i], ve = d.ve[i];
+    const float w = decode<WF>(ld1w<WF>(d.w, i));
+    const float g = ld1g<GF>(d.g, i);
+    const float wn = step_elem(w, g, m, v, ve, s);
+    const uint32_t r16 = SR ? draw_one((uint64_t)(d.gbase + i), s) : 0u;
+    st1w<WF>(d.w, i, encode<WF>(wn, SR, r16));
+    d.m[i] = m;
+    d.v[i] = v;
+    d.ve[i] = ve;
+  }
+}
+
+template <int WF, int GF, bool SR>
+__global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* __restrict__ table,
+                                                             int ntab, TensorDesc single,
+                                                             Scalars s) {
+  const int64_t chunk = blockIdx.x;
+  const TensorDesc d = find_tensor(table, ntab, single, chunk);
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+#pragma unroll 1
+  for (int tile = 0; tile < kTilesPerChunk; ++tile) {
+    const int64_t e0 = c0 + (int64_t)tile * kTile + (int64_t)threadIdx.x * kVec;
+    if (e0 >= cend) break;
+    if (d.vec_ok && e0 + kVec <= cend) {
+      WVec<WF> wv;
+      wv.load(d.w, e0);
+      float g[8], m[8], v[8], ve[8];
+      ld8g<GF>(d.g, e0, g);
+      ld8f(d.m, e0, m);
+      ld8f(d.v, e0, v);
+      ld8f(d.ve, e0, ve);
+      uint32_t r[8];
+      draws8<SR>((uint64_t)(d.gbase + e0), s, r);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float wn = step_elem(decode<WF>(wv.code(k)), g[k], m[k], v[k], ve[k], s);
+        wv.set(k, encode<WF>(wn, SR, r[k]));
+      }
+      wv.store(d.w, e0);
+      st8f(d.m, e0, m);
+      st8f(d.v, e0, v);
+      st8f(d.ve, e0, ve);
+    } else {
+      const int64_t e1 = (e0 + kVec < cend) ? e0 + kVec : cend;
+      step_scalar_range<WF, GF, SR>(d, e0, e1, s);
+    }
+  }
+}
+
+// Block-scaled FP8: sixteen consecutive threads hold one 128-element block;
+// the block's max |w'| is combined across them with lane shuffles.  Every
+// thread of the workgroup runs the shuffles (inactive ones with zeros), and
+// the launch requires n % 128 == 0, so a block is never split.
+template <int WF, int GF, bool SR>
+__global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
+    const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
+  const int64_t chunk = blockIdx.x;
+  const TensorDesc d = find_tensor(table, ntab, single, chunk);
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+#pragma unroll 1
+  for (int tile = 0; tile < kTilesPerChunk; ++tile) {
+    const int64_t tbase = c0 + (int64_t)tile * kTile;
+    if (tbase >= cend) break;  // uniform across the workgroup
+    const int64_t e0 = tbase + (int64_t)threadIdx.x * kVec;
+    const bool active = e0 < cend;  // whole 16-thread groups agree
+    WVec<WF> wv;
+    float g[8], m[8], v[8], ve[8], wn[8];
+    uint32_t amax = 0u;
+    uint32_t r[8];
+    if (active) {
+      wv.load(d.w, e0);
+      ld8g<GF>(d.g, e0, g);
+      ld8f(d.m, e0, m);
+      ld8f(d.v, e0, v);
+      ld8f(d.ve, e0, ve);
+      const float sold = dec_fp16(d.scales[e0 / kBlock]);
+      draws8<SR>((uint64_t)(d.gbase + e0), s, r);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        wn[k] = step_elem(decode<WF>(wv.code(k)) * sold, g[k], m[k], v[k], ve[k], s);
+        const uint32_t ab = __float_as_uint(wn[k]) & 0x7FFFFFFFu;
+        amax = ab > amax ? ab : amax;
+      }
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) {
+      const uint32_t o = (uint32_t)__shfl_xor((int)amax, off, 16);
+      amax = o > amax ? o : amax;
+    }
+    if (active) {
+      const uint32_t sc = block_scale<WF>(amax);
+      const float sf = dec_fp16(sc);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) wv.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
+      wv.store(d.w, e0);
+      st8f(d.m, e0, m);
+      st8f(d.v, e0, v);
+      st8f(d.ve, e0, ve);
+      if ((threadIdx.x & 15u) == 0u) d.scales[e0 / kBlock] = (uint16_t)sc;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Auxiliary kernels: zero state, encode weights
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kThreads) void zero_kernel(float* __restrict__ p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
+}
+
+template <int WF>
+__global__ __launch_bounds__(kThreads) void encode_kernel(const float* __restrict__ x, void* w,
+                                                          int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride)
+    st1w<WF>(w, i, encode<WF>(x[i], false, 0u));
+}
+
+// One thread per 128-element block.
+template <int WF>
+__global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __restrict__ x,
+                                                                uint8_t* q, uint16_t* scales,
+                                                                int64_t nblocks) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < nblocks; b += stride) {
+    const float* xb = x + b * kBlock;
+    uint32_t amax = 0u;
+    for (int k = 0; k < kBlock; ++k) {
+      const uint32_t ab = __float_as_uint(xb[k]) & 0x7FFFFFFFu;
+      amax = ab > amax ? ab : amax;
+    }
+    const uint32_t sc = block_scale<WF>(amax);
+    const float sf = dec_fp16(sc);
+    for (int k = 0; k < kBlock; ++k) q[b * kBlock + k] = (uint8_t)enc_fp8<WF>(xb[k] / sf, false, 0u);
+    scales[b] = (uint16_t)sc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+
+typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
+
+template <int WF, int GF>
+step_fn pick_plain(bool sr) {
+  return sr ? madd_step_kernel<WF, GF, true> : madd_step_kernel<WF, GF, false>;
+}
+template <int WF, int GF>
+step_fn pick_block(bool sr) {
+  return sr ? madd_step_block_kernel<WF, GF, true> : madd_step_block_kernel<WF, GF, false>;
+}
+
+step_fn pick_kernel(int wf, int gf, bool sr, bool blk) {
+  if (blk) {
+    if (wf == WF_E4M3) return gf == GF_FP32 ? pick_block<WF_E4M3, GF_FP32>(sr) : pick_block<WF_E4M3, GF_BF16>(sr);
+    if (wf == WF_E5M2) return gf == GF_FP32 ? pick_block<WF_E5M2, GF_FP32>(sr) : pick_block<WF_E5M2, GF_BF16>(sr);
+    return nullptr;
+  }
+  switch (wf) {
+    case WF_BF16: return gf == GF_FP32 ? pick_plain<WF_BF16, GF_FP32>(sr) : pick_plain<WF_BF16, GF_BF16>(sr);
+    case WF_E4M3: return gf == GF_FP32 ? pick_plain<WF_E4M3, GF_FP32>(sr) : pick_plain<WF_E4M3, GF_BF16>(sr);
+    case WF_E5M2: return gf == GF_FP32 ? pick_plain<WF_E5M2, GF_FP32>(sr) : pick_plain<WF_E5M2, GF_BF16>(sr);
+    case WF_FP32: return gf == GF_FP32 ? pick_plain<WF_FP32, GF_FP32>(sr) : pick_plain<WF_FP32, GF_BF16>(sr);
+    default: return nullptr;
+  }
+}
+
+bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_FP32; }
+bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
+int wbytes(int32_t f) { return f == MADD_W_BF16 ? 2 : (f == MADD_W_FP32 ? 4 : 1); }
+int gbytes(int32_t f) { return f == MADD_G_FP32 ? 4 : 2; }
+bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int32_t check_hparams(const madd_hparams* hp) {
+  if (!hp) return MADD_EINVAL;
+  if (!(hp->beta1 >= 0.0 && hp->beta1 < 1.0)) return MADD_EINVAL;
+  if (!(hp->beta2 >= 0.0 && hp->beta2 < 1.0)) return MADD_EINVAL;
+  if (!(hp->eps >= 0.0)) return MADD_EINVAL;
+  if (!(hp->tau > 0.0)) return MADD_EINVAL;
+  if (!(hp->r_max > 0.0 && hp->r_max < 1.0)) return MADD_EINVAL;
+  if (!(hp->eps0 >= 0.0 && hp->eps0 < hp->r_max)) return MADD_EINVAL;
+  if (!(hp->g_max > 0.0) || !(hp->d_mult_max > 0.0) || !(hp->w_max > 0.0)) return MADD_EINVAL;
+  if (hp->bias_correction != 0 && hp->bias_correction != 1) return MADD_EINVAL;
+  if (hp->rounding != MADD_ROUND_RNE && hp->rounding != MADD_ROUND_SR) return MADD_EINVAL;
+  if (hp->step < 1 || hp->step > (int64_t)0xFFFFFFFFll) return MADD_EINVAL;
+  if (std::isnan(hp->lr_add) || std::isnan(hp->lr_mul)) return MADD_EINVAL;
+  return MADD_OK;
+}
+
+Scalars make_scalars(const madd_hparams& hp) {
+  Scalars s;
+  const double t = (double)hp.step;
+  s.B1 = (float)hp.beta1;
+  s.B2 = (float)hp.beta2;
+  s.OMB1 = (float)(1.0 - hp.beta1);
+  s.OMB2 = (float)(1.0 - hp.beta2);
+  if (hp.bias_correction) {
+    s.SA = (float)(hp.lr_add / (1.0 - pow(hp.beta1, t)));
+    s.IBC2 = (float)(1.0 / (1.0 - pow(hp.beta2, t)));
+  } else {
+    s.SA = (float)hp.lr_add;
+    s.IBC2 = 1.0f;
+  }
+  s.LRM = (float)hp.lr_mul;
+  s.EPS = (float)hp.eps;
+  s.TAU = (float)hp.tau;
+  s.GMAX = (float)hp.g_max;
+  double lo = -(hp.r_max - hp.eps0), hi = hp.r_max;
+  if (std::isfinite(hp.d_mult_max)) {
+    lo = std::fmax(lo, exp2(-hp.d_mult_max) - 1.0);
+    hi = std::fmin(hi, exp2(hp.d_mult_max) - 1.0);
+  }
+  s.ULO = (float)lo;
+  s.UHI = (float)hi;
+  s.WMAX = (float)hp.w_max;
+  s.key0 = (uint32_t)hp.seed;
+  s.key1 = (uint32_t)(hp.seed >> 32);
+  s.t = (uint32_t)hp.step;
+  return s;
+}
+
+int64_t chunks_of(int64_t n) { return (n + kChunk - 1) / kChunk; }
+
+// Device descriptor tables, cached by content.
+struct TableEntry {
+  int device;
+  std::vector<TensorDesc> host;
+  TensorDesc* dev;
+  uint64_t last_use;
+};
+std::mutex g_mu;
+std::vector<TableEntry> g_tables;
+uint64_t g_clock = 0;
+constexpr size_t kMaxTables = 32;
+
+int32_t get_table(const std::vector<TensorDesc>& descs, TensorDesc** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MADD_EDEVICE;
+  std::lock_guard<std::mutex> lock(g_mu);
+  ++g_clock;
+  const size_t bytes = descs.size() * sizeof(TensorDesc);
+  for (auto& t : g_tables) {
+    if (t.device == dev && t.host.size() == descs.size() &&
+        memcmp(t.host.data(), descs.data(), bytes) == 0) {
+      t.last_use = g_clock;
+      *out = t.dev;
+      return MADD_OK;
+    }
+  }
+  if (g_tables.size() >= kMaxTables) {
+    size_t victim = 0;
+    for (size_t i = 1; i < g_tables.size(); ++i)
+      if (g_tables[i].last_use < g_tables[victim].last_use) victim = i;
+    int cur = dev;
+    if (hipSetDevice(g_tables[victim].device) != hipSuccess) return MADD_EDEVICE;
+    // A launch still in flight may read the table: drain the device first.
+    if (hipDeviceSynchronize() != hipSuccess) return MADD_EDEVICE;
+    (void)hipFree(g_tables[victim].dev);
+    if (hipSetDevice(cur) != hipSuccess) return MADD_EDEVICE;
+    g_tables.erase(g_tables.begin() + (long)victim);
+  }
+  TensorDesc* d = nullptr;
+  if (hipMalloc((void**)&d, bytes) != hipSuccess) return MADD_ENOMEM;
+  if (hipMemcpy(d, descs.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(d);
+    return MADD_EDEVICE;
+  }
+  g_tables.push_back(TableEntry{dev, descs, d, g_clock});
+  *out = d;
+  return MADD_OK;
+}
+
+int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& single,
+               int64_t nchunks, const Scalars& s, hipStream_t stream) {
+  if (nchunks <= 0) return MADD_OK;
+  if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+  hipLaunchKernelGGL(fn, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab, single, s);
+  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+}
+
+TensorDesc make_desc(void* w, uint16_t* scales, const void* g, float* m, float* v, float* ve,
+                     int64_t n, int64_t gbase) {
+  TensorDesc d;
+  memset(&d, 0, sizeof(d));
+  d.w = w;
+  d.g = g;
+  d.m = m;
+  d.v = v;
+  d.ve = ve;
+  d.scales = scales;
+  d.n = n;
+  d.gbase = gbase;
+  d.chunk0 = 0;
+  d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve);
+  return d;
+}
+
+int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, const void* g, float* m, float* v,
+                     float* ve, int64_t n) {
+  if (n < 0) return MADD_EINVAL;
+  if (n == 0) return MADD_OK;
+  if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
+  if (!valid_wfmt(wfmt)) return MADD_EINVAL;
+  if (scales) {
+    if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
+    if (n % kBlock != 0) return MADD_EINVAL;
+    if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve))) return MADD_EALIGN;
+  }
+  return MADD_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char* madd_status_string(int32_t status) {
+  switch (status) {
+    case MADD_OK: return "MADD_OK";
+    case MADD_EINVAL: return "MADD_EINVAL: invalid argument";
+    case MADD_EALIGN: return "MADD_EALIGN: block-scaled buffers must be 16-byte aligned";
+    case MADD_EUNSUPPORTED: return "MADD_EUNSUPPORTED: request not implemented";
+    case MADD_EDEVICE: return "MADD_EDEVICE: HIP runtime or launch failure";
+    case MADD_ENOMEM: return "MADD_ENOMEM: device allocation failed";
+    default: return "unknown madd status";
+  }
+}
+
+int32_t madd_init_state(float* m, float* v, float* ve, int64_t n, void* stream) {
+  if (n < 0) return MADD_EINVAL;
+  if (n == 0) return MADD_OK;
+  if (!m || !v || !ve) return MADD_EINVAL;
+  const int64_t want = (n + kThreads - 1) / kThreads;
+  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  hipStream_t st = (hipStream_t)stream;
+  float* arr[3] = {m, v, ve};
+  for (float* p : arr) {
+    hipLaunchKernelGGL(zero_kernel, dim3(grid), dim3(kThreads), 0, st, p, n);
+    if (hipGetLastError() != hipSuccess) return MADD_EDEVICE;
+  }
+  return MADD_OK;
+}
+
+int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* scales, int64_t n,
+                            void* stream) {
+  if (n < 0 || !valid_wfmt(wfmt)) return MADD_EINVAL;
+  if (n == 0) return MADD_OK;
+  if (!x || !w) return MADD_EINVAL;
+  hipStream_t st = (hipStream_t)stream;
+  if (scales) {
+    if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
+    if (n % kBlock != 0) return MADD_EINVAL;
+    const int64_t nb = n / kBlock;
+    const int64_t want = (nb + kThreads - 1) / kThreads;
+    const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+    if (wfmt == MADD_W_FP8_E4M3)
+      hipLaunchKernelGGL(encode_block_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), 0, st, x,
+                         (uint8_t*)w, scales, nb);
+    else
+      hipLaunchKernelGGL(encode_block_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), 0, st, x,
+                         (uint8_t*)w, scales, nb);
+    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  }
+  const int64_t want = (n + kThreads - 1) / kThreads;
+  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  switch (wfmt) {
+    case MADD_W_BF16: hipLaunchKernelGGL(encode_kernel<WF_BF16>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
+    case MADD_W_FP8_E4M3: hipLaunchKernelGGL(encode_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
+    case MADD_W_FP8_E5M2: hipLaunchKernelGGL(encode_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
+    default: hipLaunchKernelGGL(encode_kernel<WF_FP32>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
+  }
+  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+}
+
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, float* m,
+                  float* v, float* ve, int64_t n, int64_t index_base, const madd_hparams* hp,
+                  void* stream) {
+  int32_t rc = check_hparams(hp);
+  if (rc != MADD_OK) return rc;
+  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0) return MADD_EINVAL;
+  rc = check_tensor(w, wfmt, scales, g, m, v, ve, n);
+  if (rc != MADD_OK) return rc;
+  if (n == 0) return MADD_OK;
+  if (n > INT64_MAX - index_base) return MADD_EINVAL;
+  const Scalars s = make_scalars(*hp);
+  step_fn fn = pick_kernel(wfmt, gfmt, hp->rounding == MADD_ROUND_SR, scales != nullptr);
+  if (!fn) return MADD_EUNSUPPORTED;
+  const TensorDesc d = make_desc(w, scales, g, m, v, ve, n, index_base);
+  return launch(fn, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
+}
+
+int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                               uint16_t* const* scales, const void* const* g, int32_t gfmt,
+                               float* const* m, float* const* v, float* const* ve,
+                               const int64_t* numel, int64_t index_base, const madd_hparams* hp,
+                               void* stream) {
+  int32_t rc = check_hparams(hp);
+  if (rc != MADD_OK) return rc;
+  if (ntensors < 0 || !valid_gfmt(gfmt) || index_base < 0) return MADD_EINVAL;
+  if (ntensors == 0) return MADD_OK;
+  if (!w || !wfmt || !g || !m || !v || !ve || !numel) return MADD_EINVAL;
+  int64_t total = 0;
+  for (int32_t i = 0; i < ntensors; ++i) {
+    if (!valid_wfmt(wfmt[i])) return MADD_EINVAL;
+    rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, g[i], m[i], v[i], ve[i],
+                      numel[i]);
+    if (rc != MADD_OK) return rc;
+    if (numel[i] > INT64_MAX - index_base - total) return MADD_EINVAL;
+    total += numel[i];
+  }
+  const Scalars s = make_scalars(*hp);
+  const bool sr = hp->rounding == MADD_ROUND_SR;
+  // One launch per (format, scaled) group; global indices follow list order.
+  // All tables are prepared before the first launch.
+  struct Group {
+    step_fn fn;
+    TensorDesc* table;
+    int ntab;
+    int64_t nchunks;
+  };
+  std::vector<Group> groups;
+  for (int wf = MADD_W_BF16; wf <= MADD_W_FP32; ++wf) {
+    for (int blk = 0; blk <= 1; ++blk) {
+      std::vector<TensorDesc> descs;
+      int64_t gbase = index_base, nch = 0;
+      for (int32_t i = 0; i < ntensors; ++i) {
+        const bool is_blk = scales && scales[i];
+        if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
+          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, g[i], m[i], v[i], ve[i],
+                                   numel[i], gbase);
+          d.chunk0 = nch;
+          nch += chunks_of(numel[i]);
+          descs.push_back(d);
+        }
+        gbase += numel[i];
+      }
+      if (descs.empty()) continue;
+      if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+      step_fn fn = pick_kernel(wf, gfmt, sr, blk != 0);
+      if (!fn) return MADD_EUNSUPPORTED;
+      TensorDesc* table = nullptr;
+      rc = get_table(descs, &table);
+      if (rc != MADD_OK) return rc;
+      groups.push_back(Group{fn, table, (int)descs.size(), nch});
+    }
+  }
+  TensorDesc none;
+  memset(&none, 0, sizeof(none));
+  for (const Group& gr : groups) {
+    rc = launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, (hipStream_t)stream);
+    if (rc != MADD_OK) return rc;
+  }
+  return MADD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+"""Helpers shared by the GPU parity tests: moving codes and states between
+numpy (oracle side) and torch device tensors (HIP side), and comparisons."""
+import numpy as np
+import torch
+
+import oracle
+from paper_2607_10611_amd import binding as B
+
+CODE_NP = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32}
+CODE_T = {"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8, "fp32": torch.int32}
+SIGNED_NP = {np.uint16: np.int16, np.uint32: np.int32, np.uint8: np.uint8}
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype in (np.uint16, np.uint32):
+        a = a.view(SIGNED_NP[a.dtype.type])
+    return torch.from_numpy(a.copy()).cuda()
+
+
+def to_host(t: torch.Tensor, np_dtype=None) -> np.ndarray:
+    a = t.detach().cpu().numpy()
+    if np_dtype is not None:
+        a = a.view(np_dtype)
+    return a
+
+
+def ulp_dist(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Distance in units in the last place between fp32 arrays (NaN pairs: 0)."""
+    ia = a.astype(np.float32).view(np.int32).astype(np.int64)
+    ib = b.astype(np.float32).view(np.int32).astype(np.int64)
+    ia = np.where(ia < 0, -(ia & 0x7FFFFFFF), ia)
+    ib = np.where(ib < 0, -(ib & 0x7FFFFFFF), ib)
+    d = np.abs(ia - ib)
+    both_nan = np.isnan(a) & np.isnan(b)
+    return np.where(both_nan, 0, d)
+
+
+def assert_state_equal(tag, w_gpu, w_ref, m_gpu, m_ref, v_gpu, v_ref, ve_gpu, ve_ref,
+                       max_ulp=2):
+    """Weight codes bit-exact; fp32 moments within max_ulp (NaN where NaN)."""
+    bad = np.nonzero(w_gpu != w_ref)[0]
+    assert bad.size == 0, (f"{tag}: {bad.size} weight codes differ, first at {bad[:5]}: "
+                           f"gpu {w_gpu[bad[:5]]} oracle {w_ref[bad[:5]]}")
+    for name, a, b in (("m", m_gpu, m_ref), ("v", v_gpu, v_ref), ("ve", ve_gpu, ve_ref)):
+        assert (np.isnan(a) == np.isnan(b)).all(), f"{tag}: {name} NaN pattern differs"
+        d = ulp_dist(a, b)
+        assert d.max() <= max_ulp, f"{tag}: {name} max ulp {d.max()} at {np.argmax(d)}"
+
+
+class DevState:
+    """Device copies of one tensor's weight codes and moments."""
+
+    def __init__(self, wfmt, codes, n, scales=None):
+        self.wfmt = wfmt
+        self.w = to_dev(codes)
+        self.m = torch.zeros(n, dtype=torch.float32, device="cuda")
+        self.v = torch.zeros(n, dtype=torch.float32, device="cuda")
+        self.ve = torch.zeros(n, dtype=torch.float32, device="cuda")
+        self.scales = to_dev(scales) if scales is not None else None
+
+    def host(self):
+        return (to_host(self.w, CODE_NP[self.wfmt]), to_host(self.m), to_host(self.v),
+                to_host(self.ve))
+
+
+class HostState:
+    """Oracle copies of one tensor's weight codes and moments."""
+
+    def __init__(self, codes, n, scales=None):
+        self.w = codes.copy()
+        self.m = np.zeros(n, np.float32)
+        self.v = np.zeros(n, np.float32)
+        self.ve = np.zeros(n, np.float32)
+        self.scales = scales.copy() if scales is not None else None
+
+
+def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
+    if hs.scales is not None:
+        oracle.step_block(wfmt, hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
+                          index_base=index_base, gidx=gidx)
+    else:
+        oracle.step(wfmt, hs.w, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt, index_base=index_base,
+                    gidx=gidx)
+
+
+def gpu_step(ds: DevState, g_dev, hp, gfmt="fp32", index_base=0):
+    B.madd_step(ds.w, ds.wfmt, g_dev, ds.m, ds.v, ds.ve, hp, gfmt=gfmt, scales=ds.scales,
+                index_base=index_base)

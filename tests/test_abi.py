@@ -1,0 +1,117 @@
+"""The C-ABI library loads, exports every entry point of include/madd.h, and
+rejects invalid arguments before any device work (CPU: no kernel runs)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2607_10611_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "madd.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(madd_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    nm = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
+    for name in declared_functions():
+        assert re.search(rf"\bT {name}\b", nm), name
+
+
+def test_status_strings():
+    lib = B.lib()
+    for code, name in B.STATUS.items():
+        assert lib.madd_status_string(code).decode().startswith(name)
+    assert lib.madd_status_string(12345) == b"unknown madd status"
+
+
+def _hp(**kw):
+    h = B.HParams(**kw).to_c()
+    return ctypes.byref(h), h
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+@pytest.mark.parametrize("kw", [dict(beta1=1.0), dict(beta2=-0.5), dict(eps=-1.0), dict(tau=0.0),
+                                dict(r_max=0.0), dict(r_max=1.0), dict(eps0=0.75),
+                                dict(g_max=0.0), dict(d_mult_max=-1.0), dict(w_max=0.0),
+                                dict(step=0), dict(step=2 ** 32), dict(bias_correction=2),
+                                dict(rounding=7), dict(lr_add=math.nan)])
+def test_step_rejects_bad_hparams(kw):
+    lib = B.lib()
+    ref, _h = _hp(**kw)
+    rc = lib.madd_step(FAKE, B.W_BF16, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 1024, 0, ref, None)
+    assert rc == -1
+
+
+def test_step_rejects_bad_arguments():
+    lib = B.lib()
+    ref, _h = _hp()
+    call = lambda *a: lib.madd_step(*a, ref, None)  # noqa: E731
+    assert lib.madd_step(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0, None, None) == -1
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, -1, 0) == -1          # n < 0
+    assert call(None, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0) == -1           # null w
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 8, 0) == -1           # null v
+    assert call(FAKE, 9, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0) == -1           # bad wfmt
+    assert call(FAKE, 0, None, FAKE, 5, FAKE, FAKE, FAKE, 8, 0) == -1           # bad gfmt
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, -3) == -1          # base < 0
+    assert call(FAKE, 0, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 128, 0) == -1         # scales + bf16
+    assert call(FAKE, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 100, 0) == -1         # n % 128
+    assert call(FAKE + 4, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 128, 0) == -2     # unaligned
+    assert call(None, 0, None, None, 0, None, None, None, 0, 0) == 0            # empty: no-op
+
+
+def test_multi_tensor_rejects_bad_arguments():
+    lib = B.lib()
+    ref, _h = _hp()
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
+    fm = (ctypes.c_int32 * 2)(0, 0)
+    ne = (ctypes.c_int64 * 2)(128, 256)
+    ok_ptrs = [arr(FAKE, FAKE) for _ in range(5)]
+    w, g, m, v, ve = ok_ptrs
+    assert lib.madd_multi_tensor_step(0, None, None, None, None, 0, None, None, None, None, 0, ref,
+                                      None) == 0
+    assert lib.madd_multi_tensor_step(-1, w, fm, None, g, 0, m, v, ve, ne, 0, ref, None) == -1
+    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, v, ve, ne, 0, None, None) == -1
+    bad = arr(FAKE, None)
+    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, bad, ve, ne, 0, ref, None) == -1
+    fm_bad = (ctypes.c_int32 * 2)(0, 11)
+    assert lib.madd_multi_tensor_step(2, w, fm_bad, None, g, 0, m, v, ve, ne, 0, ref, None) == -1
+    ne_bad = (ctypes.c_int64 * 2)(128, -5)
+    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, v, ve, ne_bad, 0, ref, None) == -1
+    sc = arr(None, FAKE)  # second tensor block-scaled but bf16
+    assert lib.madd_multi_tensor_step(2, w, fm, sc, g, 0, m, v, ve, ne, 0, ref, None) == -1
+
+
+def test_init_and_encode_reject_bad_arguments():
+    lib = B.lib()
+    assert lib.madd_init_state(FAKE, FAKE, FAKE, -1, None) == -1
+    assert lib.madd_init_state(None, FAKE, FAKE, 5, None) == -1
+    assert lib.madd_init_state(None, None, None, 0, None) == 0
+    assert lib.madd_encode_weights(FAKE, FAKE, 7, None, 8, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, 0, FAKE, 128, None) == -1   # scales + bf16
+    assert lib.madd_encode_weights(FAKE, FAKE, 1, FAKE, 130, None) == -1   # n % 128
+    assert lib.madd_encode_weights(None, FAKE, 1, None, 8, None) == -1
+
+
+def test_binding_has_no_cpu_fallback(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(B, "_lib", None)
+    with pytest.raises(ImportError):
+        B.lib()

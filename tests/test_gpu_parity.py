@@ -1,0 +1,339 @@
+"""Parity of the HIP step (through the C ABI) with the CPU oracle, on the same
+seeded inputs.  Bar: weight codes bit-exact; fp32 moments within 2 ulp.
+
+Small cases are compared element by element in full (sizes spanning several
+workgroup tiles and ragged tails); the full-size parameter lists run in the
+benchmark's launch configuration and are compared on sampled elements, whose
+trajectories the oracle recomputes one by one (the step is elementwise and its
+random draws are keyed by global index, so a sample is exact).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_10611_amd import binding as B
+from paper_2607_10611_amd import workloads as W
+from gpu_parity_util import (CODE_NP, DevState, HostState, assert_state_equal, gpu_step,
+                             oracle_step, to_dev, to_host)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()  # the HIP library must be built
+    yield
+    torch.cuda.synchronize()
+
+
+def hp(**kw):
+    h = dict(W.DEFAULT_HPARAMS)
+    h.update(kw)
+    return h
+
+
+def random_weights(rng, n, wfmt):
+    x = rng.normal(0, 0.02, n).astype(np.float32)
+    x[rng.random(n) < 0.02] = 0.0
+    big = rng.random(n) < 0.01
+    x[big] = rng.normal(0, 3.0, big.sum())
+    tiny = rng.random(n) < 0.01
+    x[tiny] = rng.normal(0, 1e-6, tiny.sum())
+    if wfmt in ("e4m3", "e5m2"):
+        lim = 448.0 if wfmt == "e4m3" else 57344.0
+        x = np.clip(x, -lim, lim)
+    return x
+
+
+def random_grad(rng, n):
+    g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-6, -1, n)).astype(np.float32)
+    g[rng.random(n) < 0.05] = 0.0
+    out = rng.random(n) < 0.001
+    g[out] *= 100.0
+    return g
+
+
+def encode_both(wfmt, x, block=False):
+    """Initial codes by the oracle and by madd_encode_weights; must agree."""
+    xd = torch.from_numpy(x).cuda()
+    n = x.size
+    if block:
+        q_ref, s_ref = oracle.encode_block(wfmt, x)
+        q = torch.empty(n, dtype=torch.uint8, device="cuda")
+        s = torch.empty(n // 128, dtype=torch.int16, device="cuda")
+        B.madd_encode_weights(xd, q, wfmt, scales=s)
+        torch.cuda.synchronize()
+        assert (to_host(q) == q_ref).all() and (to_host(s, np.uint16) == s_ref).all()
+        return q_ref, s_ref
+    ref = oracle.encode_array(wfmt, x)
+    out = torch.empty(n, dtype={"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8,
+                                "fp32": torch.int32}[wfmt], device="cuda")
+    B.madd_encode_weights(xd, out, wfmt)
+    torch.cuda.synchronize()
+    got = to_host(out, CODE_NP[wfmt])
+    assert (got == ref).all(), f"encode {wfmt}: {np.nonzero(got != ref)[0][:5]}"
+    return ref
+
+
+def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False):
+    rng = np.random.default_rng(seed)
+    x = random_weights(rng, n, wfmt)
+    enc = encode_both(wfmt, x, block)
+    codes, scales = (enc if block else (enc, None))
+    ds = DevState(wfmt, codes, n, scales)
+    hs = HostState(codes, n, scales)
+    for t in range(1, steps + 1):
+        g = random_grad(rng, n)
+        if gfmt == "bf16":
+            g = oracle.encode_array("bf16", g)
+        h = hp(step=t, **hpkw)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
+        oracle_step(wfmt, hs, g, h, gfmt=gfmt, index_base=index_base)
+        torch.cuda.synchronize()
+        w_g, m_g, v_g, ve_g = ds.host()
+        assert_state_equal(f"{wfmt} n={n} t={t}", w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+        if block:
+            assert (to_host(ds.scales, np.uint16) == hs.scales).all(), f"scales t={t}"
+
+
+# ---------------------------------------------------------------------------
+# full element-by-element parity at small sizes
+# ---------------------------------------------------------------------------
+
+def test_config1_full_trajectory():
+    """1024x1024 bf16, N(0, 0.02) weights, fresh N(0, 1e-3) gradients, 10 RNE steps."""
+    n = 1024 * 1024
+    x = W.init_fp32("c1", 0)
+    codes = encode_both("bf16", x)
+    ds, hs = DevState("bf16", codes, n), HostState(codes, n)
+    for t in range(1, 11):
+        g = W.grad_fp32("c1", 0, t)
+        h = W.hparams("c1", step=t)
+        gpu_step(ds, to_dev(g), h)
+        oracle_step("bf16", hs, g, h)
+        torch.cuda.synchronize()
+        assert_state_equal(f"c1 t={t}", *[a for pair in zip(ds.host(), (hs.w, hs.m, hs.v, hs.ve))
+                                          for a in pair])
+
+
+@pytest.mark.parametrize("bias_correction", [1, 0])
+def test_fp32_passthrough_unrounded_step_is_bit_exact(bias_correction):
+    """No rounding into a storage format: the fp32 new weights themselves match."""
+    run_pair("fp32", 3 * 2048 + 77, 6, 11, dict(rounding="rne", bias_correction=bias_correction))
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 9, 127, 2047, 2049, 8191, 8193, 65536 + 13])
+def test_ragged_sizes_sr(n):
+    run_pair("bf16", n, 3, 100 + n, dict(rounding="sr", seed=77), index_base=12345)
+
+
+@pytest.mark.parametrize("index_base", [0, 3, 8, 2 ** 33 + 5])
+def test_index_base_keys_the_draws(index_base):
+    run_pair("bf16", 4096 + 40, 2, 5, dict(rounding="sr", seed=2 ** 40 + 1), index_base=index_base)
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_fp8_storage(wfmt, rounding):
+    run_pair(wfmt, 3 * 8192 + 24, 4, 21, dict(rounding=rounding, lr_add=3e-3, lr_mul=5e-3))
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_block_scaled_fp8(wfmt, rounding):
+    run_pair(wfmt, 5 * 8192 + 3 * 128, 4, 31, dict(rounding=rounding), block=True)
+
+
+def test_bf16_gradients():
+    run_pair("bf16", 20000, 3, 41, dict(rounding="sr"), gfmt="bf16")
+
+
+@pytest.mark.parametrize("kw", [dict(g_max=0.5), dict(d_mult_max=0.05), dict(w_max=0.03),
+                                dict(eps0=0.2), dict(bias_correction=0),
+                                dict(lr_add=0.0), dict(lr_mul=0.0), dict(beta1=0.0, beta2=0.0)])
+def test_algorithm2_options(kw):
+    run_pair("bf16", 10000, 3, 51, dict(rounding="sr", lr_mul=5e-3, **kw))
+
+
+def test_unaligned_buffers_take_the_scalar_path():
+    n = 5000
+    rng = np.random.default_rng(61)
+    x = random_weights(rng, n + 1, "bf16")
+    codes = encode_both("bf16", x)
+    wbuf = to_dev(codes)
+    mbuf, vbuf, vebuf = (torch.zeros(n + 1, device="cuda") for _ in range(3))
+    hs = HostState(codes[1:], n)
+    for t in range(1, 4):
+        g = random_grad(rng, n + 1)
+        gd = to_dev(g)
+        h = hp(step=t, rounding="sr")
+        # element offset 1: every pointer is 2 or 4 bytes off a 16-byte boundary
+        B.madd_step(wbuf[1:], "bf16", gd[1:], mbuf[1:], vbuf[1:], vebuf[1:], h, index_base=7)
+        oracle_step("bf16", hs, np.ascontiguousarray(g[1:]), h, index_base=7)
+        torch.cuda.synchronize()
+        assert_state_equal(f"unaligned t={t}", to_host(wbuf, np.uint16)[1:], hs.w,
+                           to_host(mbuf)[1:], hs.m, to_host(vbuf)[1:], hs.v, to_host(vebuf)[1:],
+                           hs.ve)
+        assert to_host(mbuf)[0] == 0.0  # untouched neighbour
+
+
+def test_nonfinite_gradients():
+    n = 4096
+    rng = np.random.default_rng(71)
+    for wfmt in ("bf16", "e4m3", "e5m2", "fp32"):
+        x = random_weights(rng, n, wfmt)
+        codes = encode_both(wfmt, x)
+        ds, hs = DevState(wfmt, codes, n), HostState(codes, n)
+        g = random_grad(rng, n)
+        g[::97] = np.nan
+        g[1::89] = np.inf
+        g[2::83] = -np.inf
+        h = hp(rounding="sr")
+        gpu_step(ds, to_dev(g), h)
+        oracle_step(wfmt, hs, g, h)
+        torch.cuda.synchronize()
+        w_g, m_g, v_g, ve_g = ds.host()
+        assert_state_equal(f"nonfinite {wfmt}", w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+
+
+def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
+    rng = np.random.default_rng(81)
+    layout = [("bf16", 3000, False), ("e4m3", 8192, True), ("fp32", 17, False),
+              ("bf16", 20480, False), ("e5m2", 1024, False), ("e5m2", 384, True),
+              ("bf16", 0, False), ("e4m3", 5000, False)]
+    devs, hosts, singles = [], [], []
+    for wfmt, n, blk in layout:
+        x = random_weights(rng, n, wfmt)
+        enc = encode_both(wfmt, x, blk) if n else ((np.zeros(0, CODE_NP[wfmt]),
+                                                    np.zeros(0, np.uint16)) if blk else
+                                                   np.zeros(0, CODE_NP[wfmt]))
+        codes, scales = (enc if blk else (enc, None))
+        devs.append(DevState(wfmt, codes, n, scales))
+        singles.append(DevState(wfmt, codes, n, scales))
+        hosts.append(HostState(codes, n, scales))
+    base = 1000
+    for t in range(1, 4):
+        gs = [random_grad(rng, n) for _, n, _ in layout]
+        gds = [to_dev(g) for g in gs]
+        h = hp(step=t, rounding="sr", seed=314)
+        tl = B.TensorList([d.w for d in devs], [d.wfmt for d in devs], gds, [d.m for d in devs],
+                          [d.v for d in devs], [d.ve for d in devs],
+                          scales=[d.scales for d in devs])
+        B.madd_multi_tensor_step(tl, h, index_base=base)
+        off = base
+        for (wfmt, n, blk), d1, hs, g, gd in zip(layout, singles, hosts, gs, gds):
+            if n:
+                gpu_step(d1, gd, h, index_base=off)
+                oracle_step(wfmt, hs, g, h, index_base=off)
+            off += n
+        torch.cuda.synchronize()
+        for (wfmt, n, blk), d, d1, hs in zip(layout, devs, singles, hosts):
+            if not n:
+                continue
+            w_g, m_g, v_g, ve_g = d.host()
+            assert_state_equal(f"multi {wfmt} n={n} t={t}", w_g, hs.w, m_g, hs.m, v_g, hs.v,
+                               ve_g, hs.ve)
+            for a, b in zip(d.host(), d1.host()):
+                assert a.tobytes() == b.tobytes()
+            if blk:
+                assert (to_host(d.scales, np.uint16) == hs.scales).all()
+
+
+def test_init_state_zeroes():
+    n = 70001
+    ts = [torch.full((n,), 3.0, device="cuda") for _ in range(3)]
+    B.madd_init_state(*ts)
+    torch.cuda.synchronize()
+    assert all(float(t.abs().max()) == 0.0 for t in ts)
+
+
+def test_encode_weights_all_formats():
+    rng = np.random.default_rng(91)
+    x = random_weights(rng, 128 * 333, "bf16")
+    x[:5] = [np.nan, np.inf, -np.inf, 1e38, -3e38]
+    for wfmt in ("bf16", "e4m3", "e5m2", "fp32"):
+        encode_both(wfmt, x)
+    for wfmt in ("e4m3", "e5m2"):
+        encode_both(wfmt, np.nan_to_num(x, nan=0.0, posinf=1.0, neginf=-1.0), block=True)
+
+
+# ---------------------------------------------------------------------------
+# full-size parameter lists, sampled
+# ---------------------------------------------------------------------------
+
+def sample_indices(n, rng, k=4096):
+    if n <= 3 * k:
+        return np.arange(n)
+    head, tail = np.arange(k), np.arange(n - k, n)
+    mid = np.sort(rng.choice(np.arange(k, n - k), size=k, replace=False))
+    return np.concatenate([head, mid, tail])
+
+
+def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096):
+    """Whole list on the GPU with one multi-tensor call per step (the benchmark
+    launch); the oracle follows sampled elements of every tensor."""
+    specs = W.specs(cfg)
+    wfmt = wfmt or W.CONFIGS[cfg]["wfmt"]
+    rng = np.random.default_rng(7)
+    ws, ms, vs, ves, gs, samples, hosts = [], [], [], [], [], [], []
+    offsets = np.cumsum([0] + [s.numel for s in specs])
+    for i, s in enumerate(specs):
+        x = W.init_fp32_device(cfg, i)
+        w = torch.empty(s.numel, dtype={"bf16": torch.int16, "e4m3": torch.uint8,
+                                        "e5m2": torch.uint8}[wfmt], device="cuda")
+        B.madd_encode_weights(x, w, wfmt)
+        idx = sample_indices(s.numel, rng, per_tensor)
+        idx_t = torch.from_numpy(idx).cuda()
+        x_s = to_host(x[idx_t])
+        codes_ref = oracle.encode_array(wfmt, x_s)
+        assert (to_host(w[idx_t], CODE_NP[wfmt]) == codes_ref).all(), f"encode {s.name}"
+        del x
+        ws.append(w)
+        ms.append(torch.zeros(s.numel, device="cuda"))
+        vs.append(torch.zeros(s.numel, device="cuda"))
+        ves.append(torch.zeros(s.numel, device="cuda"))
+        gs.append(torch.empty(s.numel, device="cuda"))
+        samples.append((idx, idx_t))
+        hosts.append(HostState(codes_ref, idx.size))
+    tl = B.TensorList(ws, [wfmt] * len(ws), gs, ms, vs, ves)
+    for t in range(1, steps + 1):
+        for i in range(len(specs)):
+            W.grad_fp32_device_(cfg, i, t, gs[i])
+        h = W.hparams(cfg, step=t)
+        B.madd_multi_tensor_step(tl, h)
+        for i, (idx, idx_t) in enumerate(samples):
+            g_s = to_host(gs[i][idx_t])
+            oracle_step(wfmt, hosts[i], g_s, h, gidx=idx + offsets[i])
+        if t == steps or t % 5 == 0:
+            torch.cuda.synchronize()
+            for i, (idx, idx_t) in enumerate(samples):
+                hs = hosts[i]
+                assert_state_equal(f"{cfg} {specs[i].name} t={t}",
+                                   to_host(ws[i][idx_t], CODE_NP[wfmt]), hs.w,
+                                   to_host(ms[i][idx_t]), hs.m, to_host(vs[i][idx_t]), hs.v,
+                                   to_host(ves[i][idx_t]), hs.ve)
+    return offsets[-1]
+
+
+def test_config2_gpt2_small_100_steps_sampled():
+    assert run_list_sampled("c2", 100, per_tensor=1024) == 124_439_808
+
+
+def test_config3_llama_1b_sampled():
+    assert run_list_sampled("c3", 10) == 1_100_048_384
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+def test_config4_llama_1b_fp8_sampled(wfmt):
+    assert run_list_sampled("c4", 10, wfmt=wfmt) == 1_100_048_384
+
+
+def test_config5_llama_7b_sampled():
+    free, _ = torch.cuda.mem_get_info()
+    need = 6_738_415_616 * 18 + (1 << 30)
+    assert free > need, f"config 5 needs {need / 2**30:.0f} GiB of device memory"
+    assert run_list_sampled("c5", 3, per_tensor=2048) == 6_738_415_616
