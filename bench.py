@@ -103,6 +103,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=1 << 23)
     ap.add_argument("--cpu-steps", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-gib", type=float, default=0.0,
+                    help="after timing, run one plain device copy of this many GiB (a known "
+                         "byte count that calibrates HBM traffic counters in a profiler run)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -184,6 +187,16 @@ def main():
     avg_launch_ms = sum(per_launch_ms) / len(per_launch_ms)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})"
         f", launches min {min(per_launch_ms):.3f} max {max(per_launch_ms):.3f} ms")
+
+    if args.copy_probe_gib > 0:
+        nbytes = int(args.copy_probe_gib * 2**30) // 4 * 4
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: {nbytes} bytes read + {nbytes} bytes written")
+        del src, dst
 
     alg_bytes = nparam * BYTES_PER_PARAM[wfmt]
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9

@@ -10,13 +10,21 @@
 // or stochastically with a Philox4x32-10 draw keyed by (seed, step, element).
 //
 // Layout of work: a launch covers a list of tensors.  The element space of
-// each tensor is cut into chunks of kChunk elements; one workgroup (256
-// threads, four wave64s) owns one chunk and walks it in tiles of 2048
-// elements, eight consecutive elements per thread, so every thread issues
-// 16-byte loads and stores (bf16 weights: one 16-byte access per 8 weights;
-// fp32 arrays: two).  A workgroup finds its tensor by a binary search over the
-// descriptor table (uniform, scalar loads).  Loads and stores of the streamed
-// arrays are non-temporal: nothing is reused within a step.
+// each tensor is cut into chunks; one workgroup (256 threads, four wave64s)
+// owns one chunk.  A chunk is made of tiles of 2048 elements, each split into
+// two sub-tiles of 1024; thread t handles the four consecutive elements
+// [4t, 4t+4) of both sub-tiles, so every load and store instruction of a
+// wave covers one contiguous span (1 KiB for fp32 arrays) and all ten loads
+// of a tile are in flight before any arithmetic.  A workgroup finds its
+// tensor by a binary search over the descriptor table (uniform, scalar
+// loads).  Loads and stores of the streamed arrays are non-temporal global
+// accesses: nothing is reused within a step.
+//
+// Random draws: the eight elements of an aligned group share one Philox
+// block.  Lanes 2k and 2k+1 cover one group of sub-tile A and one of
+// sub-tile B; the even lane computes the A block, the odd lane the B block,
+// and each hands the half its partner needs across a DPP lane swap, so a
+// block is computed once per eight elements.
 //
 // Arithmetic: FP32, one fixed operation order (step_elem), built with
 // -ffp-contract=off so that only the written fmaf calls fuse; division and
@@ -38,9 +46,10 @@
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kVec = 8;                      // consecutive elements per thread
-constexpr int kTile = kThreads * kVec;       // 2048 elements per workgroup tile
-constexpr int kTilesPerChunk = 4;
+constexpr int kQuad = 4;                     // consecutive elements per thread and sub-tile
+constexpr int kSub = kThreads * kQuad;       // 1024 elements per sub-tile
+constexpr int kTile = 2 * kSub;              // sub-tiles A and B
+constexpr int kTilesPerChunk = 1;
 constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
 constexpr int kBlock = 128;                  // block-scaled FP8 block length
 
@@ -69,7 +78,7 @@ struct TensorDesc {
   int64_t n;       // elements
   int64_t gbase;   // global index of element 0
   int64_t chunk0;  // first chunk of this tensor within the launch
-  int32_t vec_ok;  // buffers aligned for 16-byte accesses
+  int32_t vec_ok;  // buffers 16-byte aligned and gbase a multiple of 8
   int32_t pad;
 };
 
@@ -93,9 +102,10 @@ __device__ __forceinline__ void st_nt(T* p, T x) {
 __device__ __forceinline__ u4 philox10(u4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
-    c = u4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;  // one v_mad_u64_u32 each
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = u4{(uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1,
+           (uint32_t)p0};
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }
@@ -254,6 +264,10 @@ __device__ __forceinline__ float clampf(float x, float lo, float hi) {
   return x < lo ? lo : (x > hi ? hi : x);  // NaN passes through
 }
 
+// CLAMP = false drops the g_max and w_max clamps; the host selects it only
+// when both bounds are +infinity, where the clamps are the identity (also for
+// NaN and infinite arguments), so the results are the same bits.
+template <bool CLAMP>
 __device__ __forceinline__ float step_elem(float w, float g, float& m, float& v, float& ve,
                                            const Scalars& s) {
   const float LN2 = 0.693147182464599609375f;  // fp32(ln 2)
@@ -264,7 +278,8 @@ __device__ __forceinline__ float step_elem(float w, float g, float& m, float& v,
   // multiplicative branch: exponent gradient and its second moment
   const float ge = (LN2 * w) * g;
   ve = fmaf(s.B2, ve, s.OMB2 * (ge * ge));
-  const float r = clampf(ge / (sqrtf(ve * s.IBC2) + s.EPS), -s.GMAX, s.GMAX);
+  float r = ge / (sqrtf(ve * s.IBC2) + s.EPS);
+  if (CLAMP) r = clampf(r, -s.GMAX, s.GMAX);
   const float ut = -(s.LRM * r);
   // relative conversion and clip
   const float aw = fabsf(w);
@@ -272,77 +287,65 @@ __device__ __forceinline__ float step_elem(float w, float g, float& m, float& v,
   const float um = clampf(ut / rho, s.ULO, s.UHI);
   // combine, optional final clamp
   const float wn = fmaf(w, um, w) + ua;
-  return clampf(wn, -s.WMAX, s.WMAX);
+  return CLAMP ? clampf(wn, -s.WMAX, s.WMAX) : wn;
 }
 
 // ---------------------------------------------------------------------------
-// Vector loads / stores of eight consecutive elements
+// Global-memory accesses of four consecutive elements
 // ---------------------------------------------------------------------------
 
+#define GLOBAL __attribute__((address_space(1)))
+
+template <typename T>
+__device__ __forceinline__ T ldg(const void* p) {
+  return __builtin_nontemporal_load((const GLOBAL T*)p);
+}
+template <typename T>
+__device__ __forceinline__ void stg(void* p, T x) {
+  __builtin_nontemporal_store(x, (GLOBAL T*)p);
+}
+
 template <int WF>
-struct WVec;
+struct WQuad;
 template <>
-struct WVec<WF_BF16> {
-  u4 raw;
-  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ld_nt((const u4*)((const uint16_t*)p + e)); }
+struct WQuad<WF_BF16> {  // 4 x 16 bits
+  u2 raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ldg<u2>((const uint16_t*)p + e); }
   __device__ __forceinline__ uint32_t code(int k) const { return (raw[k >> 1] >> (16 * (k & 1))) & 0xFFFFu; }
   __device__ __forceinline__ void set(int k, uint32_t c) {
     raw[k >> 1] = (k & 1) ? ((raw[k >> 1] & 0xFFFFu) | (c << 16)) : ((raw[k >> 1] & 0xFFFF0000u) | c);
   }
-  __device__ __forceinline__ void store(void* p, int64_t e) { st_nt((u4*)((uint16_t*)p + e), raw); }
+  __device__ __forceinline__ void store(void* p, int64_t e) const { stg<u2>((uint16_t*)p + e, raw); }
 };
 template <int WF>
-struct WVec8 {
-  u2 raw;
-  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ld_nt((const u2*)((const uint8_t*)p + e)); }
-  __device__ __forceinline__ uint32_t code(int k) const { return (raw[k >> 2] >> (8 * (k & 3))) & 0xFFu; }
-  __device__ __forceinline__ void set(int k, uint32_t c) {
-    const int sh = 8 * (k & 3);
-    raw[k >> 2] = (raw[k >> 2] & ~(0xFFu << sh)) | (c << sh);
-  }
-  __device__ __forceinline__ void store(void* p, int64_t e) { st_nt((u2*)((uint8_t*)p + e), raw); }
+struct WQuad8 {  // 4 x 8 bits
+  uint32_t raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ldg<uint32_t>((const uint8_t*)p + e); }
+  __device__ __forceinline__ uint32_t code(int k) const { return (raw >> (8 * k)) & 0xFFu; }
+  __device__ __forceinline__ void set(int k, uint32_t c) { raw = (raw & ~(0xFFu << (8 * k))) | (c << (8 * k)); }
+  __device__ __forceinline__ void store(void* p, int64_t e) const { stg<uint32_t>((uint8_t*)p + e, raw); }
 };
 template <>
-struct WVec<WF_E4M3> : WVec8<WF_E4M3> {};
+struct WQuad<WF_E4M3> : WQuad8<WF_E4M3> {};
 template <>
-struct WVec<WF_E5M2> : WVec8<WF_E5M2> {};
+struct WQuad<WF_E5M2> : WQuad8<WF_E5M2> {};
 template <>
-struct WVec<WF_FP32> {
-  u4 a, b;
-  __device__ __forceinline__ void load(const void* p, int64_t e) {
-    a = ld_nt((const u4*)((const uint32_t*)p + e));
-    b = ld_nt((const u4*)((const uint32_t*)p + e + 4));
-  }
-  __device__ __forceinline__ uint32_t code(int k) const { return k < 4 ? a[k] : b[k - 4]; }
-  __device__ __forceinline__ void set(int k, uint32_t c) {
-    if (k < 4) a[k] = c;
-    else b[k - 4] = c;
-  }
-  __device__ __forceinline__ void store(void* p, int64_t e) {
-    st_nt((u4*)((uint32_t*)p + e), a);
-    st_nt((u4*)((uint32_t*)p + e + 4), b);
-  }
+struct WQuad<WF_FP32> {  // 4 x 32 bits
+  u4 raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) { raw = ldg<u4>((const uint32_t*)p + e); }
+  __device__ __forceinline__ uint32_t code(int k) const { return raw[k]; }
+  __device__ __forceinline__ void set(int k, uint32_t c) { raw[k] = c; }
+  __device__ __forceinline__ void store(void* p, int64_t e) const { stg<u4>((uint32_t*)p + e, raw); }
 };
-
-__device__ __forceinline__ void ld8f(const float* p, int64_t e, float (&x)[8]) {
-  const f4 a = ld_nt((const f4*)(p + e));
-  const f4 b = ld_nt((const f4*)(p + e + 4));
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-}
-__device__ __forceinline__ void st8f(float* p, int64_t e, const float (&x)[8]) {
-  st_nt((f4*)(p + e), f4{x[0], x[1], x[2], x[3]});
-  st_nt((f4*)(p + e + 4), f4{x[4], x[5], x[6], x[7]});
-}
 
 template <int GF>
-__device__ __forceinline__ void ld8g(const void* p, int64_t e, float (&x)[8]) {
+__device__ __forceinline__ f4 ld4g(const void* p, int64_t e) {
   if constexpr (GF == GF_FP32) {
-    ld8f((const float*)p, e, x);
+    return ldg<f4>((const float*)p + e);
   } else {
-    const u4 r = ld_nt((const u4*)((const uint16_t*)p + e));
-#pragma unroll
-    for (int k = 0; k < 8; ++k) x[k] = dec_bf16((r[k >> 1] >> (16 * (k & 1))) & 0xFFFFu);
+    const u2 r = ldg<u2>((const uint16_t*)p + e);
+    return f4{dec_bf16(r.x & 0xFFFFu), dec_bf16(r.x >> 16), dec_bf16(r.y & 0xFFFFu),
+              dec_bf16(r.y >> 16)};
   }
 }
 
@@ -365,26 +368,92 @@ __device__ __forceinline__ void st1w(void* p, int64_t e, uint32_t c) {
   else ((uint8_t*)p)[e] = (uint8_t)c;
 }
 
-// The eight 16-bit draws of elements gidx0 .. gidx0+7.
+// One sub-tile's worth of a thread's inputs: four consecutive elements.
+template <int WF>
+struct Quad {
+  WQuad<WF> w;
+  f4 g, m, v, ve;
+};
+
+template <int WF, int GF>
+__device__ __forceinline__ void load_quad(Quad<WF>& q, const TensorDesc& d, int64_t e) {
+  q.w.load(d.w, e);
+  q.g = ld4g<GF>(d.g, e);
+  q.m = ldg<f4>(d.m + e);
+  q.v = ldg<f4>(d.v + e);
+  q.ve = ldg<f4>(d.ve + e);
+}
+
+template <int WF>
+__device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& d, int64_t e) {
+  q.w.store(d.w, e);
+  stg<f4>(d.m + e, q.m);
+  stg<f4>(d.v + e, q.v);
+  stg<f4>(d.ve + e, q.ve);
+}
+
+// Swap a value with the neighbouring lane (DPP quad_perm [1,0,3,2]).
+__device__ __forceinline__ uint32_t swap_lane_pair(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);
+}
+
+// The 16-bit draws of a thread's four A elements and four B elements when
+// the groups are 8-aligned in the global index (gA = global index of the
+// pair's first A element, a multiple of 8; the pair's B group is gA + 1024).
+// Every lane of the wave must call this (lane swap).
 template <bool SR>
-__device__ __forceinline__ void draws8(uint64_t gidx0, const Scalars& s, uint32_t (&r)[8]) {
+__device__ __forceinline__ void draws_aligned(uint64_t gA, const Scalars& s, uint32_t (&rA)[4],
+                                              uint32_t (&rB)[4]) {
   if constexpr (!SR) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) r[k] = 0u;
+    for (int k = 0; k < 4; ++k) rA[k] = rB[k] = 0u;
   } else {
-    const uint32_t off = (uint32_t)(gidx0 & 7u);
-    const u4 a = draw_group(gidx0 >> 3, s);
-    if (off == 0u) {
+    const bool odd = (threadIdx.x & 1u) != 0u;
+    const u4 P = draw_group((gA >> 3) + (odd ? (uint64_t)(kSub / 8) : 0u), s);
+    // even lane keeps words x,y of its A block and sends z,w; odd lane keeps
+    // z,w of its B block and sends x,y
+    const uint32_t r0 = swap_lane_pair(odd ? P.x : P.z);
+    const uint32_t r1 = swap_lane_pair(odd ? P.y : P.w);
+    const uint32_t a0 = odd ? r0 : P.x, a1 = odd ? r1 : P.y;
+    const uint32_t b0 = odd ? P.z : r0, b1 = odd ? P.w : r1;
+    rA[0] = a0 & 0xFFFFu; rA[1] = a0 >> 16; rA[2] = a1 & 0xFFFFu; rA[3] = a1 >> 16;
+    rB[0] = b0 & 0xFFFFu; rB[1] = b0 >> 16; rB[2] = b1 & 0xFFFFu; rB[3] = b1 >> 16;
+  }
+}
+
+// Draws of four consecutive elements starting at an arbitrary global index.
+template <bool SR>
+__device__ __forceinline__ void draws_any(uint64_t g0, const Scalars& s, uint32_t (&r)[4]) {
+  if constexpr (!SR) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) r[k] = lane16(a, (uint32_t)k);
+    for (int k = 0; k < 4; ++k) r[k] = 0u;
+  } else {
+    const uint32_t off = (uint32_t)(g0 & 7u);
+    const u4 a = draw_group(g0 >> 3, s);
+    if (off <= 4u) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[k] = lane16(a, off + (uint32_t)k);
     } else {
-      const u4 b = draw_group((gidx0 >> 3) + 1u, s);
+      const u4 b = draw_group((g0 >> 3) + 1u, s);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < 4; ++k) {
         const uint32_t l = off + (uint32_t)k;
         r[k] = l < 8u ? lane16(a, l) : lane16(b, l - 8u);
       }
     }
+  }
+}
+
+template <int WF, bool SR, bool CLAMP>
+__device__ __forceinline__ void step_quad(Quad<WF>& q, const uint32_t (&r)[4], const Scalars& s) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float m = q.m[k], v = q.v[k], ve = q.ve[k];
+    const float wn = step_elem<CLAMP>(decode<WF>(q.w.code(k)), q.g[k], m, v, ve, s);
+    q.m[k] = m;
+    q.v[k] = v;
+    q.ve[k] = ve;
+    q.w.set(k, encode<WF>(wn, SR, r[k]));
   }
 }
 
@@ -404,14 +473,15 @@ __device__ __forceinline__ TensorDesc find_tensor(const TensorDesc* __restrict__
   return table[lo];
 }
 
-template <int WF, int GF, bool SR>
+// Elements [b, e) one at a time (tails and unaligned buffers).
+template <int WF, int GF, bool SR, bool CLAMP>
 __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b, int64_t e,
                                                   const Scalars& s) {
   for (int64_t i = b; i < e; ++i) {
     float m = d.m[i], v = d.v[i], ve = d.ve[i];
     const float w = decode<WF>(ld1w<WF>(d.w, i));
     const float g = ld1g<GF>(d.g, i);
-    const float wn = step_elem(w, g, m, v, ve, s);
+    const float wn = step_elem<CLAMP>(w, g, m, v, ve, s);
     const uint32_t r16 = SR ? draw_one((uint64_t)(d.gbase + i), s) : 0u;
     st1w<WF>(d.w, i, encode<WF>(wn, SR, r16));
     d.m[i] = m;
@@ -420,7 +490,7 @@ __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b
   }
 }
 
-template <int WF, int GF, bool SR>
+template <int WF, int GF, bool SR, bool CLAMP>
 __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* __restrict__ table,
                                                              int ntab, TensorDesc single,
                                                              Scalars s) {
@@ -430,39 +500,77 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
   const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
-    const int64_t e0 = c0 + (int64_t)tile * kTile + (int64_t)threadIdx.x * kVec;
-    if (e0 >= cend) break;
-    if (d.vec_ok && e0 + kVec <= cend) {
-      WVec<WF> wv;
-      wv.load(d.w, e0);
-      float g[8], m[8], v[8], ve[8];
-      ld8g<GF>(d.g, e0, g);
-      ld8f(d.m, e0, m);
-      ld8f(d.v, e0, v);
-      ld8f(d.ve, e0, ve);
-      uint32_t r[8];
-      draws8<SR>((uint64_t)(d.gbase + e0), s, r);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float wn = step_elem(decode<WF>(wv.code(k)), g[k], m[k], v[k], ve[k], s);
-        wv.set(k, encode<WF>(wn, SR, r[k]));
-      }
-      wv.store(d.w, e0);
-      st8f(d.m, e0, m);
-      st8f(d.v, e0, v);
-      st8f(d.ve, e0, ve);
-    } else {
-      const int64_t e1 = (e0 + kVec < cend) ? e0 + kVec : cend;
-      step_scalar_range<WF, GF, SR>(d, e0, e1, s);
+    const int64_t tb = c0 + (int64_t)tile * kTile;
+    if (tb >= cend) break;  // uniform
+    const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
+    if (!d.vec_ok) {  // uniform: unaligned buffers or index base
+      if (eA < cend) step_scalar_range<WF, GF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+      if (eB < cend) step_scalar_range<WF, GF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
+      continue;
+    }
+    const bool fullA = eA + kQuad <= cend, fullB = eB + kQuad <= cend;
+    Quad<WF> qa, qb;
+    if (fullA) load_quad<WF, GF>(qa, d, eA);
+    if (fullB) load_quad<WF, GF>(qb, d, eB);
+    uint32_t rA[4], rB[4];
+    draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+    if (fullA) {
+      step_quad<WF, SR, CLAMP>(qa, rA, s);
+      store_quad<WF>(qa, d, eA);
+    } else if (eA < cend) {
+      step_scalar_range<WF, GF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+    }
+    if (fullB) {
+      step_quad<WF, SR, CLAMP>(qb, rB, s);
+      store_quad<WF>(qb, d, eB);
+    } else if (eB < cend) {
+      step_scalar_range<WF, GF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
     }
   }
 }
 
-// Block-scaled FP8: sixteen consecutive threads hold one 128-element block;
-// the block's max |w'| is combined across them with lane shuffles.  Every
-// thread of the workgroup runs the shuffles (inactive ones with zeros), and
-// the launch requires n % 128 == 0, so a block is never split.
-template <int WF, int GF, bool SR>
+// Block-scaled FP8: 32 consecutive lanes hold one 128-element block of a
+// sub-tile; the block's max |w'| is combined across them with lane shuffles.
+// The launch requires n % 128 == 0, so a block is never split and whole
+// 32-lane groups are active or inactive together; every lane runs the
+// shuffles and the draw exchange.
+__device__ __forceinline__ uint32_t block_amax32(uint32_t a) {
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)a, off, 32);
+    a = o > a ? o : a;
+  }
+  return a;
+}
+
+template <int WF, bool SR, bool CLAMP>
+__device__ __forceinline__ uint32_t step_quad_unrounded(Quad<WF>& q, float sold, float (&wn)[4],
+                                                        const Scalars& s) {
+  uint32_t amax = 0u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float m = q.m[k], v = q.v[k], ve = q.ve[k];
+    wn[k] = step_elem<CLAMP>(decode<WF>(q.w.code(k)) * sold, q.g[k], m, v, ve, s);
+    q.m[k] = m;
+    q.v[k] = v;
+    q.ve[k] = ve;
+    const uint32_t ab = __float_as_uint(wn[k]) & 0x7FFFFFFFu;
+    amax = ab > amax ? ab : amax;
+  }
+  return amax;
+}
+
+template <int WF, bool SR>
+__device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[4], uint32_t amax,
+                                                 const uint32_t (&r)[4]) {
+  const uint32_t sc = block_scale<WF>(amax);
+  const float sf = dec_fp16(sc);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) q.w.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
+  return sc;
+}
+
+template <int WF, int GF, bool SR, bool CLAMP>
 __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
   const int64_t chunk = blockIdx.x;
@@ -471,44 +579,35 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
   const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
-    const int64_t tbase = c0 + (int64_t)tile * kTile;
-    if (tbase >= cend) break;  // uniform across the workgroup
-    const int64_t e0 = tbase + (int64_t)threadIdx.x * kVec;
-    const bool active = e0 < cend;  // whole 16-thread groups agree
-    WVec<WF> wv;
-    float g[8], m[8], v[8], ve[8], wn[8];
-    uint32_t amax = 0u;
-    uint32_t r[8];
-    if (active) {
-      wv.load(d.w, e0);
-      ld8g<GF>(d.g, e0, g);
-      ld8f(d.m, e0, m);
-      ld8f(d.v, e0, v);
-      ld8f(d.ve, e0, ve);
-      const float sold = dec_fp16(d.scales[e0 / kBlock]);
-      draws8<SR>((uint64_t)(d.gbase + e0), s, r);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        wn[k] = step_elem(decode<WF>(wv.code(k)) * sold, g[k], m[k], v[k], ve[k], s);
-        const uint32_t ab = __float_as_uint(wn[k]) & 0x7FFFFFFFu;
-        amax = ab > amax ? ab : amax;
-      }
+    const int64_t tb = c0 + (int64_t)tile * kTile;
+    if (tb >= cend) break;
+    const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
+    const bool actA = eA < cend, actB = eB < cend;  // whole 32-lane groups agree
+    Quad<WF> qa, qb;
+    float wa[4], wb[4];
+    uint32_t amaxA = 0u, amaxB = 0u;
+    if (actA) load_quad<WF, GF>(qa, d, eA);
+    if (actB) load_quad<WF, GF>(qb, d, eB);
+    uint32_t rA[4], rB[4];
+    if (d.vec_ok) {  // uniform: index base a multiple of 8
+      draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+    } else {
+      draws_any<SR>((uint64_t)(d.gbase + eA), s, rA);
+      draws_any<SR>((uint64_t)(d.gbase + eB), s, rB);
     }
-#pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) {
-      const uint32_t o = (uint32_t)__shfl_xor((int)amax, off, 16);
-      amax = o > amax ? o : amax;
+    if (actA) amaxA = step_quad_unrounded<WF, SR, CLAMP>(qa, dec_fp16(d.scales[eA / kBlock]), wa, s);
+    if (actB) amaxB = step_quad_unrounded<WF, SR, CLAMP>(qb, dec_fp16(d.scales[eB / kBlock]), wb, s);
+    amaxA = block_amax32(amaxA);
+    amaxB = block_amax32(amaxB);
+    if (actA) {
+      const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA);
+      store_quad<WF>(qa, d, eA);
+      if ((threadIdx.x & 31u) == 0u) d.scales[eA / kBlock] = (uint16_t)sc;
     }
-    if (active) {
-      const uint32_t sc = block_scale<WF>(amax);
-      const float sf = dec_fp16(sc);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) wv.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
-      wv.store(d.w, e0);
-      st8f(d.m, e0, m);
-      st8f(d.v, e0, v);
-      st8f(d.ve, e0, ve);
-      if ((threadIdx.x & 15u) == 0u) d.scales[e0 / kBlock] = (uint16_t)sc;
+    if (actB) {
+      const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB);
+      store_quad<WF>(qb, d, eB);
+      if ((threadIdx.x & 31u) == 0u) d.scales[eB / kBlock] = (uint16_t)sc;
     }
   }
 }
@@ -556,28 +655,46 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
 
 typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
 
-template <int WF, int GF>
-step_fn pick_plain(bool sr) {
-  return sr ? madd_step_kernel<WF, GF, true> : madd_step_kernel<WF, GF, false>;
+template <int WF, int GF, bool SR>
+step_fn pick_plain(bool clamp) {
+  return clamp ? madd_step_kernel<WF, GF, SR, true> : madd_step_kernel<WF, GF, SR, false>;
+}
+template <int WF, int GF, bool SR>
+step_fn pick_block(bool clamp) {
+  return clamp ? madd_step_block_kernel<WF, GF, SR, true> : madd_step_block_kernel<WF, GF, SR, false>;
 }
 template <int WF, int GF>
-step_fn pick_block(bool sr) {
-  return sr ? madd_step_block_kernel<WF, GF, true> : madd_step_block_kernel<WF, GF, false>;
+step_fn pick_plain_sr(bool sr, bool clamp) {
+  return sr ? pick_plain<WF, GF, true>(clamp) : pick_plain<WF, GF, false>(clamp);
+}
+template <int WF, int GF>
+step_fn pick_fp8(bool sr, bool clamp, bool blk) {
+  if (blk) return sr ? pick_block<WF, GF, true>(clamp) : pick_block<WF, GF, false>(clamp);
+  return pick_plain_sr<WF, GF>(sr, clamp);
 }
 
-step_fn pick_kernel(int wf, int gf, bool sr, bool blk) {
-  if (blk) {
-    if (wf == WF_E4M3) return gf == GF_FP32 ? pick_block<WF_E4M3, GF_FP32>(sr) : pick_block<WF_E4M3, GF_BF16>(sr);
-    if (wf == WF_E5M2) return gf == GF_FP32 ? pick_block<WF_E5M2, GF_FP32>(sr) : pick_block<WF_E5M2, GF_BF16>(sr);
-    return nullptr;
-  }
+// Kernel instantiation for (weight format, gradient format, rounding, optional
+// clamps present, block-scaled); nullptr for combinations that do not exist.
+step_fn pick_kernel(int wf, int gf, bool sr, bool clamp, bool blk) {
+  const bool g32 = gf == GF_FP32;
   switch (wf) {
-    case WF_BF16: return gf == GF_FP32 ? pick_plain<WF_BF16, GF_FP32>(sr) : pick_plain<WF_BF16, GF_BF16>(sr);
-    case WF_E4M3: return gf == GF_FP32 ? pick_plain<WF_E4M3, GF_FP32>(sr) : pick_plain<WF_E4M3, GF_BF16>(sr);
-    case WF_E5M2: return gf == GF_FP32 ? pick_plain<WF_E5M2, GF_FP32>(sr) : pick_plain<WF_E5M2, GF_BF16>(sr);
-    case WF_FP32: return gf == GF_FP32 ? pick_plain<WF_FP32, GF_FP32>(sr) : pick_plain<WF_FP32, GF_BF16>(sr);
-    default: return nullptr;
+    case WF_BF16:
+      if (blk) return nullptr;
+      return g32 ? pick_plain_sr<WF_BF16, GF_FP32>(sr, clamp) : pick_plain_sr<WF_BF16, GF_BF16>(sr, clamp);
+    case WF_E4M3:
+      return g32 ? pick_fp8<WF_E4M3, GF_FP32>(sr, clamp, blk) : pick_fp8<WF_E4M3, GF_BF16>(sr, clamp, blk);
+    case WF_E5M2:
+      return g32 ? pick_fp8<WF_E5M2, GF_FP32>(sr, clamp, blk) : pick_fp8<WF_E5M2, GF_BF16>(sr, clamp, blk);
+    case WF_FP32:
+      if (blk) return nullptr;
+      return g32 ? pick_plain_sr<WF_FP32, GF_FP32>(sr, clamp) : pick_plain_sr<WF_FP32, GF_BF16>(sr, clamp);
+    default:
+      return nullptr;
   }
+}
+
+bool needs_clamp(const madd_hparams& hp) {
+  return !(std::isinf(hp.g_max) && hp.g_max > 0) || !(std::isinf(hp.w_max) && hp.w_max > 0);
 }
 
 bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_FP32; }
@@ -706,7 +823,7 @@ TensorDesc make_desc(void* w, uint16_t* scales, const void* g, float* m, float* 
   d.n = n;
   d.gbase = gbase;
   d.chunk0 = 0;
-  d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve);
+  d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (gbase & 7) == 0;
   return d;
 }
 
@@ -801,7 +918,8 @@ int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_
   if (n == 0) return MADD_OK;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
   const Scalars s = make_scalars(*hp);
-  step_fn fn = pick_kernel(wfmt, gfmt, hp->rounding == MADD_ROUND_SR, scales != nullptr);
+  step_fn fn = pick_kernel(wfmt, gfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
+                           scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
   const TensorDesc d = make_desc(w, scales, g, m, v, ve, n, index_base);
   return launch(fn, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
@@ -854,7 +972,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
       }
       if (descs.empty()) continue;
       if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-      step_fn fn = pick_kernel(wf, gfmt, sr, blk != 0);
+      step_fn fn = pick_kernel(wf, gfmt, sr, needs_clamp(*hp), blk != 0);
       if (!fn) return MADD_EUNSUPPORTED;
       TensorDesc* table = nullptr;
       rc = get_table(descs, &table);

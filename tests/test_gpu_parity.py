@@ -156,7 +156,7 @@ def test_bf16_gradients():
                                 dict(eps0=0.2), dict(bias_correction=0),
                                 dict(lr_add=0.0), dict(lr_mul=0.0), dict(beta1=0.0, beta2=0.0)])
 def test_algorithm2_options(kw):
-    run_pair("bf16", 10000, 3, 51, dict(rounding="sr", lr_mul=5e-3, **kw))
+    run_pair("bf16", 10000, 3, 51, {**dict(rounding="sr", lr_mul=5e-3), **kw})
 
 
 def test_unaligned_buffers_take_the_scalar_path():
