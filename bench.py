@@ -6,8 +6,9 @@ kernel launch for a single-format list): read weight codes, gradients and the
 three fp32 moments, update, round the weights back with stochastic rounding,
 write back.  Default workload: the Llama-7B-shaped list (291 tensors,
 6,738,415,616 parameters, bf16 weights, fp32 gradients and m / v / v_e),
-all resident in HBM before timing starts.  Gradients are synthetic (two
-pre-generated sets, alternating between steps).
+all resident in HBM before timing starts, in flat per-role buffers (weights,
+gradients, m, v, v_e each one allocation, tensors as views).  Gradients are
+synthetic (two pre-generated sets, alternating between steps).
 
 Prints one JSON line with optimizer-step throughput (Gparam/s), the achieved
 HBM bandwidth of the step kernel against the 8 TB/s peak, and the CPU oracle
@@ -100,8 +101,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
-    ap.add_argument("--cpu-sample", type=int, default=1 << 23)
-    ap.add_argument("--cpu-steps", type=int, default=4)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24)
+    ap.add_argument("--cpu-steps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run one plain device copy of this many GiB (a known "
@@ -132,28 +133,37 @@ def main():
 
     log(f"workload {cfg}: {len(specs)} tensors, {nparam:,} params, {wfmt} weights")
     t0 = time.perf_counter()
-    ws, ms, vs, ves = [], [], [], []
-    for i, s in enumerate(specs):
+    # Flat per-role layout: one allocation each for the weight codes, the two
+    # gradient sets and each moment, with the 291 tensors as views in list
+    # order (the layout fused optimizers keep their state in).
+    sizes = [s.numel for s in specs]
+
+    def flat(dtype):
+        buf = torch.empty(nparam, dtype=dtype, device=dev)
+        views, off = [], 0
+        for n in sizes:
+            views.append(buf[off:off + n])
+            off += n
+        return buf, views
+
+    wbuf, ws = flat(code_dt)
+    gbufs, grad_sets = [], []
+    gb, gl = flat(torch.float32)
+    gbufs.append(gb)
+    grad_sets.append(gl)
+    mbuf, ms = flat(torch.float32)
+    vbuf, vs = flat(torch.float32)
+    vebuf, ves = flat(torch.float32)
+    gb, gl = flat(torch.float32)
+    gbufs.append(gb)
+    grad_sets.append(gl)
+    for i in range(len(specs)):
         x = W.init_fp32_device(cfg, i, dev)
-        w = torch.empty(s.numel, dtype=code_dt, device=dev)
-        B.madd_encode_weights(x, w, wfmt)
+        B.madd_encode_weights(x, ws[i], wfmt)
         del x
-        ws.append(w)
-        m = torch.empty(s.numel, dtype=torch.float32, device=dev)
-        v = torch.empty_like(m)
-        ve = torch.empty_like(m)
-        B.madd_init_state(m, v, ve)
-        ms.append(m)
-        vs.append(v)
-        ves.append(ve)
-    grad_sets = []
-    for k in range(2):
-        gl = []
-        for i, s in enumerate(specs):
-            g = torch.empty(s.numel, dtype=torch.float32, device=dev)
-            W.grad_fp32_device_(cfg, i, k + 1, g)
-            gl.append(g)
-        grad_sets.append(gl)
+        B.madd_init_state(ms[i], vs[i], ves[i])
+        for k in range(2):
+            W.grad_fp32_device_(cfg, i, k + 1, grad_sets[k][i])
     torch.cuda.synchronize()
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
         f"{time.perf_counter() - t0:.1f} s")
