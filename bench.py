@@ -32,9 +32,13 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
 
-# algorithmic bytes per parameter: read w + g + m + v + v_e, write w + m + v + v_e
-BYTES_PER_PARAM = {"bf16": 2 + 4 + 12 + 2 + 12, "e4m3": 1 + 4 + 12 + 1 + 12,
-                   "e5m2": 1 + 4 + 12 + 1 + 12}
+WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1}
+SBYTES = {"fp32": 4, "bf16": 2}
+
+
+def bytes_per_param(wfmt: str, sfmt: str) -> int:
+    """Algorithmic bytes: read w, g (fp32), m, v, v_e; write w, m, v, v_e."""
+    return 2 * WBYTES[wfmt] + 4 + 6 * SBYTES[sfmt]
 
 WORKLOAD_NAMES = {
     "c5": "llama-7b-shaped list (32 layers, d=4096, SwiGLU 11008, vocab 32000)",
@@ -65,7 +69,7 @@ def traffic_from_profile():
     return float(val.group(1))
 
 
-def cpu_baseline(cfg: str, sample: int, steps: int) -> dict:
+def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32") -> dict:
     """The CPU oracle (single thread) on a bounded sample of the workload: the
     first `sample` elements of the list, `steps` steps."""
     import numpy as np
@@ -85,10 +89,10 @@ def cpu_baseline(cfg: str, sample: int, steps: int) -> dict:
             break
     codes = oracle.encode_array(wfmt, np.concatenate(xs))
     grads = [np.concatenate([g[t] for g in gs]) for t in range(steps)]
-    m, v, ve = (np.zeros(sample, np.float32) for _ in range(3))
+    m, v, ve = (np.zeros(sample, np.float32 if sfmt == "fp32" else np.uint16) for _ in range(3))
     t0 = time.perf_counter()
     for t in range(1, steps + 1):
-        oracle.step(wfmt, codes, grads[t - 1], m, v, ve, W.hparams(cfg, step=t))
+        oracle.step(wfmt, codes, grads[t - 1], m, v, ve, W.hparams(cfg, step=t), sfmt=sfmt)
     dt = time.perf_counter() - t0
     return {"value": sample * steps / dt / 1e9, "unit": "Gparam/s", "cores": 1, "kind": "oracle",
             "sample": f"first {sample:,} parameters of the list, {steps} steps "
@@ -101,8 +105,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
+    ap.add_argument("--states", default="fp32", choices=["fp32", "bf16"],
+                    help="storage of m, v, v_e (bf16: the paper's optimizer-state precision)")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
-    ap.add_argument("--cpu-steps", type=int, default=10)
+    ap.add_argument("--cpu-steps", type=int, default=None,
+                    help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
+                         "whose encoding makes the oracle slower)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run one plain device copy of this many GiB (a known "
@@ -151,9 +159,10 @@ def main():
     gb, gl = flat(torch.float32)
     gbufs.append(gb)
     grad_sets.append(gl)
-    mbuf, ms = flat(torch.float32)
-    vbuf, vs = flat(torch.float32)
-    vebuf, ves = flat(torch.float32)
+    st_dt = torch.float32 if args.states == "fp32" else torch.int16
+    mbuf, ms = flat(st_dt)
+    vbuf, vs = flat(st_dt)
+    vebuf, ves = flat(st_dt)
     gb, gl = flat(torch.float32)
     gbufs.append(gb)
     grad_sets.append(gl)
@@ -208,19 +217,22 @@ def main():
         log(f"copy probe: {nbytes} bytes read + {nbytes} bytes written")
         del src, dst
 
-    alg_bytes = nparam * BYTES_PER_PARAM[wfmt]
+    bpp = bytes_per_param(wfmt, args.states)
+    alg_bytes = nparam * bpp
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
-    traffic = traffic_from_profile() if cfg == "c5" else None
+    traffic = traffic_from_profile() if (cfg == "c5" and args.states == "fp32") else None
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": alg_bytes,
-                "kernel": f"madd_step_kernel<{wfmt}, fp32 grad, SR>",
+                "kernel": f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
+                          f"{W.CONFIGS[cfg]['rounding'].upper()}>",
                 "avg_launch_ms": round(avg_launch_ms, 4)}
 
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
-        cpu = cpu_baseline(cfg, args.cpu_sample, args.cpu_steps)
+        steps = args.cpu_steps or (10 if args.states == "fp32" else 4)
+        cpu = cpu_baseline(cfg, args.cpu_sample, steps, args.states)
 
     out = {
         "metric": METRIC,
@@ -236,9 +248,9 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[cfg], "params": nparam, "tensors": len(specs),
-                   "weight_format": wfmt, "grad_format": "fp32", "state": "fp32 m, v, v_e",
-                   "rounding": W.CONFIGS[cfg]["rounding"],
-                   "bytes_per_param": BYTES_PER_PARAM[wfmt]},
+                   "weight_format": wfmt, "grad_format": "fp32",
+                   "state": f"{args.states} m, v, v_e",
+                   "rounding": W.CONFIGS[cfg]["rounding"], "bytes_per_param": bpp},
         "hbm_gbps": round(alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -77,6 +77,15 @@ typedef enum madd_wfmt {
 /* Gradient formats (decoded exactly to FP32). */
 typedef enum madd_gfmt { MADD_G_FP32 = 0, MADD_G_BF16 = 1 } madd_gfmt;
 
+/* Storage of the moments m, v, v_e.
+ *   FP32 : float arrays.
+ *   BF16 : bfloat16 codes -- the precision of the optimizer states in the
+ *          paper's per-parameter memory accounting (Appendix, memory
+ *          comparison table).  A step decodes them exactly, computes in FP32,
+ *          uses the FP32 results within the step and stores them rounded to
+ *          nearest (ties to even). */
+typedef enum madd_sfmt { MADD_S_FP32 = 0, MADD_S_BF16 = 1 } madd_sfmt;
+
 /* Rounding of the new weight into its storage format.
  *   RNE : round to nearest, ties to even.
  *   SR  : stochastic.  For |x| between adjacent grid points lo < |x| < hi,
@@ -118,9 +127,9 @@ typedef struct madd_hparams {
 } madd_hparams;
 
 /* Zero the optimizer state (Algorithm 1: moments start at 0).
- * m, v, ve: device float arrays of n elements (n >= 0; may be NULL if n == 0).
- * Enqueued on `stream`. */
-int32_t madd_init_state(float* m, float* v, float* ve, int64_t n, void* stream);
+ * m, v, ve: device arrays of n elements stored as sfmt (a madd_sfmt); n >= 0,
+ * NULL allowed when n == 0.  Enqueued on `stream`. */
+int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, void* stream);
 
 /* Round n fp32 values x into weight storage w with round-to-nearest-even.
  * w: device codes of format wfmt (2, 1, 1 or 4 bytes per element).
@@ -143,29 +152,32 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
  *           n % 128 == 0 and 16-byte-aligned w, g, m, v, ve (else
  *           MADD_EINVAL / MADD_EALIGN).
  * g       : device gradient of format gfmt (read only).
- * m, v, ve: device fp32 moments (first, second, multiplicative second).
+ * m, v, ve: device moments (first, second, multiplicative second) stored as
+ *           sfmt (a madd_sfmt), updated in place.
  * index_base: global index of element 0 (keys the stochastic-rounding draw);
  *           a loop of madd_step calls whose bases are the prefix sums of the
  *           sizes is bit-identical to one madd_multi_tensor_step call, and to
  *           any split of the index space (sharding).
  * Unaligned unscaled buffers are accepted and take a slower path with
  * identical results. */
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, float* m,
-                  float* v, float* ve, int64_t n, int64_t index_base, const madd_hparams* hp,
-                  void* stream);
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, void* m,
+                  void* v, void* ve, int32_t sfmt, int64_t n, int64_t index_base,
+                  const madd_hparams* hp, void* stream);
 
 /* One M+Adam step on a list of tensors in as few launches as the formats
  * allow (one per distinct (format, scaled) pair).
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
- * entries; scales: NULL (no tensor block-scaled) or a host array whose entry
- * i is NULL or tensor i's scale array.  Tensor i's elements have global
+ * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
+ * block-scaled) or a host array whose entry i is NULL or tensor i's scale
+ * array.  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
- * The first call with a given list (same pointers and sizes) uploads a small
- * device descriptor table with a synchronous copy and caches it; later calls
- * with the same list enqueue only the kernels. */
+ * The first call with a given list (same pointers and sizes) uploads a device
+ * descriptor table (80 bytes per tensor) with a synchronous copy and caches it
+ * (up to 32 lists per process; evicting one drains the device first).  Later
+ * calls with the same list enqueue only the kernels. */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
                                uint16_t* const* scales, const void* const* g, int32_t gfmt,
-                               float* const* m, float* const* v, float* const* ve,
+                               void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream);
 

@@ -41,6 +41,7 @@ _LIB = os.path.join(_HERE, "libmadd_oracle.so")
 # format / rounding numbering of the oracle's C interface
 FMT = {"bf16": 0, "e4m3": 1, "e5m2": 2, "fp32": 3, "fp16": 4}
 GFMT = {"fp32": 0, "bf16": 1}
+SFMT = {"fp32": 0, "bf16": 1}
 ROUND = {"rne": 0, "sr": 1}
 
 _CODE_DTYPE = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,
@@ -75,9 +76,9 @@ def lib():
         U64 = ctypes.c_uint64
         U32 = ctypes.c_uint32
         hp_args = [D] * 11 + [I, I, U64, I64]
-        L.oracle_step.argtypes = [I, P, I, P, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step.argtypes = [I, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step.restype = I
-        L.oracle_step_block.argtypes = [I, P, P, I, P, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_block.argtypes = [I, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step_block.restype = I
         L.oracle_encode_array.argtypes = [I, P, P, I64]
         L.oracle_encode_array.restype = I
@@ -116,17 +117,21 @@ class OracleError(RuntimeError):
     pass
 
 
-def _check_state(n, g, m, v, ve, gfmt):
+def _check_state(n, g, m, v, ve, gfmt, sfmt):
     gd = np.float32 if gfmt == "fp32" else np.uint16
-    for name, a, dt in (("g", g, gd), ("m", m, np.float32), ("v", v, np.float32),
-                        ("ve", ve, np.float32)):
+    sd = np.float32 if sfmt == "fp32" else np.uint16
+    for name, a, dt in (("g", g, gd), ("m", m, sd), ("v", v, sd), ("ve", ve, sd)):
         if a.dtype != dt or a.size != n:
             raise OracleError(f"{name}: expected {n} x {np.dtype(dt)}, got {a.size} x {a.dtype}")
 
 
 def step(wfmt: str, w: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, ve: np.ndarray,
-         hp: dict, gfmt: str = "fp32", index_base: int = 0, gidx: np.ndarray | None = None):
+         hp: dict, gfmt: str = "fp32", index_base: int = 0, gidx: np.ndarray | None = None,
+         sfmt: str = "fp32"):
     """One M+Adam step in place on host arrays (w codes, g, m, v, ve).
+
+    ``sfmt`` is the storage of the moments: "fp32" (float32 arrays) or
+    "bf16" (uint16 codes).
 
     ``gidx`` (int64, one per element) gives each element's global index for the
     stochastic-rounding draw; without it element i has index ``index_base + i``.
@@ -134,30 +139,30 @@ def step(wfmt: str, w: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, 
     n = w.size
     if w.dtype != _CODE_DTYPE[wfmt]:
         raise OracleError(f"w: expected {np.dtype(_CODE_DTYPE[wfmt])} codes, got {w.dtype}")
-    _check_state(n, g, m, v, ve, gfmt)
+    _check_state(n, g, m, v, ve, gfmt, sfmt)
     if gidx is not None:
         gidx = np.ascontiguousarray(gidx, dtype=np.int64)
         assert gidx.size == n
-    rc = lib().oracle_step(FMT[wfmt], _ptr(w), GFMT[gfmt], _ptr(g), _ptr(m), _ptr(v), _ptr(ve),
-                           n, _ptr(gidx), int(index_base), *_hp_args(hp))
+    rc = lib().oracle_step(FMT[wfmt], _ptr(w), GFMT[gfmt], _ptr(g), SFMT[sfmt], _ptr(m), _ptr(v),
+                           _ptr(ve), n, _ptr(gidx), int(index_base), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step returned {rc}")
 
 
 def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray,
                v: np.ndarray, ve: np.ndarray, hp: dict, gfmt: str = "fp32", index_base: int = 0,
-               gidx: np.ndarray | None = None):
+               gidx: np.ndarray | None = None, sfmt: str = "fp32"):
     """Block-scaled FP8 step (blocks of 128 contiguous elements, FP16 scales)."""
     n = q.size
     if q.dtype != np.uint8 or scales.dtype != np.uint16 or scales.size * 128 != n:
         raise OracleError("q must be uint8 codes and scales uint16, one per 128 elements")
-    _check_state(n, g, m, v, ve, gfmt)
+    _check_state(n, g, m, v, ve, gfmt, sfmt)
     if gidx is not None:
         gidx = np.ascontiguousarray(gidx, dtype=np.int64)
         assert gidx.size == n
-    rc = lib().oracle_step_block(FMT[wfmt], _ptr(q), _ptr(scales), GFMT[gfmt], _ptr(g), _ptr(m),
-                                 _ptr(v), _ptr(ve), n, _ptr(gidx), int(index_base),
-                                 *_hp_args(hp))
+    rc = lib().oracle_step_block(FMT[wfmt], _ptr(q), _ptr(scales), GFMT[gfmt], _ptr(g),
+                                 SFMT[sfmt], _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
+                                 int(index_base), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_block returned {rc}")
 

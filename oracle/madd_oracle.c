@@ -57,6 +57,11 @@
  *     meaningful, so it is dropped).
  *   - FP32 "storage" (test passthrough) keeps the float bits; a NaN is stored
  *     as 0x7FC00000.
+ *   - Moments m, v, v_e are stored in fp32, or in bf16 (the precision of the
+ *     optimizer states in the paper's memory accounting table).  With bf16
+ *     storage the step decodes them exactly, computes in fp32 as above, uses
+ *     the fp32 results within the step and stores them rounded to nearest
+ *     (ties to even).
  *   - Block-scaled FP8: contiguous blocks of 128 elements, one FP16 scale s
  *     per block, weight = q * s (fp32 product).  After the update,
  *     amax = max|w'| over the block; s' = RNE_fp16(amax / FMAX) with
@@ -77,6 +82,7 @@
 
 enum { OF_BF16 = 0, OF_E4M3 = 1, OF_E5M2 = 2, OF_FP32 = 3, OF_FP16 = 4, OF_NFMT = 5 };
 enum { OG_FP32 = 0, OG_BF16 = 1 };
+enum { OS_FP32 = 0, OS_BF16 = 1 }; /* storage of the moments m, v, v_e */
 enum { OR_RNE = 0, OR_SR = 1 };
 
 enum {
@@ -396,6 +402,29 @@ static float load_grad(int gfmt, const void *g, int64_t i) {
   return (float)decode(OF_BF16, ((const uint16_t *)g)[i]);
 }
 
+/* A moment as stored: fp32, or a bf16 code decoded exactly. */
+static float load_state(int sfmt, const void *a, int64_t i) {
+  if (sfmt == OS_FP32) return ((const float *)a)[i];
+  return (float)decode(OF_BF16, ((const uint16_t *)a)[i]);
+}
+
+/* Store a moment: fp32 as is, or rounded to bf16 (nearest, ties to even). */
+static void store_state(int sfmt, void *a, int64_t i, float x) {
+  if (sfmt == OS_FP32) ((float *)a)[i] = x;
+  else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);
+}
+
+/* One element: load the three moments, step, store them back. */
+static float step_stored(float w, float g, int sfmt, void *m, void *v, void *ve, int64_t i,
+                         const oscal *s) {
+  float mi = load_state(sfmt, m, i), vi = load_state(sfmt, v, i), vei = load_state(sfmt, ve, i);
+  const float wn = oracle_step_elem(w, g, &mi, &vi, &vei, s);
+  store_state(sfmt, m, i, mi);
+  store_state(sfmt, v, i, vi);
+  store_state(sfmt, ve, i, vei);
+  return wn;
+}
+
 static uint32_t load_code(int fmt, const void *w, int64_t i) {
   switch (fmt_bits(fmt)) {
   case 8: return ((const uint8_t *)w)[i];
@@ -436,7 +465,7 @@ static int fill_hp(ohp *h, double lr_add, double lr_mul, double beta1, double be
 /* Per-element M+Adam step on an unscaled storage format.
  * Element i has global index gidx[i] (or index_base + i when gidx is NULL),
  * which keys its stochastic-rounding draw. */
-int oracle_step(int wfmt, void *w, int gfmt, const void *g, float *m, float *v, float *ve,
+int oracle_step(int wfmt, void *w, int gfmt, const void *g, int sfmt, void *m, void *v, void *ve,
                 int64_t n, const int64_t *gidx, int64_t index_base, double lr_add, double lr_mul,
                 double beta1, double beta2, double eps, double tau, double r_max, double eps0,
                 double g_max, double d_mult_max, double w_max, int bias_correction, int rounding,
@@ -448,13 +477,14 @@ int oracle_step(int wfmt, void *w, int gfmt, const void *g, float *m, float *v, 
     return ORACLE_EINVAL;
   if (wfmt != OF_BF16 && wfmt != OF_E4M3 && wfmt != OF_E5M2 && wfmt != OF_FP32) return ORACLE_EINVAL;
   if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
   if (n < 0) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
   for (int64_t i = 0; i < n; ++i) {
     const float wv = (float)decode(wfmt, load_code(wfmt, w, i));
     const float gv = load_grad(gfmt, g, i);
-    const float wn = oracle_step_elem(wv, gv, &m[i], &v[i], &ve[i], &s);
+    const float wn = step_stored(wv, gv, sfmt, m, v, ve, i, &s);
     const int64_t idx = gidx ? gidx[i] : index_base + i;
     const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
     store_code(wfmt, w, i, encode(wfmt, wn, h.rounding, r16));
@@ -485,8 +515,8 @@ static uint16_t block_scale(int fmt, const float *wn) {
 
 /* Block-scaled FP8 M+Adam step.  n must be a multiple of 128; elements
  * [128 b, 128 b + 128) form block b with scale scales[b]. */
-int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const void *g, float *m,
-                      float *v, float *ve, int64_t n, const int64_t *gidx, int64_t index_base,
+int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const void *g, int sfmt,
+                      void *m, void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base,
                       double lr_add, double lr_mul, double beta1, double beta2, double eps,
                       double tau, double r_max, double eps0, double g_max, double d_mult_max,
                       double w_max, int bias_correction, int rounding, uint64_t seed,
@@ -498,6 +528,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const vo
     return ORACLE_EINVAL;
   if (wfmt != OF_E4M3 && wfmt != OF_E5M2) return ORACLE_EINVAL;
   if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
   if (n < 0 || n % BLOCK != 0) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
@@ -508,7 +539,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const vo
       const int64_t i = b * BLOCK + k;
       const float wv = (float)decode(wfmt, q[i]) * sold;
       const float gv = load_grad(gfmt, g, i);
-      wn[k] = oracle_step_elem(wv, gv, &m[i], &v[i], &ve[i], &s);
+      wn[k] = step_stored(wv, gv, sfmt, m, v, ve, i, &s);
     }
     const uint16_t snew = block_scale(wfmt, wn);
     const float sf = (float)decode(OF_FP16, snew);

@@ -22,6 +22,8 @@ G_FP32, G_BF16 = 0, 1
 ROUND_RNE, ROUND_SR = 0, 1
 WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32}
 GFMT = {"fp32": G_FP32, "bf16": G_BF16}
+S_FP32, S_BF16 = 0, 1
+SFMT = {"fp32": S_FP32, "bf16": S_BF16}
 ROUND = {"rne": ROUND_RNE, "sr": ROUND_SR}
 
 STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPORTED",
@@ -97,15 +99,15 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         HP = ctypes.POINTER(madd_hparams)
-        L.madd_init_state.argtypes = [P, P, P, I64, P]
+        L.madd_init_state.argtypes = [P, P, P, I32, I64, P]
         L.madd_init_state.restype = I32
         L.madd_encode_weights.argtypes = [P, P, I32, P, I64, P]
         L.madd_encode_weights.restype = I32
-        L.madd_step.argtypes = [P, I32, P, P, I32, P, P, P, I64, I64, HP, P]
+        L.madd_step.argtypes = [P, I32, P, P, I32, P, P, P, I32, I64, I64, HP, P]
         L.madd_step.restype = I32
         PP = ctypes.POINTER(ctypes.c_void_p)
         L.madd_multi_tensor_step.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, I32, PP, PP, PP,
-                                             ctypes.POINTER(I64), I64, HP, P]
+                                             I32, ctypes.POINTER(I64), I64, HP, P]
         L.madd_multi_tensor_step.restype = I32
         L.madd_status_string.argtypes = [I32]
         L.madd_status_string.restype = ctypes.c_char_p
@@ -143,9 +145,22 @@ def _hp(hp) -> madd_hparams:
     return hp.to_c()
 
 
-def madd_init_state(m, v, ve, stream=None):
+def state_format(t) -> str:
+    """Moment storage of a torch tensor: float32 -> "fp32"; bfloat16 (or its
+    16-bit integer view) -> "bf16"."""
+    import torch
+    if t.dtype == torch.float32:
+        return "fp32"
+    if t.dtype in (torch.bfloat16, torch.int16):
+        return "bf16"
+    raise TypeError(f"unsupported moment dtype {t.dtype}")
+
+
+def madd_init_state(m, v, ve, sfmt: str | None = None, stream=None):
     n = m.numel()
-    _check("madd_init_state", lib().madd_init_state(_ptr(m), _ptr(v), _ptr(ve), n, _stream(stream)))
+    sfmt = sfmt or state_format(m)
+    _check("madd_init_state", lib().madd_init_state(_ptr(m), _ptr(v), _ptr(ve), SFMT[sfmt], n,
+                                                    _stream(stream)))
 
 
 def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
@@ -155,21 +170,25 @@ def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
 
 
 def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, index_base: int = 0,
-              n: int | None = None, stream=None):
+              n: int | None = None, sfmt: str | None = None, stream=None):
     """One step on one tensor.  ``w`` holds the weight codes (uint16 / uint8 /
-    int32 storage for bf16 / fp8 / fp32)."""
+    int32 storage for bf16 / fp8 / fp32); the moments' storage follows their
+    dtype unless ``sfmt`` is given."""
     h = _hp(hp)
     n = m.numel() if n is None else n
+    sfmt = sfmt or state_format(m)
     _check("madd_step",
            lib().madd_step(_ptr(w), WFMT[wfmt], _ptr(scales), _ptr(g), GFMT[gfmt], _ptr(m), _ptr(v),
-                           _ptr(ve), int(n), int(index_base), ctypes.byref(h), _stream(stream)))
+                           _ptr(ve), SFMT[sfmt], int(n), int(index_base), ctypes.byref(h),
+                           _stream(stream)))
 
 
 class TensorList:
     """Marshalled pointer arrays of a tensor list, built once and reused."""
 
-    def __init__(self, ws, wfmts, gs, ms, vs, ves, scales=None):
+    def __init__(self, ws, wfmts, gs, ms, vs, ves, scales=None, sfmt: str | None = None):
         k = len(ws)
+        self.sfmt = sfmt or (state_format(ms[0]) if k else "fp32")
         assert all(len(x) == k for x in (wfmts, gs, ms, vs, ves))
         self.n = k
         Arr = ctypes.c_void_p * k
@@ -197,5 +216,6 @@ def madd_multi_tensor_step(tl: TensorList, hp, gfmt: str = "fp32", index_base: i
     cast = lambda a: ctypes.cast(a, PP) if a is not None else None  # noqa: E731
     _check("madd_multi_tensor_step",
            lib().madd_multi_tensor_step(tl.n, cast(tl.w), tl.wfmt, cast(tl.scales), cast(tl.g),
-                                        GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve), tl.numel,
-                                        int(index_base), ctypes.byref(h), _stream(stream)))
+                                        GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve),
+                                        SFMT[tl.sfmt], tl.numel, int(index_base),
+                                        ctypes.byref(h), _stream(stream)))

@@ -71,9 +71,9 @@ struct Scalars {
 struct TensorDesc {
   void* w;
   const void* g;
-  float* m;
-  float* v;
-  float* ve;
+  void* m;   // moments: fp32, or bf16 codes
+  void* v;
+  void* ve;
   uint16_t* scales;
   int64_t n;       // elements
   int64_t gbase;   // global index of element 0
@@ -133,6 +133,7 @@ __device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s) {
 
 enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3 };
 enum : int { GF_FP32 = 0, GF_BF16 = 1 };
+enum : int { SF_FP32 = 0, SF_BF16 = 1 };  // storage of the moments
 
 __device__ __forceinline__ float dec_bf16(uint32_t c) { return __uint_as_float(c << 16); }
 
@@ -368,6 +369,39 @@ __device__ __forceinline__ void st1w(void* p, int64_t e, uint32_t c) {
   else ((uint8_t*)p)[e] = (uint8_t)c;
 }
 
+// Moments as stored: fp32, or bf16 codes (decoded exactly; stored rounded to
+// nearest, ties to even).
+template <int SF>
+__device__ __forceinline__ f4 ld4s(const void* p, int64_t e) {
+  if constexpr (SF == SF_FP32) {
+    return ldg<f4>((const float*)p + e);
+  } else {
+    const u2 r = ldg<u2>((const uint16_t*)p + e);
+    return f4{dec_bf16(r.x & 0xFFFFu), dec_bf16(r.x >> 16), dec_bf16(r.y & 0xFFFFu),
+              dec_bf16(r.y >> 16)};
+  }
+}
+template <int SF>
+__device__ __forceinline__ void st4s(void* p, int64_t e, f4 x) {
+  if constexpr (SF == SF_FP32) {
+    stg<f4>((float*)p + e, x);
+  } else {
+    const u2 r = u2{enc_bf16(x.x, false, 0u) | (enc_bf16(x.y, false, 0u) << 16),
+                    enc_bf16(x.z, false, 0u) | (enc_bf16(x.w, false, 0u) << 16)};
+    stg<u2>((uint16_t*)p + e, r);
+  }
+}
+template <int SF>
+__device__ __forceinline__ float ld1s(const void* p, int64_t e) {
+  if constexpr (SF == SF_FP32) return ((const float*)p)[e];
+  else return dec_bf16(((const uint16_t*)p)[e]);
+}
+template <int SF>
+__device__ __forceinline__ void st1s(void* p, int64_t e, float x) {
+  if constexpr (SF == SF_FP32) ((float*)p)[e] = x;
+  else ((uint16_t*)p)[e] = (uint16_t)enc_bf16(x, false, 0u);
+}
+
 // One sub-tile's worth of a thread's inputs: four consecutive elements.
 template <int WF>
 struct Quad {
@@ -375,21 +409,21 @@ struct Quad {
   f4 g, m, v, ve;
 };
 
-template <int WF, int GF>
+template <int WF, int GF, int SF>
 __device__ __forceinline__ void load_quad(Quad<WF>& q, const TensorDesc& d, int64_t e) {
   q.w.load(d.w, e);
   q.g = ld4g<GF>(d.g, e);
-  q.m = ldg<f4>(d.m + e);
-  q.v = ldg<f4>(d.v + e);
-  q.ve = ldg<f4>(d.ve + e);
+  q.m = ld4s<SF>(d.m, e);
+  q.v = ld4s<SF>(d.v, e);
+  q.ve = ld4s<SF>(d.ve, e);
 }
 
-template <int WF>
+template <int WF, int SF>
 __device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& d, int64_t e) {
   q.w.store(d.w, e);
-  stg<f4>(d.m + e, q.m);
-  stg<f4>(d.v + e, q.v);
-  stg<f4>(d.ve + e, q.ve);
+  st4s<SF>(d.m, e, q.m);
+  st4s<SF>(d.v, e, q.v);
+  st4s<SF>(d.ve, e, q.ve);
 }
 
 // Swap a value with the neighbouring lane (DPP quad_perm [1,0,3,2]).
@@ -474,23 +508,23 @@ __device__ __forceinline__ TensorDesc find_tensor(const TensorDesc* __restrict__
 }
 
 // Elements [b, e) one at a time (tails and unaligned buffers).
-template <int WF, int GF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP>
 __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b, int64_t e,
                                                   const Scalars& s) {
   for (int64_t i = b; i < e; ++i) {
-    float m = d.m[i], v = d.v[i], ve = d.ve[i];
+    float m = ld1s<SF>(d.m, i), v = ld1s<SF>(d.v, i), ve = ld1s<SF>(d.ve, i);
     const float w = decode<WF>(ld1w<WF>(d.w, i));
     const float g = ld1g<GF>(d.g, i);
     const float wn = step_elem<CLAMP>(w, g, m, v, ve, s);
     const uint32_t r16 = SR ? draw_one((uint64_t)(d.gbase + i), s) : 0u;
     st1w<WF>(d.w, i, encode<WF>(wn, SR, r16));
-    d.m[i] = m;
-    d.v[i] = v;
-    d.ve[i] = ve;
+    st1s<SF>(d.m, i, m);
+    st1s<SF>(d.v, i, v);
+    st1s<SF>(d.ve, i, ve);
   }
 }
 
-template <int WF, int GF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP>
 __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* __restrict__ table,
                                                              int ntab, TensorDesc single,
                                                              Scalars s) {
@@ -504,27 +538,48 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
     if (tb >= cend) break;  // uniform
     const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
     if (!d.vec_ok) {  // uniform: unaligned buffers or index base
-      if (eA < cend) step_scalar_range<WF, GF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
-      if (eB < cend) step_scalar_range<WF, GF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
+      if (eA < cend) step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+      if (eB < cend) step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
       continue;
     }
     const bool fullA = eA + kQuad <= cend, fullB = eB + kQuad <= cend;
     Quad<WF> qa, qb;
-    if (fullA) load_quad<WF, GF>(qa, d, eA);
-    if (fullB) load_quad<WF, GF>(qb, d, eB);
+    if (fullA && fullB) {
+      // Both sub-tiles whole (every tile but a tensor's last): loads grouped
+      // by array, so a wave's two requests to one array are adjacent spans.
+      qa.w.load(d.w, eA);
+      qb.w.load(d.w, eB);
+      qa.g = ld4g<GF>(d.g, eA);
+      qb.g = ld4g<GF>(d.g, eB);
+      qa.m = ld4s<SF>(d.m, eA);
+      qb.m = ld4s<SF>(d.m, eB);
+      qa.v = ld4s<SF>(d.v, eA);
+      qb.v = ld4s<SF>(d.v, eB);
+      qa.ve = ld4s<SF>(d.ve, eA);
+      qb.ve = ld4s<SF>(d.ve, eB);
+      uint32_t rA[4], rB[4];
+      draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+      step_quad<WF, SR, CLAMP>(qa, rA, s);
+      store_quad<WF, SF>(qa, d, eA);
+      step_quad<WF, SR, CLAMP>(qb, rB, s);
+      store_quad<WF, SF>(qb, d, eB);
+      continue;
+    }
+    if (fullA) load_quad<WF, GF, SF>(qa, d, eA);
+    if (fullB) load_quad<WF, GF, SF>(qb, d, eB);
     uint32_t rA[4], rB[4];
     draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
     if (fullA) {
       step_quad<WF, SR, CLAMP>(qa, rA, s);
-      store_quad<WF>(qa, d, eA);
+      store_quad<WF, SF>(qa, d, eA);
     } else if (eA < cend) {
-      step_scalar_range<WF, GF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+      step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
     }
     if (fullB) {
       step_quad<WF, SR, CLAMP>(qb, rB, s);
-      store_quad<WF>(qb, d, eB);
+      store_quad<WF, SF>(qb, d, eB);
     } else if (eB < cend) {
-      step_scalar_range<WF, GF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
+      step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
     }
   }
 }
@@ -570,7 +625,7 @@ __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[
   return sc;
 }
 
-template <int WF, int GF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP>
 __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
   const int64_t chunk = blockIdx.x;
@@ -586,8 +641,8 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     Quad<WF> qa, qb;
     float wa[4], wb[4];
     uint32_t amaxA = 0u, amaxB = 0u;
-    if (actA) load_quad<WF, GF>(qa, d, eA);
-    if (actB) load_quad<WF, GF>(qb, d, eB);
+    if (actA) load_quad<WF, GF, SF>(qa, d, eA);
+    if (actB) load_quad<WF, GF, SF>(qb, d, eB);
     uint32_t rA[4], rB[4];
     if (d.vec_ok) {  // uniform: index base a multiple of 8
       draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
@@ -601,12 +656,12 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     amaxB = block_amax32(amaxB);
     if (actA) {
       const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA);
-      store_quad<WF>(qa, d, eA);
+      store_quad<WF, SF>(qa, d, eA);
       if ((threadIdx.x & 31u) == 0u) d.scales[eA / kBlock] = (uint16_t)sc;
     }
     if (actB) {
       const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB);
-      store_quad<WF>(qb, d, eB);
+      store_quad<WF, SF>(qb, d, eB);
       if ((threadIdx.x & 31u) == 0u) d.scales[eB / kBlock] = (uint16_t)sc;
     }
   }
@@ -616,9 +671,10 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
 // Auxiliary kernels: zero state, encode weights
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kThreads) void zero_kernel(float* __restrict__ p, int64_t n) {
+template <typename T>
+__global__ __launch_bounds__(kThreads) void zero_kernel(T* __restrict__ p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * kThreads;
-  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) p[i] = 0.0f;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) p[i] = T(0);
 }
 
 template <int WF>
@@ -655,41 +711,42 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
 
 typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
 
-template <int WF, int GF, bool SR>
-step_fn pick_plain(bool clamp) {
-  return clamp ? madd_step_kernel<WF, GF, SR, true> : madd_step_kernel<WF, GF, SR, false>;
+template <int WF, int GF, int SF, bool SR>
+step_fn pick_clamp(bool clamp, bool blk) {
+  if constexpr (WF == WF_E4M3 || WF == WF_E5M2) {
+    if (blk)
+      return clamp ? madd_step_block_kernel<WF, GF, SF, SR, true>
+                   : madd_step_block_kernel<WF, GF, SF, SR, false>;
+  } else {
+    if (blk) return nullptr;  // block scaling exists for FP8 payloads only
+  }
+  return clamp ? madd_step_kernel<WF, GF, SF, SR, true> : madd_step_kernel<WF, GF, SF, SR, false>;
 }
-template <int WF, int GF, bool SR>
-step_fn pick_block(bool clamp) {
-  return clamp ? madd_step_block_kernel<WF, GF, SR, true> : madd_step_block_kernel<WF, GF, SR, false>;
+template <int WF, int GF, int SF>
+step_fn pick_sr(bool sr, bool clamp, bool blk) {
+  return sr ? pick_clamp<WF, GF, SF, true>(clamp, blk) : pick_clamp<WF, GF, SF, false>(clamp, blk);
 }
 template <int WF, int GF>
-step_fn pick_plain_sr(bool sr, bool clamp) {
-  return sr ? pick_plain<WF, GF, true>(clamp) : pick_plain<WF, GF, false>(clamp);
+step_fn pick_sf(int sf, bool sr, bool clamp, bool blk) {
+  return sf == SF_FP32 ? pick_sr<WF, GF, SF_FP32>(sr, clamp, blk)
+                       : pick_sr<WF, GF, SF_BF16>(sr, clamp, blk);
 }
-template <int WF, int GF>
-step_fn pick_fp8(bool sr, bool clamp, bool blk) {
-  if (blk) return sr ? pick_block<WF, GF, true>(clamp) : pick_block<WF, GF, false>(clamp);
-  return pick_plain_sr<WF, GF>(sr, clamp);
+template <int WF>
+step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool blk) {
+  return gf == GF_FP32 ? pick_sf<WF, GF_FP32>(sf, sr, clamp, blk)
+                       : pick_sf<WF, GF_BF16>(sf, sr, clamp, blk);
 }
 
-// Kernel instantiation for (weight format, gradient format, rounding, optional
-// clamps present, block-scaled); nullptr for combinations that do not exist.
-step_fn pick_kernel(int wf, int gf, bool sr, bool clamp, bool blk) {
-  const bool g32 = gf == GF_FP32;
+// Kernel instantiation for (weight, gradient and moment formats, rounding,
+// optional clamps present, block-scaled); nullptr for combinations that do
+// not exist.
+step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool blk) {
   switch (wf) {
-    case WF_BF16:
-      if (blk) return nullptr;
-      return g32 ? pick_plain_sr<WF_BF16, GF_FP32>(sr, clamp) : pick_plain_sr<WF_BF16, GF_BF16>(sr, clamp);
-    case WF_E4M3:
-      return g32 ? pick_fp8<WF_E4M3, GF_FP32>(sr, clamp, blk) : pick_fp8<WF_E4M3, GF_BF16>(sr, clamp, blk);
-    case WF_E5M2:
-      return g32 ? pick_fp8<WF_E5M2, GF_FP32>(sr, clamp, blk) : pick_fp8<WF_E5M2, GF_BF16>(sr, clamp, blk);
-    case WF_FP32:
-      if (blk) return nullptr;
-      return g32 ? pick_plain_sr<WF_FP32, GF_FP32>(sr, clamp) : pick_plain_sr<WF_FP32, GF_BF16>(sr, clamp);
-    default:
-      return nullptr;
+    case WF_BF16: return pick_gf<WF_BF16>(gf, sf, sr, clamp, blk);
+    case WF_E4M3: return pick_gf<WF_E4M3>(gf, sf, sr, clamp, blk);
+    case WF_E5M2: return pick_gf<WF_E5M2>(gf, sf, sr, clamp, blk);
+    case WF_FP32: return pick_gf<WF_FP32>(gf, sf, sr, clamp, blk);
+    default: return nullptr;
   }
 }
 
@@ -699,6 +756,7 @@ bool needs_clamp(const madd_hparams& hp) {
 
 bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_FP32; }
 bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
+bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16; }
 int wbytes(int32_t f) { return f == MADD_W_BF16 ? 2 : (f == MADD_W_FP32 ? 4 : 1); }
 int gbytes(int32_t f) { return f == MADD_G_FP32 ? 4 : 2; }
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -810,7 +868,7 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-TensorDesc make_desc(void* w, uint16_t* scales, const void* g, float* m, float* v, float* ve,
+TensorDesc make_desc(void* w, uint16_t* scales, const void* g, void* m, void* v, void* ve,
                      int64_t n, int64_t gbase) {
   TensorDesc d;
   memset(&d, 0, sizeof(d));
@@ -827,8 +885,8 @@ TensorDesc make_desc(void* w, uint16_t* scales, const void* g, float* m, float* 
   return d;
 }
 
-int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, const void* g, float* m, float* v,
-                     float* ve, int64_t n) {
+int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, const void* g, void* m, void* v,
+                     void* ve, int64_t n) {
   if (n < 0) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
@@ -861,16 +919,19 @@ const char* madd_status_string(int32_t status) {
   }
 }
 
-int32_t madd_init_state(float* m, float* v, float* ve, int64_t n, void* stream) {
-  if (n < 0) return MADD_EINVAL;
+int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, void* stream) {
+  if (n < 0 || !valid_sfmt(sfmt)) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!m || !v || !ve) return MADD_EINVAL;
   const int64_t want = (n + kThreads - 1) / kThreads;
   const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
   hipStream_t st = (hipStream_t)stream;
-  float* arr[3] = {m, v, ve};
-  for (float* p : arr) {
-    hipLaunchKernelGGL(zero_kernel, dim3(grid), dim3(kThreads), 0, st, p, n);
+  void* arr[3] = {m, v, ve};
+  for (void* p : arr) {
+    if (sfmt == MADD_S_FP32)
+      hipLaunchKernelGGL(zero_kernel<float>, dim3(grid), dim3(kThreads), 0, st, (float*)p, n);
+    else
+      hipLaunchKernelGGL(zero_kernel<uint16_t>, dim3(grid), dim3(kThreads), 0, st, (uint16_t*)p, n);
     if (hipGetLastError() != hipSuccess) return MADD_EDEVICE;
   }
   return MADD_OK;
@@ -907,18 +968,19 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, float* m,
-                  float* v, float* ve, int64_t n, int64_t index_base, const madd_hparams* hp,
-                  void* stream) {
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, void* m,
+                  void* v, void* ve, int32_t sfmt, int64_t n, int64_t index_base,
+                  const madd_hparams* hp, void* stream) {
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
-  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0) return MADD_EINVAL;
+  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
+    return MADD_EINVAL;
   rc = check_tensor(w, wfmt, scales, g, m, v, ve, n);
   if (rc != MADD_OK) return rc;
   if (n == 0) return MADD_OK;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
   const Scalars s = make_scalars(*hp);
-  step_fn fn = pick_kernel(wfmt, gfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
+  step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                            scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
   const TensorDesc d = make_desc(w, scales, g, m, v, ve, n, index_base);
@@ -927,12 +989,13 @@ int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
                                uint16_t* const* scales, const void* const* g, int32_t gfmt,
-                               float* const* m, float* const* v, float* const* ve,
+                               void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream) {
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
-  if (ntensors < 0 || !valid_gfmt(gfmt) || index_base < 0) return MADD_EINVAL;
+  if (ntensors < 0 || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
+    return MADD_EINVAL;
   if (ntensors == 0) return MADD_OK;
   if (!w || !wfmt || !g || !m || !v || !ve || !numel) return MADD_EINVAL;
   int64_t total = 0;
@@ -972,7 +1035,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
       }
       if (descs.empty()) continue;
       if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-      step_fn fn = pick_kernel(wf, gfmt, sr, needs_clamp(*hp), blk != 0);
+      step_fn fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), blk != 0);
       if (!fn) return MADD_EUNSUPPORTED;
       TensorDesc* table = nullptr;
       rc = get_table(descs, &table);

@@ -38,52 +38,64 @@ def ulp_dist(a: np.ndarray, b: np.ndarray) -> np.ndarray:
 
 def assert_state_equal(tag, w_gpu, w_ref, m_gpu, m_ref, v_gpu, v_ref, ve_gpu, ve_ref,
                        max_ulp=2):
-    """Weight codes bit-exact; fp32 moments within max_ulp (NaN where NaN)."""
+    """Weight codes bit-exact; fp32 moments within max_ulp (NaN where NaN);
+    bf16 moment codes bit-exact."""
     bad = np.nonzero(w_gpu != w_ref)[0]
     assert bad.size == 0, (f"{tag}: {bad.size} weight codes differ, first at {bad[:5]}: "
                            f"gpu {w_gpu[bad[:5]]} oracle {w_ref[bad[:5]]}")
     for name, a, b in (("m", m_gpu, m_ref), ("v", v_gpu, v_ref), ("ve", ve_gpu, ve_ref)):
+        if a.dtype == np.uint16:
+            nb = np.nonzero(a != b)[0]
+            assert nb.size == 0, f"{tag}: {name}: {nb.size} bf16 codes differ, first at {nb[:5]}"
+            continue
         assert (np.isnan(a) == np.isnan(b)).all(), f"{tag}: {name} NaN pattern differs"
         d = ulp_dist(a, b)
         assert d.max() <= max_ulp, f"{tag}: {name} max ulp {d.max()} at {np.argmax(d)}"
 
 
+STATE_T = {"fp32": torch.float32, "bf16": torch.int16}
+STATE_NP = {"fp32": np.float32, "bf16": np.uint16}
+
+
 class DevState:
     """Device copies of one tensor's weight codes and moments."""
 
-    def __init__(self, wfmt, codes, n, scales=None):
+    def __init__(self, wfmt, codes, n, scales=None, sfmt="fp32"):
         self.wfmt = wfmt
+        self.sfmt = sfmt
         self.w = to_dev(codes)
-        self.m = torch.zeros(n, dtype=torch.float32, device="cuda")
-        self.v = torch.zeros(n, dtype=torch.float32, device="cuda")
-        self.ve = torch.zeros(n, dtype=torch.float32, device="cuda")
+        self.m = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
+        self.v = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
+        self.ve = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
         self.scales = to_dev(scales) if scales is not None else None
 
     def host(self):
-        return (to_host(self.w, CODE_NP[self.wfmt]), to_host(self.m), to_host(self.v),
-                to_host(self.ve))
+        sn = STATE_NP[self.sfmt]
+        return (to_host(self.w, CODE_NP[self.wfmt]), to_host(self.m, sn), to_host(self.v, sn),
+                to_host(self.ve, sn))
 
 
 class HostState:
     """Oracle copies of one tensor's weight codes and moments."""
 
-    def __init__(self, codes, n, scales=None):
+    def __init__(self, codes, n, scales=None, sfmt="fp32"):
+        self.sfmt = sfmt
         self.w = codes.copy()
-        self.m = np.zeros(n, np.float32)
-        self.v = np.zeros(n, np.float32)
-        self.ve = np.zeros(n, np.float32)
+        self.m = np.zeros(n, STATE_NP[sfmt])
+        self.v = np.zeros(n, STATE_NP[sfmt])
+        self.ve = np.zeros(n, STATE_NP[sfmt])
         self.scales = scales.copy() if scales is not None else None
 
 
 def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
     if hs.scales is not None:
         oracle.step_block(wfmt, hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
-                          index_base=index_base, gidx=gidx)
+                          index_base=index_base, gidx=gidx, sfmt=hs.sfmt)
     else:
         oracle.step(wfmt, hs.w, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt, index_base=index_base,
-                    gidx=gidx)
+                    gidx=gidx, sfmt=hs.sfmt)
 
 
 def gpu_step(ds: DevState, g_dev, hp, gfmt="fp32", index_base=0):
     B.madd_step(ds.w, ds.wfmt, g_dev, ds.m, ds.v, ds.ve, hp, gfmt=gfmt, scales=ds.scales,
-                index_base=index_base)
+                index_base=index_base, sfmt=ds.sfmt)

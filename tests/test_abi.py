@@ -55,7 +55,8 @@ FAKE = 0x10000  # never dereferenced: every call below fails validation first
 def test_step_rejects_bad_hparams(kw):
     lib = B.lib()
     ref, _h = _hp(**kw)
-    rc = lib.madd_step(FAKE, B.W_BF16, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 1024, 0, ref, None)
+    rc = lib.madd_step(FAKE, B.W_BF16, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 0, 1024, 0, ref,
+                       None)
     assert rc == -1
 
 
@@ -63,17 +64,18 @@ def test_step_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
     call = lambda *a: lib.madd_step(*a, ref, None)  # noqa: E731
-    assert lib.madd_step(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0, None, None) == -1
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, -1, 0) == -1          # n < 0
-    assert call(None, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0) == -1           # null w
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 8, 0) == -1           # null v
-    assert call(FAKE, 9, None, FAKE, 0, FAKE, FAKE, FAKE, 8, 0) == -1           # bad wfmt
-    assert call(FAKE, 0, None, FAKE, 5, FAKE, FAKE, FAKE, 8, 0) == -1           # bad gfmt
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 8, -3) == -1          # base < 0
-    assert call(FAKE, 0, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 128, 0) == -1         # scales + bf16
-    assert call(FAKE, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 100, 0) == -1         # n % 128
-    assert call(FAKE + 4, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 128, 0) == -2     # unaligned
-    assert call(None, 0, None, None, 0, None, None, None, 0, 0) == 0            # empty: no-op
+    assert lib.madd_step(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0, None, None) == -1
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, -1, 0) == -1          # n < 0
+    assert call(None, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # null w
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 0, 8, 0) == -1           # null v
+    assert call(FAKE, 9, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad wfmt
+    assert call(FAKE, 0, None, FAKE, 5, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad gfmt
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 2, 8, 0) == -1           # bad sfmt
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, -3) == -1          # base < 0
+    assert call(FAKE, 0, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0) == -1         # scales + bf16
+    assert call(FAKE, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 100, 0) == -1         # n % 128
+    assert call(FAKE + 4, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0) == -2     # unaligned
+    assert call(None, 0, None, None, 0, None, None, None, 0, 0, 0) == 0            # empty: no-op
 
 
 def test_multi_tensor_rejects_bad_arguments():
@@ -85,25 +87,27 @@ def test_multi_tensor_rejects_bad_arguments():
     ne = (ctypes.c_int64 * 2)(128, 256)
     ok_ptrs = [arr(FAKE, FAKE) for _ in range(5)]
     w, g, m, v, ve = ok_ptrs
-    assert lib.madd_multi_tensor_step(0, None, None, None, None, 0, None, None, None, None, 0, ref,
-                                      None) == 0
-    assert lib.madd_multi_tensor_step(-1, w, fm, None, g, 0, m, v, ve, ne, 0, ref, None) == -1
-    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, v, ve, ne, 0, None, None) == -1
+    mt = lib.madd_multi_tensor_step
+    assert mt(0, None, None, None, None, 0, None, None, None, 0, None, 0, ref, None) == 0
+    assert mt(-1, w, fm, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, None, g, 0, m, v, ve, 0, ne, 0, None, None) == -1
+    assert mt(2, w, fm, None, g, 0, m, v, ve, 3, ne, 0, ref, None) == -1      # bad sfmt
     bad = arr(FAKE, None)
-    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, bad, ve, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, None, g, 0, m, bad, ve, 0, ne, 0, ref, None) == -1
     fm_bad = (ctypes.c_int32 * 2)(0, 11)
-    assert lib.madd_multi_tensor_step(2, w, fm_bad, None, g, 0, m, v, ve, ne, 0, ref, None) == -1
+    assert mt(2, w, fm_bad, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
     ne_bad = (ctypes.c_int64 * 2)(128, -5)
-    assert lib.madd_multi_tensor_step(2, w, fm, None, g, 0, m, v, ve, ne_bad, 0, ref, None) == -1
+    assert mt(2, w, fm, None, g, 0, m, v, ve, 0, ne_bad, 0, ref, None) == -1
     sc = arr(None, FAKE)  # second tensor block-scaled but bf16
-    assert lib.madd_multi_tensor_step(2, w, fm, sc, g, 0, m, v, ve, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, sc, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
 
 
 def test_init_and_encode_reject_bad_arguments():
     lib = B.lib()
-    assert lib.madd_init_state(FAKE, FAKE, FAKE, -1, None) == -1
-    assert lib.madd_init_state(None, FAKE, FAKE, 5, None) == -1
-    assert lib.madd_init_state(None, None, None, 0, None) == 0
+    assert lib.madd_init_state(FAKE, FAKE, FAKE, 0, -1, None) == -1
+    assert lib.madd_init_state(None, FAKE, FAKE, 0, 5, None) == -1
+    assert lib.madd_init_state(FAKE, FAKE, FAKE, 4, 5, None) == -1   # bad sfmt
+    assert lib.madd_init_state(None, None, None, 1, 0, None) == 0
     assert lib.madd_encode_weights(FAKE, FAKE, 7, None, 8, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, 0, FAKE, 128, None) == -1   # scales + bf16
     assert lib.madd_encode_weights(FAKE, FAKE, 1, FAKE, 130, None) == -1   # n % 128

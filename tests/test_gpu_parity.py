@@ -79,13 +79,13 @@ def encode_both(wfmt, x, block=False):
     return ref
 
 
-def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False):
+def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False, sfmt="fp32"):
     rng = np.random.default_rng(seed)
     x = random_weights(rng, n, wfmt)
     enc = encode_both(wfmt, x, block)
     codes, scales = (enc if block else (enc, None))
-    ds = DevState(wfmt, codes, n, scales)
-    hs = HostState(codes, n, scales)
+    ds = DevState(wfmt, codes, n, scales, sfmt=sfmt)
+    hs = HostState(codes, n, scales, sfmt=sfmt)
     for t in range(1, steps + 1):
         g = random_grad(rng, n)
         if gfmt == "bf16":
@@ -150,6 +150,21 @@ def test_block_scaled_fp8(wfmt, rounding):
 
 def test_bf16_gradients():
     run_pair("bf16", 20000, 3, 41, dict(rounding="sr"), gfmt="bf16")
+
+
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "fp32"])
+@pytest.mark.parametrize("n", [9, 2049, 3 * 8192 + 24])
+def test_bf16_moments(wfmt, n):
+    run_pair(wfmt, n, 4, 43 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16", index_base=16)
+
+
+def test_bf16_moments_bf16_gradients_misaligned_base():
+    run_pair("bf16", 10000, 3, 44, dict(rounding="sr"), gfmt="bf16", sfmt="bf16", index_base=5)
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+def test_block_scaled_fp8_bf16_moments(wfmt):
+    run_pair(wfmt, 3 * 8192 + 5 * 128, 3, 45, dict(rounding="sr"), block=True, sfmt="bf16")
 
 
 @pytest.mark.parametrize("kw", [dict(g_max=0.5), dict(d_mult_max=0.05), dict(w_max=0.03),
@@ -245,10 +260,13 @@ def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
 
 def test_init_state_zeroes():
     n = 70001
-    ts = [torch.full((n,), 3.0, device="cuda") for _ in range(3)]
-    B.madd_init_state(*ts)
+    ts = [torch.full((n + 1,), 3.0, device="cuda") for _ in range(3)]
+    B.madd_init_state(*[t[:n] for t in ts])
+    hs = [torch.full((n + 1,), 7, dtype=torch.int16, device="cuda") for _ in range(3)]
+    B.madd_init_state(*[t[:n] for t in hs])
     torch.cuda.synchronize()
-    assert all(float(t.abs().max()) == 0.0 for t in ts)
+    assert all(float(t[:n].abs().max()) == 0.0 and float(t[n]) == 3.0 for t in ts)
+    assert all(int(t[:n].abs().max()) == 0 and int(t[n]) == 7 for t in hs)
 
 
 def test_encode_weights_all_formats():
@@ -273,7 +291,7 @@ def sample_indices(n, rng, k=4096):
     return np.concatenate([head, mid, tail])
 
 
-def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096):
+def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096, sfmt="fp32"):
     """Whole list on the GPU with one multi-tensor call per step (the benchmark
     launch); the oracle follows sampled elements of every tensor."""
     specs = W.specs(cfg)
@@ -293,12 +311,13 @@ def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096):
         assert (to_host(w[idx_t], CODE_NP[wfmt]) == codes_ref).all(), f"encode {s.name}"
         del x
         ws.append(w)
-        ms.append(torch.zeros(s.numel, device="cuda"))
-        vs.append(torch.zeros(s.numel, device="cuda"))
-        ves.append(torch.zeros(s.numel, device="cuda"))
+        st = torch.float32 if sfmt == "fp32" else torch.int16
+        ms.append(torch.zeros(s.numel, dtype=st, device="cuda"))
+        vs.append(torch.zeros(s.numel, dtype=st, device="cuda"))
+        ves.append(torch.zeros(s.numel, dtype=st, device="cuda"))
         gs.append(torch.empty(s.numel, device="cuda"))
         samples.append((idx, idx_t))
-        hosts.append(HostState(codes_ref, idx.size))
+        hosts.append(HostState(codes_ref, idx.size, sfmt=sfmt))
     tl = B.TensorList(ws, [wfmt] * len(ws), gs, ms, vs, ves)
     for t in range(1, steps + 1):
         for i in range(len(specs)):
@@ -310,12 +329,13 @@ def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096):
             oracle_step(wfmt, hosts[i], g_s, h, gidx=idx + offsets[i])
         if t == steps or t % 5 == 0:
             torch.cuda.synchronize()
+            sn = np.float32 if sfmt == "fp32" else np.uint16
             for i, (idx, idx_t) in enumerate(samples):
                 hs = hosts[i]
                 assert_state_equal(f"{cfg} {specs[i].name} t={t}",
                                    to_host(ws[i][idx_t], CODE_NP[wfmt]), hs.w,
-                                   to_host(ms[i][idx_t]), hs.m, to_host(vs[i][idx_t]), hs.v,
-                                   to_host(ves[i][idx_t]), hs.ve)
+                                   to_host(ms[i][idx_t], sn), hs.m, to_host(vs[i][idx_t], sn),
+                                   hs.v, to_host(ves[i][idx_t], sn), hs.ve)
     return offsets[-1]
 
 
@@ -332,8 +352,19 @@ def test_config4_llama_1b_fp8_sampled(wfmt):
     assert run_list_sampled("c4", 10, wfmt=wfmt) == 1_100_048_384
 
 
+def test_config3_llama_1b_bf16_moments_sampled():
+    assert run_list_sampled("c3", 5, sfmt="bf16") == 1_100_048_384
+
+
 def test_config5_llama_7b_sampled():
     free, _ = torch.cuda.mem_get_info()
     need = 6_738_415_616 * 18 + (1 << 30)
     assert free > need, f"config 5 needs {need / 2**30:.0f} GiB of device memory"
     assert run_list_sampled("c5", 3, per_tensor=2048) == 6_738_415_616
+
+
+def test_config5_llama_7b_bf16_moments_sampled():
+    free, _ = torch.cuda.mem_get_info()
+    need = 6_738_415_616 * 12 + (1 << 30)
+    assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
+    assert run_list_sampled("c5", 2, per_tensor=1024, sfmt="bf16") == 6_738_415_616

@@ -47,6 +47,8 @@ MUTANTS = {
     "eps0 sign": ("double ulo = -(h->r_max - h->eps0)", "double ulo = -(h->r_max + h->eps0)"),
     "block scale constant": ("const float ratio = (float)amax / fp8_max(fmt);",
                              "const float ratio = (float)amax / 256.0f;"),
+    "bf16 moments truncated": ("else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);",
+                               "else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, 0u);"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }

@@ -395,3 +395,32 @@ def test_validation():
                 dict(eps0=0.75), dict(g_max=0.0)):
         with pytest.raises(oracle.OracleError):
             oracle.step("bf16", w, g, m, v, ve, hp(**bad))
+
+
+# --------------------------------------------------------------------------
+# moments stored in bf16
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3"])
+def test_bf16_moments_are_fp32_step_then_nearest_rounding(wfmt):
+    # With bf16 moments a step is the fp32-moment step on the decoded moments,
+    # the new moments then rounded to bf16 by the library conversion.
+    rng = np.random.default_rng(8)
+    n = 5000
+    codes = oracle.encode_array(wfmt, rng.normal(0, 0.02, n).astype(np.float32))
+    to_bf16 = lambda x: torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(  # noqa: E731
+        torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    ms = [to_bf16(rng.normal(0, s, n)) for s in (1e-3, 1e-6, 1e-6)]
+    ms[1] = to_bf16(np.abs(oracle.decode_array("bf16", ms[1])))
+    ms[2] = to_bf16(np.abs(oracle.decode_array("bf16", ms[2])))
+    for t in range(1, 4):
+        g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-5, -2, n)).astype(np.float32)
+        h = hp(step=t, rounding="sr", seed=3)
+        w32, c32 = codes.copy(), codes.copy()
+        f32 = [oracle.decode_array("bf16", a).astype(np.float32) for a in ms]
+        oracle.step(wfmt, c32, g, *f32, h)
+        oracle.step(wfmt, codes, g, *ms, h, sfmt="bf16")
+        assert (codes == c32).all()
+        for a, b in zip(ms, f32):
+            assert (a == to_bf16(b)).all()
+        del w32
