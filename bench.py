@@ -107,6 +107,10 @@ def main():
     ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--states", default="fp32", choices=["fp32", "bf16"],
                     help="storage of m, v, v_e (bf16: the paper's optimizer-state precision)")
+    ap.add_argument("--weights", default="list", choices=["list", "fp8-master"],
+                    help="list: the configuration's weight format for every tensor; fp8-master: "
+                         "linear layers block-scaled E4M3 with bf16 compute copies, embeddings, "
+                         "norms and head bf16 (the paper's FP8-master setting)")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
     ap.add_argument("--cpu-steps", type=int, default=None,
                     help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
@@ -154,7 +158,33 @@ def main():
             off += n
         return buf, views
 
-    wbuf, ws = flat(code_dt)
+    if args.weights == "fp8-master":
+        plan = W.fp8_master_plan(cfg)
+    else:
+        plan = [(wfmt, False, False)] * len(specs)
+
+    def flat_subset(dtype, pick, per_elem=1):
+        """One buffer for the tensors selected by pick, views (None elsewhere)."""
+        tot = sum(n // per_elem for n, p in zip(sizes, plan) if pick(p))
+        buf = torch.empty(max(tot, 1), dtype=dtype, device=dev)
+        views, off = [], 0
+        for n, p in zip(sizes, plan):
+            if pick(p):
+                views.append(buf[off:off + n // per_elem])
+                off += n // per_elem
+            else:
+                views.append(None)
+        return buf, views
+
+    if args.weights == "list":
+        wbuf, ws = flat(code_dt)
+        scales = copies = None
+    else:
+        wb16, w16 = flat_subset(torch.int16, lambda p: p[0] == "bf16")
+        wb8, w8 = flat_subset(torch.uint8, lambda p: p[0] != "bf16")
+        ws = [a if a is not None else b for a, b in zip(w16, w8)]
+        sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
+        cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
     gbufs, grad_sets = [], []
     gb, gl = flat(torch.float32)
     gbufs.append(gb)
@@ -168,7 +198,7 @@ def main():
     grad_sets.append(gl)
     for i in range(len(specs)):
         x = W.init_fp32_device(cfg, i, dev)
-        B.madd_encode_weights(x, ws[i], wfmt)
+        B.madd_encode_weights(x, ws[i], plan[i][0], scales=scales[i] if scales else None)
         del x
         B.madd_init_state(ms[i], vs[i], ves[i])
         for k in range(2):
@@ -177,7 +207,8 @@ def main():
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
         f"{time.perf_counter() - t0:.1f} s")
 
-    lists = [B.TensorList(ws, [wfmt] * len(ws), gl, ms, vs, ves) for gl in grad_sets]
+    lists = [B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
+                          copies=copies) for gl in grad_sets]
     stream = torch.cuda.current_stream()
     step_no = 0
 
@@ -217,15 +248,21 @@ def main():
         log(f"copy probe: {nbytes} bytes read + {nbytes} bytes written")
         del src, dst
 
-    bpp = bytes_per_param(wfmt, args.states)
-    alg_bytes = nparam * bpp
+    alg_bytes = 0
+    for n, (wf, blk, cp) in zip(sizes, plan):
+        alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
+        alg_bytes += (n // 128) * 4 if blk else 0  # FP16 scale read + written
+    bpp = alg_bytes / nparam
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
-    traffic = traffic_from_profile() if (cfg == "c5" and args.states == "fp32") else None
+    traffic = (traffic_from_profile()
+               if (cfg == "c5" and args.states == "fp32" and args.weights == "list") else None)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": alg_bytes,
-                "kernel": f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
-                          f"{W.CONFIGS[cfg]['rounding'].upper()}>",
+                "kernel": (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
+                           f"{W.CONFIGS[cfg]['rounding'].upper()}>" if args.weights == "list" else
+                           "madd_step_block_kernel<e4m3> + madd_step_kernel<bf16> (two launches "
+                           "per step; timed together)"),
                 "avg_launch_ms": round(avg_launch_ms, 4)}
 
     cpu = None
@@ -248,9 +285,11 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[cfg], "params": nparam, "tensors": len(specs),
-                   "weight_format": wfmt, "grad_format": "fp32",
+                   "weight_format": wfmt if args.weights == "list" else
+                   "e4m3 block-scaled linear layers + bf16 compute copies; bf16 embed/norms/head",
+                   "grad_format": "fp32",
                    "state": f"{args.states} m, v, v_e",
-                   "rounding": W.CONFIGS[cfg]["rounding"], "bytes_per_param": bpp},
+                   "rounding": W.CONFIGS[cfg]["rounding"], "bytes_per_param": round(bpp, 4)},
         "hbm_gbps": round(alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,

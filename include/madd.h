@@ -145,6 +145,12 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
 /* One M+Adam step on one tensor of n elements (Algorithm 1 with the optional
  * clamps of Algorithm 2).
  * w       : device weight codes of format wfmt, updated in place.
+ * copy    : NULL, or a device array of n bf16 codes that receives the compute
+ *           copy of the new weights: each new stored value (payload x scale
+ *           when block-scaled) rounded to nearest-even -- the BF16 copy the
+ *           next step's GEMMs read, refreshed by dequantization after every
+ *           update in the paper's FP8-master dataflow (Appendix figure), here
+ *           written by the same pass.  16-byte aligned for the fast path.
  * scales  : NULL, or block-scaled FP8 as in madd_encode_weights: the weight
  *           is payload * scale (fp32 product); after the update each block's
  *           scale is recomputed from the new weights by the same rule and the
@@ -160,23 +166,28 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
  *           any split of the index space (sharding).
  * Unaligned unscaled buffers are accepted and take a slower path with
  * identical results. */
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, void* m,
-                  void* v, void* ve, int32_t sfmt, int64_t n, int64_t index_base,
-                  const madd_hparams* hp, void* stream);
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+                  int32_t gfmt, void* m, void* v, void* ve, int32_t sfmt, int64_t n,
+                  int64_t index_base, const madd_hparams* hp, void* stream);
 
 /* One M+Adam step on a list of tensors in as few launches as the formats
  * allow (one per distinct (format, scaled) pair).
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
  * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
  * block-scaled) or a host array whose entry i is NULL or tensor i's scale
- * array.  Tensor i's elements have global
+ * array; copy: NULL (no compute copies) or a host array whose entry i is NULL
+ * or tensor i's bf16 compute-copy array (as in madd_step).  Tensors of
+ * different weight formats may be mixed -- e.g. block-scaled FP8 linear
+ * layers with BF16 embeddings, norms and head, the paper's FP8-master
+ * setting (Section 4.2).  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
  * The first call with a given list (same pointers and sizes) uploads a device
  * descriptor table (80 bytes per tensor) with a synchronous copy and caches it
  * (up to 32 lists per process; evicting one drains the device first).  Later
  * calls with the same list enqueue only the kernels. */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
-                               uint16_t* const* scales, const void* const* g, int32_t gfmt,
+                               uint16_t* const* scales, uint16_t* const* copy,
+                               const void* const* g, int32_t gfmt,
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream);

@@ -76,9 +76,9 @@ def lib():
         U64 = ctypes.c_uint64
         U32 = ctypes.c_uint32
         hp_args = [D] * 11 + [I, I, U64, I64]
-        L.oracle_step.argtypes = [I, P, I, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step.argtypes = [I, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step.restype = I
-        L.oracle_step_block.argtypes = [I, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_block.argtypes = [I, P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step_block.restype = I
         L.oracle_encode_array.argtypes = [I, P, P, I64]
         L.oracle_encode_array.restype = I
@@ -125,13 +125,19 @@ def _check_state(n, g, m, v, ve, gfmt, sfmt):
             raise OracleError(f"{name}: expected {n} x {np.dtype(dt)}, got {a.size} x {a.dtype}")
 
 
+def _check_copy(copy, n):
+    if copy is not None and (copy.dtype != np.uint16 or copy.size != n):
+        raise OracleError("copy must hold one uint16 bf16 code per element")
+
+
 def step(wfmt: str, w: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, ve: np.ndarray,
          hp: dict, gfmt: str = "fp32", index_base: int = 0, gidx: np.ndarray | None = None,
-         sfmt: str = "fp32"):
+         sfmt: str = "fp32", copy: np.ndarray | None = None):
     """One M+Adam step in place on host arrays (w codes, g, m, v, ve).
 
     ``sfmt`` is the storage of the moments: "fp32" (float32 arrays) or
-    "bf16" (uint16 codes).
+    "bf16" (uint16 codes).  ``copy`` (uint16, optional) receives the bf16
+    compute copy of the new stored weights.
 
     ``gidx`` (int64, one per element) gives each element's global index for the
     stochastic-rounding draw; without it element i has index ``index_base + i``.
@@ -143,15 +149,18 @@ def step(wfmt: str, w: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, 
     if gidx is not None:
         gidx = np.ascontiguousarray(gidx, dtype=np.int64)
         assert gidx.size == n
-    rc = lib().oracle_step(FMT[wfmt], _ptr(w), GFMT[gfmt], _ptr(g), SFMT[sfmt], _ptr(m), _ptr(v),
-                           _ptr(ve), n, _ptr(gidx), int(index_base), *_hp_args(hp))
+    _check_copy(copy, n)
+    rc = lib().oracle_step(FMT[wfmt], _ptr(w), _ptr(copy), GFMT[gfmt], _ptr(g), SFMT[sfmt],
+                           _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx), int(index_base),
+                           *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step returned {rc}")
 
 
 def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray,
                v: np.ndarray, ve: np.ndarray, hp: dict, gfmt: str = "fp32", index_base: int = 0,
-               gidx: np.ndarray | None = None, sfmt: str = "fp32"):
+               gidx: np.ndarray | None = None, sfmt: str = "fp32",
+               copy: np.ndarray | None = None):
     """Block-scaled FP8 step (blocks of 128 contiguous elements, FP16 scales)."""
     n = q.size
     if q.dtype != np.uint8 or scales.dtype != np.uint16 or scales.size * 128 != n:
@@ -160,8 +169,9 @@ def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: n
     if gidx is not None:
         gidx = np.ascontiguousarray(gidx, dtype=np.int64)
         assert gidx.size == n
-    rc = lib().oracle_step_block(FMT[wfmt], _ptr(q), _ptr(scales), GFMT[gfmt], _ptr(g),
-                                 SFMT[sfmt], _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
+    _check_copy(copy, n)
+    rc = lib().oracle_step_block(FMT[wfmt], _ptr(q), _ptr(scales), _ptr(copy), GFMT[gfmt],
+                                 _ptr(g), SFMT[sfmt], _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
                                  int(index_base), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_block returned {rc}")

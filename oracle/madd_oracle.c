@@ -57,6 +57,10 @@
  *     meaningful, so it is dropped).
  *   - FP32 "storage" (test passthrough) keeps the float bits; a NaN is stored
  *     as 0x7FC00000.
+ *   - Compute copy (optional): after the update, the BF16 value of each stored
+ *     weight (payload x scale for block-scaled FP8), rounded to nearest-even,
+ *     for the GEMMs of the next step (the FP8-master dataflow figure refreshes
+ *     a BF16 compute copy by dequantization each step).
  *   - Moments m, v, v_e are stored in fp32, or in bf16 (the precision of the
  *     optimizer states in the paper's memory accounting table).  With bf16
  *     storage the step decodes them exactly, computes in fp32 as above, uses
@@ -462,11 +466,16 @@ static int fill_hp(ohp *h, double lr_add, double lr_mul, double beta1, double be
   return check_hp(h);
 }
 
+/* The BF16 compute copy of a stored weight value: the value the forward and
+ * backward GEMMs read, refreshed from the master storage after each update
+ * (the FP8-master dataflow figure), rounded to nearest-even. */
+static uint16_t compute_copy(float stored) { return (uint16_t)encode(OF_BF16, stored, OR_RNE, 0u); }
+
 /* Per-element M+Adam step on an unscaled storage format.
  * Element i has global index gidx[i] (or index_base + i when gidx is NULL),
  * which keys its stochastic-rounding draw. */
-int oracle_step(int wfmt, void *w, int gfmt, const void *g, int sfmt, void *m, void *v, void *ve,
-                int64_t n, const int64_t *gidx, int64_t index_base, double lr_add, double lr_mul,
+int oracle_step(int wfmt, void *w, uint16_t *copy, int gfmt, const void *g, int sfmt, void *m,
+                void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base, double lr_add, double lr_mul,
                 double beta1, double beta2, double eps, double tau, double r_max, double eps0,
                 double g_max, double d_mult_max, double w_max, int bias_correction, int rounding,
                 uint64_t seed, int64_t step) {
@@ -487,7 +496,9 @@ int oracle_step(int wfmt, void *w, int gfmt, const void *g, int sfmt, void *m, v
     const float wn = step_stored(wv, gv, sfmt, m, v, ve, i, &s);
     const int64_t idx = gidx ? gidx[i] : index_base + i;
     const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
-    store_code(wfmt, w, i, encode(wfmt, wn, h.rounding, r16));
+    const uint32_t code = encode(wfmt, wn, h.rounding, r16);
+    store_code(wfmt, w, i, code);
+    if (copy) copy[i] = compute_copy((float)decode(wfmt, code));
   }
   return ORACLE_OK;
 }
@@ -515,8 +526,8 @@ static uint16_t block_scale(int fmt, const float *wn) {
 
 /* Block-scaled FP8 M+Adam step.  n must be a multiple of 128; elements
  * [128 b, 128 b + 128) form block b with scale scales[b]. */
-int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const void *g, int sfmt,
-                      void *m, void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base,
+int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, uint16_t *copy, int gfmt,
+                      const void *g, int sfmt, void *m, void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base,
                       double lr_add, double lr_mul, double beta1, double beta2, double eps,
                       double tau, double r_max, double eps0, double g_max, double d_mult_max,
                       double w_max, int bias_correction, int rounding, uint64_t seed,
@@ -548,6 +559,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, int gfmt, const vo
       const int64_t idx = gidx ? gidx[i] : index_base + i;
       const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
       q[i] = (uint8_t)encode(wfmt, wn[k] / sf, h.rounding, r16);
+      if (copy) copy[i] = compute_copy((float)decode(wfmt, q[i]) * sf);
     }
     scales[b] = snew;
   }

@@ -103,11 +103,11 @@ def lib():
         L.madd_init_state.restype = I32
         L.madd_encode_weights.argtypes = [P, P, I32, P, I64, P]
         L.madd_encode_weights.restype = I32
-        L.madd_step.argtypes = [P, I32, P, P, I32, P, P, P, I32, I64, I64, HP, P]
+        L.madd_step.argtypes = [P, I32, P, P, P, I32, P, P, P, I32, I64, I64, HP, P]
         L.madd_step.restype = I32
         PP = ctypes.POINTER(ctypes.c_void_p)
-        L.madd_multi_tensor_step.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, I32, PP, PP, PP,
-                                             I32, ctypes.POINTER(I64), I64, HP, P]
+        L.madd_multi_tensor_step.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, PP, I32, PP, PP,
+                                             PP, I32, ctypes.POINTER(I64), I64, HP, P]
         L.madd_multi_tensor_step.restype = I32
         L.madd_status_string.argtypes = [I32]
         L.madd_status_string.restype = ctypes.c_char_p
@@ -170,23 +170,25 @@ def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
 
 
 def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, index_base: int = 0,
-              n: int | None = None, sfmt: str | None = None, stream=None):
+              n: int | None = None, sfmt: str | None = None, copy=None, stream=None):
     """One step on one tensor.  ``w`` holds the weight codes (uint16 / uint8 /
     int32 storage for bf16 / fp8 / fp32); the moments' storage follows their
-    dtype unless ``sfmt`` is given."""
+    dtype unless ``sfmt`` is given; ``copy`` (16-bit tensor) receives the
+    bf16 compute copy of the new weights."""
     h = _hp(hp)
     n = m.numel() if n is None else n
     sfmt = sfmt or state_format(m)
     _check("madd_step",
-           lib().madd_step(_ptr(w), WFMT[wfmt], _ptr(scales), _ptr(g), GFMT[gfmt], _ptr(m), _ptr(v),
-                           _ptr(ve), SFMT[sfmt], int(n), int(index_base), ctypes.byref(h),
-                           _stream(stream)))
+           lib().madd_step(_ptr(w), WFMT[wfmt], _ptr(scales), _ptr(copy), _ptr(g), GFMT[gfmt],
+                           _ptr(m), _ptr(v), _ptr(ve), SFMT[sfmt], int(n), int(index_base),
+                           ctypes.byref(h), _stream(stream)))
 
 
 class TensorList:
     """Marshalled pointer arrays of a tensor list, built once and reused."""
 
-    def __init__(self, ws, wfmts, gs, ms, vs, ves, scales=None, sfmt: str | None = None):
+    def __init__(self, ws, wfmts, gs, ms, vs, ves, scales=None, sfmt: str | None = None,
+                 copies=None):
         k = len(ws)
         self.sfmt = sfmt or (state_format(ms[0]) if k else "fp32")
         assert all(len(x) == k for x in (wfmts, gs, ms, vs, ves))
@@ -198,6 +200,7 @@ class TensorList:
         self.v = Arr(*[_ptr(t) for t in vs])
         self.ve = Arr(*[_ptr(t) for t in ves])
         self.scales = Arr(*[_ptr(t) for t in scales]) if scales is not None else None
+        self.copy = Arr(*[_ptr(t) for t in copies]) if copies is not None else None
         self.wfmt = (ctypes.c_int32 * k)(*[WFMT[f] if isinstance(f, str) else int(f)
                                            for f in wfmts])
         self.numel = (ctypes.c_int64 * k)(*[t.numel() for t in ms])
@@ -215,7 +218,7 @@ def madd_multi_tensor_step(tl: TensorList, hp, gfmt: str = "fp32", index_base: i
     PP = ctypes.POINTER(ctypes.c_void_p)
     cast = lambda a: ctypes.cast(a, PP) if a is not None else None  # noqa: E731
     _check("madd_multi_tensor_step",
-           lib().madd_multi_tensor_step(tl.n, cast(tl.w), tl.wfmt, cast(tl.scales), cast(tl.g),
-                                        GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve),
+           lib().madd_multi_tensor_step(tl.n, cast(tl.w), tl.wfmt, cast(tl.scales), cast(tl.copy),
+                                        cast(tl.g), GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve),
                                         SFMT[tl.sfmt], tl.numel, int(index_base),
                                         ctypes.byref(h), _stream(stream)))

@@ -75,6 +75,7 @@ struct TensorDesc {
   void* v;
   void* ve;
   uint16_t* scales;
+  uint16_t* copy;  // optional bf16 compute copy of the new weights
   int64_t n;       // elements
   int64_t gbase;   // global index of element 0
   int64_t chunk0;  // first chunk of this tensor within the launch
@@ -426,6 +427,17 @@ __device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& 
   st4s<SF>(d.ve, e, q.ve);
 }
 
+// The bf16 compute copy of four new stored weights (value x scale for
+// block-scaled FP8), rounded to nearest-even.
+template <int WF>
+__device__ __forceinline__ void store_copy(const WQuad<WF>& w, float scale, uint16_t* copy,
+                                           int64_t e) {
+  uint32_t c[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) c[k] = enc_bf16(decode<WF>(w.code(k)) * scale, false, 0u);
+  stg<u2>(copy + e, u2{c[0] | (c[1] << 16), c[2] | (c[3] << 16)});
+}
+
 // Swap a value with the neighbouring lane (DPP quad_perm [1,0,3,2]).
 __device__ __forceinline__ uint32_t swap_lane_pair(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);
@@ -508,7 +520,7 @@ __device__ __forceinline__ TensorDesc find_tensor(const TensorDesc* __restrict__
 }
 
 // Elements [b, e) one at a time (tails and unaligned buffers).
-template <int WF, int GF, int SF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b, int64_t e,
                                                   const Scalars& s) {
   for (int64_t i = b; i < e; ++i) {
@@ -517,14 +529,16 @@ __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b
     const float g = ld1g<GF>(d.g, i);
     const float wn = step_elem<CLAMP>(w, g, m, v, ve, s);
     const uint32_t r16 = SR ? draw_one((uint64_t)(d.gbase + i), s) : 0u;
-    st1w<WF>(d.w, i, encode<WF>(wn, SR, r16));
+    const uint32_t code = encode<WF>(wn, SR, r16);
+    st1w<WF>(d.w, i, code);
+    if (COPY && d.copy) d.copy[i] = (uint16_t)enc_bf16(decode<WF>(code), false, 0u);
     st1s<SF>(d.m, i, m);
     st1s<SF>(d.v, i, v);
     st1s<SF>(d.ve, i, ve);
   }
 }
 
-template <int WF, int GF, int SF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* __restrict__ table,
                                                              int ntab, TensorDesc single,
                                                              Scalars s) {
@@ -538,8 +552,8 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
     if (tb >= cend) break;  // uniform
     const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
     if (!d.vec_ok) {  // uniform: unaligned buffers or index base
-      if (eA < cend) step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
-      if (eB < cend) step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
+      if (eA < cend) step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+      if (eB < cend) step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
       continue;
     }
     const bool fullA = eA + kQuad <= cend, fullB = eB + kQuad <= cend;
@@ -561,8 +575,10 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
       draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
       step_quad<WF, SR, CLAMP>(qa, rA, s);
       store_quad<WF, SF>(qa, d, eA);
+      if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
       step_quad<WF, SR, CLAMP>(qb, rB, s);
       store_quad<WF, SF>(qb, d, eB);
+      if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
       continue;
     }
     if (fullA) load_quad<WF, GF, SF>(qa, d, eA);
@@ -572,14 +588,16 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
     if (fullA) {
       step_quad<WF, SR, CLAMP>(qa, rA, s);
       store_quad<WF, SF>(qa, d, eA);
+      if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
     } else if (eA < cend) {
-      step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
+      step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
     }
     if (fullB) {
       step_quad<WF, SR, CLAMP>(qb, rB, s);
       store_quad<WF, SF>(qb, d, eB);
+      if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
     } else if (eB < cend) {
-      step_scalar_range<WF, GF, SF, SR, CLAMP>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
+      step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
     }
   }
 }
@@ -625,7 +643,7 @@ __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[
   return sc;
 }
 
-template <int WF, int GF, int SF, bool SR, bool CLAMP>
+template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
   const int64_t chunk = blockIdx.x;
@@ -657,11 +675,13 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     if (actA) {
       const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA);
       store_quad<WF, SF>(qa, d, eA);
+      if (COPY && d.copy) store_copy<WF>(qa.w, dec_fp16(sc), d.copy, eA);
       if ((threadIdx.x & 31u) == 0u) d.scales[eA / kBlock] = (uint16_t)sc;
     }
     if (actB) {
       const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB);
       store_quad<WF, SF>(qb, d, eB);
+      if (COPY && d.copy) store_copy<WF>(qb.w, dec_fp16(sc), d.copy, eB);
       if ((threadIdx.x & 31u) == 0u) d.scales[eB / kBlock] = (uint16_t)sc;
     }
   }
@@ -711,41 +731,48 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
 
 typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
 
-template <int WF, int GF, int SF, bool SR>
-step_fn pick_clamp(bool clamp, bool blk) {
+template <int WF, int GF, int SF, bool SR, bool CLAMP>
+step_fn pick_copy(bool copy, bool blk) {
   if constexpr (WF == WF_E4M3 || WF == WF_E5M2) {
     if (blk)
-      return clamp ? madd_step_block_kernel<WF, GF, SF, SR, true>
-                   : madd_step_block_kernel<WF, GF, SF, SR, false>;
+      return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
+                  : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
   } else {
     if (blk) return nullptr;  // block scaling exists for FP8 payloads only
   }
-  return clamp ? madd_step_kernel<WF, GF, SF, SR, true> : madd_step_kernel<WF, GF, SF, SR, false>;
+  return copy ? madd_step_kernel<WF, GF, SF, SR, CLAMP, true>
+              : madd_step_kernel<WF, GF, SF, SR, CLAMP, false>;
+}
+template <int WF, int GF, int SF, bool SR>
+step_fn pick_clamp(bool clamp, bool copy, bool blk) {
+  return clamp ? pick_copy<WF, GF, SF, SR, true>(copy, blk)
+               : pick_copy<WF, GF, SF, SR, false>(copy, blk);
 }
 template <int WF, int GF, int SF>
-step_fn pick_sr(bool sr, bool clamp, bool blk) {
-  return sr ? pick_clamp<WF, GF, SF, true>(clamp, blk) : pick_clamp<WF, GF, SF, false>(clamp, blk);
+step_fn pick_sr(bool sr, bool clamp, bool copy, bool blk) {
+  return sr ? pick_clamp<WF, GF, SF, true>(clamp, copy, blk)
+            : pick_clamp<WF, GF, SF, false>(clamp, copy, blk);
 }
 template <int WF, int GF>
-step_fn pick_sf(int sf, bool sr, bool clamp, bool blk) {
-  return sf == SF_FP32 ? pick_sr<WF, GF, SF_FP32>(sr, clamp, blk)
-                       : pick_sr<WF, GF, SF_BF16>(sr, clamp, blk);
+step_fn pick_sf(int sf, bool sr, bool clamp, bool copy, bool blk) {
+  return sf == SF_FP32 ? pick_sr<WF, GF, SF_FP32>(sr, clamp, copy, blk)
+                       : pick_sr<WF, GF, SF_BF16>(sr, clamp, copy, blk);
 }
 template <int WF>
-step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool blk) {
-  return gf == GF_FP32 ? pick_sf<WF, GF_FP32>(sf, sr, clamp, blk)
-                       : pick_sf<WF, GF_BF16>(sf, sr, clamp, blk);
+step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
+  return gf == GF_FP32 ? pick_sf<WF, GF_FP32>(sf, sr, clamp, copy, blk)
+                       : pick_sf<WF, GF_BF16>(sf, sr, clamp, copy, blk);
 }
 
 // Kernel instantiation for (weight, gradient and moment formats, rounding,
-// optional clamps present, block-scaled); nullptr for combinations that do
-// not exist.
-step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool blk) {
+// optional clamps present, compute copies present, block-scaled); nullptr for
+// combinations that do not exist.
+step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
   switch (wf) {
-    case WF_BF16: return pick_gf<WF_BF16>(gf, sf, sr, clamp, blk);
-    case WF_E4M3: return pick_gf<WF_E4M3>(gf, sf, sr, clamp, blk);
-    case WF_E5M2: return pick_gf<WF_E5M2>(gf, sf, sr, clamp, blk);
-    case WF_FP32: return pick_gf<WF_FP32>(gf, sf, sr, clamp, blk);
+    case WF_BF16: return pick_gf<WF_BF16>(gf, sf, sr, clamp, copy, blk);
+    case WF_E4M3: return pick_gf<WF_E4M3>(gf, sf, sr, clamp, copy, blk);
+    case WF_E5M2: return pick_gf<WF_E5M2>(gf, sf, sr, clamp, copy, blk);
+    case WF_FP32: return pick_gf<WF_FP32>(gf, sf, sr, clamp, copy, blk);
     default: return nullptr;
   }
 }
@@ -868,8 +895,8 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-TensorDesc make_desc(void* w, uint16_t* scales, const void* g, void* m, void* v, void* ve,
-                     int64_t n, int64_t gbase) {
+TensorDesc make_desc(void* w, uint16_t* scales, uint16_t* copy, const void* g, void* m, void* v,
+                     void* ve, int64_t n, int64_t gbase) {
   TensorDesc d;
   memset(&d, 0, sizeof(d));
   d.w = w;
@@ -878,15 +905,17 @@ TensorDesc make_desc(void* w, uint16_t* scales, const void* g, void* m, void* v,
   d.v = v;
   d.ve = ve;
   d.scales = scales;
+  d.copy = copy;
   d.n = n;
   d.gbase = gbase;
   d.chunk0 = 0;
-  d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (gbase & 7) == 0;
+  d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy)) &&
+             (gbase & 7) == 0;
   return d;
 }
 
-int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, const void* g, void* m, void* v,
-                     void* ve, int64_t n) {
+int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+                     void* m, void* v, void* ve, int64_t n) {
   if (n < 0) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
@@ -894,7 +923,8 @@ int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, const void* g, voi
   if (scales) {
     if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
     if (n % kBlock != 0) return MADD_EINVAL;
-    if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve))) return MADD_EALIGN;
+    if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy))))
+      return MADD_EALIGN;
   }
   return MADD_OK;
 }
@@ -968,27 +998,28 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, const void* g, int32_t gfmt, void* m,
-                  void* v, void* ve, int32_t sfmt, int64_t n, int64_t index_base,
-                  const madd_hparams* hp, void* stream) {
+int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+                  int32_t gfmt, void* m, void* v, void* ve, int32_t sfmt, int64_t n,
+                  int64_t index_base, const madd_hparams* hp, void* stream) {
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
   if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
     return MADD_EINVAL;
-  rc = check_tensor(w, wfmt, scales, g, m, v, ve, n);
+  rc = check_tensor(w, wfmt, scales, copy, g, m, v, ve, n);
   if (rc != MADD_OK) return rc;
   if (n == 0) return MADD_OK;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
   const Scalars s = make_scalars(*hp);
   step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
-                           scales != nullptr);
+                           copy != nullptr, scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
-  const TensorDesc d = make_desc(w, scales, g, m, v, ve, n, index_base);
+  const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
   return launch(fn, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
 }
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
-                               uint16_t* const* scales, const void* const* g, int32_t gfmt,
+                               uint16_t* const* scales, uint16_t* const* copy,
+                               const void* const* g, int32_t gfmt,
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream) {
@@ -1001,8 +1032,8 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
   int64_t total = 0;
   for (int32_t i = 0; i < ntensors; ++i) {
     if (!valid_wfmt(wfmt[i])) return MADD_EINVAL;
-    rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, g[i], m[i], v[i], ve[i],
-                      numel[i]);
+    rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, copy ? copy[i] : nullptr, g[i],
+                      m[i], v[i], ve[i], numel[i]);
     if (rc != MADD_OK) return rc;
     if (numel[i] > INT64_MAX - index_base - total) return MADD_EINVAL;
     total += numel[i];
@@ -1025,8 +1056,8 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
       for (int32_t i = 0; i < ntensors; ++i) {
         const bool is_blk = scales && scales[i];
         if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
-          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, g[i], m[i], v[i], ve[i],
-                                   numel[i], gbase);
+          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, copy ? copy[i] : nullptr,
+                                   g[i], m[i], v[i], ve[i], numel[i], gbase);
           d.chunk0 = nch;
           nch += chunks_of(numel[i]);
           descs.push_back(d);
@@ -1035,7 +1066,9 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
       }
       if (descs.empty()) continue;
       if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-      step_fn fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), blk != 0);
+      bool any_copy = false;
+      for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
+      step_fn fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
       if (!fn) return MADD_EUNSUPPORTED;
       TensorDesc* table = nullptr;
       rc = get_table(descs, &table);

@@ -206,3 +206,15 @@ def grad_fp32_device_(cfg: str, i: int, step: int, out, sigma: float | None = No
         out.mul_(torch.where(u > 0.999, 100.0, 1.0))
         del u
     return out
+
+
+def fp8_master_plan(cfg: str):
+    """Per-tensor storage for the FP8-master setting of Section 4.2: attention
+    and MLP linear weights as block-scaled E4M3 (FP16 scale per 128 elements)
+    with a bf16 compute copy; embeddings, norms and the LM head in bf16.
+    Returns (weight format, block-scaled, compute copy) per tensor."""
+    plan = []
+    for s in specs(cfg):
+        linear = s.kind == "matrix" and s.name not in ("embed", "lm_head", "wte", "wpe")
+        plan.append(("e4m3", True, True) if linear else ("bf16", False, False))
+    return plan

@@ -60,10 +60,11 @@ STATE_NP = {"fp32": np.float32, "bf16": np.uint16}
 class DevState:
     """Device copies of one tensor's weight codes and moments."""
 
-    def __init__(self, wfmt, codes, n, scales=None, sfmt="fp32"):
+    def __init__(self, wfmt, codes, n, scales=None, sfmt="fp32", copy=False):
         self.wfmt = wfmt
         self.sfmt = sfmt
         self.w = to_dev(codes)
+        self.copy = torch.full((n,), 0x1234, dtype=torch.int16, device="cuda") if copy else None
         self.m = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
         self.v = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
         self.ve = torch.zeros(n, dtype=STATE_T[sfmt], device="cuda")
@@ -78,9 +79,10 @@ class DevState:
 class HostState:
     """Oracle copies of one tensor's weight codes and moments."""
 
-    def __init__(self, codes, n, scales=None, sfmt="fp32"):
+    def __init__(self, codes, n, scales=None, sfmt="fp32", copy=False):
         self.sfmt = sfmt
         self.w = codes.copy()
+        self.copy = np.full(n, 0x1234, np.uint16) if copy else None
         self.m = np.zeros(n, STATE_NP[sfmt])
         self.v = np.zeros(n, STATE_NP[sfmt])
         self.ve = np.zeros(n, STATE_NP[sfmt])
@@ -90,12 +92,20 @@ class HostState:
 def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
     if hs.scales is not None:
         oracle.step_block(wfmt, hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
-                          index_base=index_base, gidx=gidx, sfmt=hs.sfmt)
+                          index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
     else:
         oracle.step(wfmt, hs.w, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt, index_base=index_base,
-                    gidx=gidx, sfmt=hs.sfmt)
+                    gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
 
 
 def gpu_step(ds: DevState, g_dev, hp, gfmt="fp32", index_base=0):
     B.madd_step(ds.w, ds.wfmt, g_dev, ds.m, ds.v, ds.ve, hp, gfmt=gfmt, scales=ds.scales,
-                index_base=index_base, sfmt=ds.sfmt)
+                index_base=index_base, sfmt=ds.sfmt, copy=ds.copy)
+
+
+def assert_copy_equal(tag, ds: DevState, hs: HostState):
+    if hs.copy is None:
+        return
+    got = to_host(ds.copy, np.uint16)
+    bad = np.nonzero(got != hs.copy)[0]
+    assert bad.size == 0, f"{tag}: {bad.size} compute-copy codes differ, first at {bad[:5]}"

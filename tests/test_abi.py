@@ -55,16 +55,19 @@ FAKE = 0x10000  # never dereferenced: every call below fails validation first
 def test_step_rejects_bad_hparams(kw):
     lib = B.lib()
     ref, _h = _hp(**kw)
-    rc = lib.madd_step(FAKE, B.W_BF16, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 0, 1024, 0, ref,
-                       None)
+    rc = lib.madd_step(FAKE, B.W_BF16, None, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 0, 1024, 0,
+                       ref, None)
     assert rc == -1
 
 
 def test_step_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
-    call = lambda *a: lib.madd_step(*a, ref, None)  # noqa: E731
-    assert lib.madd_step(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0, None, None) == -1
+    call = lambda w, wf, sc, *a: lib.madd_step(w, wf, sc, None, *a, ref, None)  # noqa: E731
+    assert lib.madd_step(FAKE, 0, None, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0, None,
+                         None) == -1
+    assert lib.madd_step(FAKE, 1, FAKE, FAKE + 8, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0, ref,
+                         None) == -2  # block-scaled with an unaligned copy
     assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, -1, 0) == -1          # n < 0
     assert call(None, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # null w
     assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 0, 8, 0) == -1           # null v
@@ -88,18 +91,18 @@ def test_multi_tensor_rejects_bad_arguments():
     ok_ptrs = [arr(FAKE, FAKE) for _ in range(5)]
     w, g, m, v, ve = ok_ptrs
     mt = lib.madd_multi_tensor_step
-    assert mt(0, None, None, None, None, 0, None, None, None, 0, None, 0, ref, None) == 0
-    assert mt(-1, w, fm, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
-    assert mt(2, w, fm, None, g, 0, m, v, ve, 0, ne, 0, None, None) == -1
-    assert mt(2, w, fm, None, g, 0, m, v, ve, 3, ne, 0, ref, None) == -1      # bad sfmt
+    assert mt(0, None, None, None, None, None, 0, None, None, None, 0, None, 0, ref, None) == 0
+    assert mt(-1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, None, None) == -1
+    assert mt(2, w, fm, None, None, g, 0, m, v, ve, 3, ne, 0, ref, None) == -1      # bad sfmt
     bad = arr(FAKE, None)
-    assert mt(2, w, fm, None, g, 0, m, bad, ve, 0, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, None, None, g, 0, m, bad, ve, 0, ne, 0, ref, None) == -1
     fm_bad = (ctypes.c_int32 * 2)(0, 11)
-    assert mt(2, w, fm_bad, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
+    assert mt(2, w, fm_bad, None, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
     ne_bad = (ctypes.c_int64 * 2)(128, -5)
-    assert mt(2, w, fm, None, g, 0, m, v, ve, 0, ne_bad, 0, ref, None) == -1
+    assert mt(2, w, fm, None, None, g, 0, m, v, ve, 0, ne_bad, 0, ref, None) == -1
     sc = arr(None, FAKE)  # second tensor block-scaled but bf16
-    assert mt(2, w, fm, sc, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
+    assert mt(2, w, fm, sc, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
 
 
 def test_init_and_encode_reject_bad_arguments():

@@ -16,8 +16,8 @@ import torch
 import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
-from gpu_parity_util import (CODE_NP, DevState, HostState, assert_state_equal, gpu_step,
-                             oracle_step, to_dev, to_host)
+from gpu_parity_util import (CODE_NP, DevState, HostState, assert_copy_equal, assert_state_equal,
+                             gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -79,13 +79,14 @@ def encode_both(wfmt, x, block=False):
     return ref
 
 
-def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False, sfmt="fp32"):
+def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False, sfmt="fp32",
+             copy=False):
     rng = np.random.default_rng(seed)
     x = random_weights(rng, n, wfmt)
     enc = encode_both(wfmt, x, block)
     codes, scales = (enc if block else (enc, None))
-    ds = DevState(wfmt, codes, n, scales, sfmt=sfmt)
-    hs = HostState(codes, n, scales, sfmt=sfmt)
+    ds = DevState(wfmt, codes, n, scales, sfmt=sfmt, copy=copy)
+    hs = HostState(codes, n, scales, sfmt=sfmt, copy=copy)
     for t in range(1, steps + 1):
         g = random_grad(rng, n)
         if gfmt == "bf16":
@@ -96,6 +97,7 @@ def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False,
         torch.cuda.synchronize()
         w_g, m_g, v_g, ve_g = ds.host()
         assert_state_equal(f"{wfmt} n={n} t={t}", w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+        assert_copy_equal(f"{wfmt} n={n} t={t}", ds, hs)
         if block:
             assert (to_host(ds.scales, np.uint16) == hs.scales).all(), f"scales t={t}"
 
@@ -156,6 +158,19 @@ def test_bf16_gradients():
 @pytest.mark.parametrize("n", [9, 2049, 3 * 8192 + 24])
 def test_bf16_moments(wfmt, n):
     run_pair(wfmt, n, 4, 43 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16", index_base=16)
+
+
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "e5m2", "fp32"])
+@pytest.mark.parametrize("n", [13, 2048 + 4, 2 * 8192 + 40])
+def test_compute_copy(wfmt, n):
+    run_pair(wfmt, n, 3, 46 + n, dict(rounding="sr"), copy=True, index_base=8 * (n % 3) + n % 2)
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+@pytest.mark.parametrize("sfmt", ["fp32", "bf16"])
+def test_block_scaled_compute_copy(wfmt, sfmt):
+    run_pair(wfmt, 2 * 8192 + 7 * 128, 3, 47, dict(rounding="sr"), block=True, copy=True,
+             sfmt=sfmt)
 
 
 def test_bf16_moments_bf16_gradients_misaligned_base():
@@ -227,9 +242,10 @@ def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
                                                     np.zeros(0, np.uint16)) if blk else
                                                    np.zeros(0, CODE_NP[wfmt]))
         codes, scales = (enc if blk else (enc, None))
-        devs.append(DevState(wfmt, codes, n, scales))
-        singles.append(DevState(wfmt, codes, n, scales))
-        hosts.append(HostState(codes, n, scales))
+        cp = wfmt in ("e4m3", "e5m2")  # compute copies for the FP8 tensors
+        devs.append(DevState(wfmt, codes, n, scales, copy=cp))
+        singles.append(DevState(wfmt, codes, n, scales, copy=cp))
+        hosts.append(HostState(codes, n, scales, copy=cp))
     base = 1000
     for t in range(1, 4):
         gs = [random_grad(rng, n) for _, n, _ in layout]
@@ -237,7 +253,7 @@ def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
         h = hp(step=t, rounding="sr", seed=314)
         tl = B.TensorList([d.w for d in devs], [d.wfmt for d in devs], gds, [d.m for d in devs],
                           [d.v for d in devs], [d.ve for d in devs],
-                          scales=[d.scales for d in devs])
+                          scales=[d.scales for d in devs], copies=[d.copy for d in devs])
         B.madd_multi_tensor_step(tl, h, index_base=base)
         off = base
         for (wfmt, n, blk), d1, hs, g, gd in zip(layout, singles, hosts, gs, gds):
@@ -254,6 +270,7 @@ def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
                                ve_g, hs.ve)
             for a, b in zip(d.host(), d1.host()):
                 assert a.tobytes() == b.tobytes()
+            assert_copy_equal(f"multi {wfmt} n={n} t={t}", d, hs)
             if blk:
                 assert (to_host(d.scales, np.uint16) == hs.scales).all()
 
@@ -368,3 +385,71 @@ def test_config5_llama_7b_bf16_moments_sampled():
     need = 6_738_415_616 * 12 + (1 << 30)
     assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
     assert run_list_sampled("c5", 2, per_tensor=1024, sfmt="bf16") == 6_738_415_616
+
+
+# ---------------------------------------------------------------------------
+# the paper's FP8-master setting on the full 7B list, sampled
+# ---------------------------------------------------------------------------
+
+def test_fp8_master_llama7b_sampled():
+    """Attention and MLP linear weights block-scaled E4M3 with bf16 compute
+    copies, embeddings / norms / head in bf16 (Section 4.2), one multi-tensor
+    call per step; the oracle follows sampled whole 128-element blocks."""
+    cfg = "c5"
+    specs = W.specs(cfg)
+    plan = W.fp8_master_plan(cfg)
+    rng = np.random.default_rng(9)
+    offsets = np.cumsum([0] + [s.numel for s in specs])
+    dev = dict(w=[], sc=[], cp=[], m=[], v=[], ve=[], g=[])
+    samples, hosts = [], []
+    for i, (s, (wfmt, blk, cp)) in enumerate(zip(specs, plan)):
+        x = W.init_fp32_device(cfg, i)
+        w = torch.empty(s.numel, dtype=torch.uint8 if blk else torch.int16, device="cuda")
+        sc = torch.empty(s.numel // 128, dtype=torch.int16, device="cuda") if blk else None
+        B.madd_encode_weights(x, w, wfmt, scales=sc)
+        nb = s.numel // 128
+        bidx = np.unique(np.concatenate([np.arange(4), np.arange(nb - 4, nb),
+                                         rng.choice(nb, size=min(nb, 24), replace=False)]))
+        idx = (bidx[:, None] * 128 + np.arange(128)[None, :]).ravel()
+        idx_t = torch.from_numpy(idx).cuda()
+        x_s = to_host(x[idx_t])
+        if blk:
+            q_ref, s_ref = oracle.encode_block(wfmt, x_s)
+            assert (to_host(w[idx_t], np.uint8) == q_ref).all()
+            assert (to_host(sc[torch.from_numpy(bidx).cuda()], np.uint16) == s_ref).all()
+            hs = HostState(q_ref, idx.size, s_ref, copy=cp)
+        else:
+            codes = oracle.encode_array(wfmt, x_s)
+            assert (to_host(w[idx_t], np.uint16) == codes).all()
+            hs = HostState(codes, idx.size, copy=cp)
+        del x
+        dev["w"].append(w)
+        dev["sc"].append(sc)
+        dev["cp"].append(torch.zeros(s.numel, dtype=torch.int16, device="cuda") if cp else None)
+        for k in ("m", "v", "ve"):
+            dev[k].append(torch.zeros(s.numel, device="cuda"))
+        dev["g"].append(torch.empty(s.numel, device="cuda"))
+        samples.append((idx, idx_t, bidx))
+        hosts.append(hs)
+    tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
+                      scales=dev["sc"], copies=dev["cp"])
+    for t in (1, 2):
+        for i in range(len(specs)):
+            W.grad_fp32_device_(cfg, i, t, dev["g"][i])
+        h = W.hparams(cfg, step=t)
+        B.madd_multi_tensor_step(tl, h)
+        for i, (idx, idx_t, bidx) in enumerate(samples):
+            oracle_step(plan[i][0], hosts[i], to_host(dev["g"][i][idx_t]), h,
+                        gidx=idx + offsets[i])
+        torch.cuda.synchronize()
+        for i, (idx, idx_t, bidx) in enumerate(samples):
+            hs, (wfmt, blk, cp) = hosts[i], plan[i]
+            tag = f"fp8-master {specs[i].name} t={t}"
+            assert_state_equal(tag, to_host(dev["w"][i][idx_t], CODE_NP[wfmt]), hs.w,
+                               to_host(dev["m"][i][idx_t]), hs.m, to_host(dev["v"][i][idx_t]),
+                               hs.v, to_host(dev["ve"][i][idx_t]), hs.ve)
+            if blk:
+                got = to_host(dev["sc"][i][torch.from_numpy(bidx).cuda()], np.uint16)
+                assert (got == hs.scales).all(), tag
+            if cp:
+                assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag

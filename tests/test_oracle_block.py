@@ -120,3 +120,38 @@ def test_block_step_sr_lands_on_neighbours():
     above = grid[np.clip(i, 0, grid.size - 1)]
     ok = (got == below) | (got == above) | (got == lo)
     assert ok.all()
+
+
+# --------------------------------------------------------------------------
+# bf16 compute copy
+# --------------------------------------------------------------------------
+
+def _torch_bf16(x: np.ndarray) -> np.ndarray:
+    return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(torch.bfloat16).view(
+        torch.int16).numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "e5m2", "fp32"])
+def test_compute_copy_is_bf16_of_the_stored_weight(wfmt):
+    # The copy the GEMMs read is the new stored weight, dequantized and
+    # rounded to bf16 by the library conversion.
+    rng = np.random.default_rng(3)
+    n = 4096
+    codes = oracle.encode_array(wfmt, rng.normal(0, 0.3, n).astype(np.float32))
+    copy = np.zeros(n, np.uint16)
+    z = [np.zeros(n, np.float32) for _ in range(3)]
+    g = rng.normal(0, 1e-2, n).astype(np.float32)
+    oracle.step(wfmt, codes, g, *z, hp(rounding="sr", seed=1, lr_add=1e-2), copy=copy)
+    assert (copy == _torch_bf16(oracle.decode_array(wfmt, codes))).all()
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_block_compute_copy_is_bf16_of_payload_times_scale(fmt):
+    rng = np.random.default_rng(4)
+    n = 16 * 128
+    q, s = oracle.encode_block(fmt, rng.normal(0, 0.05, n).astype(np.float32))
+    copy = np.zeros(n, np.uint16)
+    z = [np.zeros(n, np.float32) for _ in range(3)]
+    g = rng.normal(0, 1e-3, n).astype(np.float32)
+    oracle.step_block(fmt, q, s, g, *z, hp(rounding="sr", seed=2), copy=copy)
+    assert (copy == _torch_bf16(dequant(fmt, q, s))).all()

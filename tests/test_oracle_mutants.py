@@ -49,6 +49,12 @@ MUTANTS = {
                              "const float ratio = (float)amax / 256.0f;"),
     "bf16 moments truncated": ("else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);",
                                "else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, 0u);"),
+    "compute copy of the unrounded weight": (
+        "    if (copy) copy[i] = compute_copy((float)decode(wfmt, code));",
+        "    if (copy) copy[i] = compute_copy(wn);"),
+    "block compute copy without the scale": (
+        "      if (copy) copy[i] = compute_copy((float)decode(wfmt, q[i]) * sf);",
+        "      if (copy) copy[i] = compute_copy((float)decode(wfmt, q[i]));"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }
