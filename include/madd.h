@@ -192,6 +192,20 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream);
 
+/* One step of the moment-free update rules of Appendix B's BF16-stored
+ * matrix-fitting diagnostic, on one tensor of n elements:
+ *   additive        u_a = -eta_a g
+ *   multiplicative  u_m = clip(-eta_m g_e / max(|w|, tau)),  g_e = ln2 w g,
+ *                   clip to [-(r_max - eps0), r_max] and the d_mult_max cap
+ *   combined        w <- clamp_{w_max}(w + w u_m + u_a), rounded into wfmt
+ * (eta_m = 0 gives the additive rule, eta_a = 0 the multiplicative one).
+ * No optimizer state.  w: device weight codes of format wfmt, in place;
+ * g: device gradient of format gfmt; index_base, rounding and seed as in
+ * madd_step; hp's beta1, beta2, eps, g_max and bias_correction are validated
+ * but unused.  Errors as in madd_step. */
+int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
+                        int64_t index_base, const madd_hparams* hp, void* stream);
+
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* madd_status_string(int32_t status);
 

@@ -80,6 +80,8 @@ def lib():
         L.oracle_step.restype = I
         L.oracle_step_block.argtypes = [I, P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step_block.restype = I
+        L.oracle_plain_step.argtypes = [I, P, I, P, I64, P, I64] + [D] * 7 + [I, U64, I64]
+        L.oracle_plain_step.restype = I
         L.oracle_encode_array.argtypes = [I, P, P, I64]
         L.oracle_encode_array.restype = I
         L.oracle_encode_block.argtypes = [I, P, P, P, I64]
@@ -175,6 +177,28 @@ def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: n
                                  int(index_base), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_block returned {rc}")
+
+
+def plain_step(wfmt: str, w: np.ndarray, g: np.ndarray, hp: dict, gfmt: str = "fp32",
+               index_base: int = 0, gidx: np.ndarray | None = None):
+    """Appendix B's moment-free rules in place on host weight codes: additive
+    (lr_mul = 0), multiplicative (lr_add = 0) or combined."""
+    n = w.size
+    if w.dtype != _CODE_DTYPE[wfmt]:
+        raise OracleError("w: wrong code dtype")
+    gd = np.float32 if gfmt == "fp32" else np.uint16
+    if g.dtype != gd or g.size != n:
+        raise OracleError("g: wrong dtype or size")
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+    rc = lib().oracle_plain_step(FMT[wfmt], _ptr(w), GFMT[gfmt], _ptr(g), n, _ptr(gidx),
+                                 int(index_base), float(hp["lr_add"]), float(hp["lr_mul"]),
+                                 float(hp["tau"]), float(hp["r_max"]), float(hp["eps0"]),
+                                 float(hp["d_mult_max"]), float(hp["w_max"]),
+                                 ROUND[hp["rounding"]], int(hp["seed"]) & (2**64 - 1),
+                                 int(hp["step"]))
+    if rc != 0:
+        raise OracleError(f"oracle_plain_step returned {rc}")
 
 
 def encode_array(fmt: str, x: np.ndarray) -> np.ndarray:

@@ -25,6 +25,11 @@
  *   weight clamp clamp_{w_max}(w).  Algorithm 2 is printed without bias
  *   correction; bias_correction = 0 reproduces it, 1 gives Algorithm 1.
  *
+ *   Appendix B (BF16-stored matrix fitting) also defines moment-free rules
+ *   used by its diagnostic (oracle_plain_step): additive -eta_a g,
+ *   multiplicative clip(-eta_m ln2 w g / max(|w|, tau), +-r_max), and their
+ *   sum, each followed by the round trip into the storage format.
+ *
  *   Appendix B (BF16-stored matrix fitting) fixes the precision: the step is
  *   computed in FP32 and the weight is rounded into the storage format before
  *   the next step.  This oracle generalises that round trip from BF16 to the
@@ -584,6 +589,52 @@ int oracle_encode_block(int fmt, const float *x, uint8_t *q, uint16_t *scales, i
     for (int k = 0; k < BLOCK; ++k)
       q[b * BLOCK + k] = (uint8_t)encode(fmt, x[b * BLOCK + k] / sf, OR_RNE, 0u);
     scales[b] = sc;
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The moment-free update rules of Appendix B                               */
+/* ------------------------------------------------------------------------ */
+
+/* One element of Appendix B's rules: additive u_a = -eta_a g; multiplicative
+ * g_e = ln2 w g, ut = -eta_m g_e, u_m = clip(ut / max(|w|, tau)); combined
+ * w + w u_m + u_a (eta_m = 0 gives the additive rule, eta_a = 0 the
+ * multiplicative one).  Same FP32 conventions as the M+Adam step. */
+static float plain_step_elem(float w, float g, float lra, const oscal *s) {
+  const float LN2 = (float)0.69314718055994530942;
+  const float ua = -(lra * g);
+  const float ge = (LN2 * w) * g;
+  const float ut = -(s->LRM * ge);
+  const float aw = fabsf(w);
+  const float rho = aw > s->TAU ? aw : s->TAU;
+  const float um = clampf(ut / rho, s->ULO, s->UHI);
+  const float wn = fmaf(w, um, w) + ua;
+  return clampf(wn, -s->WMAX, s->WMAX);
+}
+
+int oracle_plain_step(int wfmt, void *w, int gfmt, const void *g, int64_t n, const int64_t *gidx,
+                      int64_t index_base, double lr_add, double lr_mul, double tau, double r_max,
+                      double eps0, double d_mult_max, double w_max, int rounding, uint64_t seed,
+                      int64_t step) {
+  init_formats();
+  ohp h;
+  /* moment hyper-parameters are unused by these rules; fixed valid values */
+  if (fill_hp(&h, lr_add, lr_mul, 0.9, 0.999, 1e-8, tau, r_max, eps0, INFINITY, d_mult_max, w_max,
+              1, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (wfmt != OF_BF16 && wfmt != OF_E4M3 && wfmt != OF_E5M2 && wfmt != OF_FP32) return ORACLE_EINVAL;
+  if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (n < 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  const float lra = (float)lr_add;
+  for (int64_t i = 0; i < n; ++i) {
+    const float wv = (float)decode(wfmt, load_code(wfmt, w, i));
+    const float wn = plain_step_elem(wv, load_grad(gfmt, g, i), lra, &s);
+    const int64_t idx = gidx ? gidx[i] : index_base + i;
+    const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+    store_code(wfmt, w, i, encode(wfmt, wn, h.rounding, r16));
   }
   return ORACLE_OK;
 }

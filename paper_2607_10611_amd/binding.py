@@ -30,7 +30,7 @@ STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPO
           -4: "MADD_EDEVICE", -5: "MADD_ENOMEM"}
 
 EXPORTS = ("madd_init_state", "madd_encode_weights", "madd_step", "madd_multi_tensor_step",
-           "madd_status_string")
+           "madd_plain_step", "madd_status_string")
 
 
 class MaddError(RuntimeError):
@@ -109,6 +109,8 @@ def lib():
         L.madd_multi_tensor_step.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, PP, I32, PP, PP,
                                              PP, I32, ctypes.POINTER(I64), I64, HP, P]
         L.madd_multi_tensor_step.restype = I32
+        L.madd_plain_step.argtypes = [P, I32, P, I32, I64, I64, HP, P]
+        L.madd_plain_step.restype = I32
         L.madd_status_string.argtypes = [I32]
         L.madd_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -182,6 +184,15 @@ def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, in
            lib().madd_step(_ptr(w), WFMT[wfmt], _ptr(scales), _ptr(copy), _ptr(g), GFMT[gfmt],
                            _ptr(m), _ptr(v), _ptr(ve), SFMT[sfmt], int(n), int(index_base),
                            ctypes.byref(h), _stream(stream)))
+
+
+def madd_plain_step(w, wfmt: str, g, hp, gfmt: str = "fp32", index_base: int = 0, stream=None):
+    """One step of Appendix B's moment-free rules (additive: lr_mul = 0,
+    multiplicative: lr_add = 0, combined: both) on one tensor."""
+    h = _hp(hp)
+    _check("madd_plain_step",
+           lib().madd_plain_step(_ptr(w), WFMT[wfmt], _ptr(g), GFMT[gfmt], w.numel(),
+                                 int(index_base), ctypes.byref(h), _stream(stream)))
 
 
 class TensorList:

@@ -688,6 +688,51 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// The moment-free rules of Appendix B's diagnostic
+// ---------------------------------------------------------------------------
+
+// Additive u_a = -eta_a g; multiplicative ut = -eta_m g_e with g_e = ln2 w g,
+// u_m = clip(ut / max(|w|, tau)); combined w + w u_m + u_a.  Same FP32
+// conventions as step_elem.
+__device__ __forceinline__ float plain_elem(float w, float g, float lra, const Scalars& s) {
+  const float LN2 = 0.693147182464599609375f;
+  const float ua = -(lra * g);
+  const float ge = (LN2 * w) * g;
+  const float ut = -(s.LRM * ge);
+  const float aw = fabsf(w);
+  const float rho = aw > s.TAU ? aw : s.TAU;
+  const float um = clampf(ut / rho, s.ULO, s.UHI);
+  return clampf(fmaf(w, um, w) + ua, -s.WMAX, s.WMAX);
+}
+
+// Four consecutive elements per thread, grid-stride (diagnostic-sized work).
+template <int WF, int GF, bool SR>
+__global__ __launch_bounds__(kThreads) void madd_plain_kernel(void* w, const void* g, int64_t n,
+                                                              int64_t gbase, float lra,
+                                                              Scalars s) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads * kQuad;
+  for (int64_t e0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kQuad; e0 < n; e0 += stride) {
+    const int64_t e1 = e0 + kQuad < n ? e0 + kQuad : n;
+    for (int64_t i = e0; i < e1; ++i) {
+      const float wn = plain_elem(decode<WF>(ld1w<WF>(w, i)), ld1g<GF>(g, i), lra, s);
+      const uint32_t r16 = SR ? draw_one((uint64_t)(gbase + i), s) : 0u;
+      st1w<WF>(w, i, encode<WF>(wn, SR, r16));
+    }
+  }
+}
+
+typedef void (*plain_fn)(void*, const void*, int64_t, int64_t, float, Scalars);
+
+template <int WF, int GF>
+plain_fn pick_plain_sr(bool sr) {
+  return sr ? madd_plain_kernel<WF, GF, true> : madd_plain_kernel<WF, GF, false>;
+}
+template <int WF>
+plain_fn pick_plain_gf(int gf, bool sr) {
+  return gf == GF_FP32 ? pick_plain_sr<WF, GF_FP32>(sr) : pick_plain_sr<WF, GF_BF16>(sr);
+}
+
+// ---------------------------------------------------------------------------
 // Auxiliary kernels: zero state, encode weights
 // ---------------------------------------------------------------------------
 
@@ -1015,6 +1060,30 @@ int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const
   if (!fn) return MADD_EUNSUPPORTED;
   const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
   return launch(fn, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
+}
+
+int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
+                        int64_t index_base, const madd_hparams* hp, void* stream) {
+  int32_t rc = check_hparams(hp);
+  if (rc != MADD_OK) return rc;
+  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0 || n < 0) return MADD_EINVAL;
+  if (n == 0) return MADD_OK;
+  if (!w || !g) return MADD_EINVAL;
+  if (n > INT64_MAX - index_base) return MADD_EINVAL;
+  const Scalars s = make_scalars(*hp);
+  const bool sr = hp->rounding == MADD_ROUND_SR;
+  plain_fn fn = nullptr;
+  switch (wfmt) {
+    case MADD_W_BF16: fn = pick_plain_gf<WF_BF16>(gfmt, sr); break;
+    case MADD_W_FP8_E4M3: fn = pick_plain_gf<WF_E4M3>(gfmt, sr); break;
+    case MADD_W_FP8_E5M2: fn = pick_plain_gf<WF_E5M2>(gfmt, sr); break;
+    default: fn = pick_plain_gf<WF_FP32>(gfmt, sr); break;
+  }
+  const int64_t want = (n + (int64_t)kThreads * kQuad - 1) / ((int64_t)kThreads * kQuad);
+  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), 0, (hipStream_t)stream, w, g, n, index_base,
+                     (float)hp->lr_add, s);
+  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,

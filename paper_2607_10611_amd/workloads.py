@@ -218,3 +218,42 @@ def fp8_master_plan(cfg: str):
         linear = s.kind == "matrix" and s.name not in ("embed", "lm_head", "wte", "wpe")
         plan.append(("e4m3", True, True) if linear else ("bf16", False, False))
     return plan
+
+
+# ---------------------------------------------------------------------------
+# Appendix B's BF16-stored matrix-fitting diagnostic: five regimes
+# ---------------------------------------------------------------------------
+
+TOY_N = 4096
+TOY_REGIMES = ("sign_flip", "zero_revival", "small", "large", "mixed")
+
+
+def toy_regime(name: str, seed: int = 0):
+    """Targets w*, initial weights w0 and per-entry loss scales c of one regime
+    (n = 4096 entries), as fp32 arrays.
+
+    sign_flip: w* in {-1, +1}, w0 = -w*, c = 1; zero_revival: w* in {-1, +1},
+    w0 = 0, c = 1; small: w* = 1e-4 z, w0 = 0, c = 1e8; large:
+    w* = 900 max(|z|, 1/900), w0 = 100, c = 1e-7; mixed: first half small,
+    second half large (z ~ N(0, 1))."""
+    rng = np.random.default_rng(np.random.SeedSequence(ROOT_SEED, spawn_key=(6, 0, seed)))
+    n = TOY_N
+    z = rng.standard_normal(n)
+    if name == "sign_flip":
+        ws = rng.choice([-1.0, 1.0], n)
+        w0, c = -ws, np.ones(n)
+    elif name == "zero_revival":
+        ws = rng.choice([-1.0, 1.0], n)
+        w0, c = np.zeros(n), np.ones(n)
+    elif name == "small":
+        ws, w0, c = 1e-4 * z, np.zeros(n), np.full(n, 1e8)
+    elif name == "large":
+        ws, w0, c = 900.0 * np.maximum(np.abs(z), 1.0 / 900.0), np.full(n, 100.0), np.full(n, 1e-7)
+    elif name == "mixed":
+        h = n // 2
+        ws = np.concatenate([1e-4 * z[:h], 900.0 * np.maximum(np.abs(z[h:]), 1.0 / 900.0)])
+        w0 = np.concatenate([np.zeros(h), np.full(n - h, 100.0)])
+        c = np.concatenate([np.full(h, 1e8), np.full(n - h, 1e-7)])
+    else:
+        raise KeyError(name)
+    return ws.astype(np.float32), w0.astype(np.float32), c.astype(np.float32)

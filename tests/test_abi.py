@@ -105,6 +105,19 @@ def test_multi_tensor_rejects_bad_arguments():
     assert mt(2, w, fm, sc, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
 
 
+def test_plain_step_rejects_bad_arguments():
+    lib = B.lib()
+    ref, _h = _hp()
+    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, 8, 0, None, None) == -1        # no hparams
+    assert lib.madd_plain_step(FAKE, 6, FAKE, 0, 8, 0, ref, None) == -1         # bad wfmt
+    assert lib.madd_plain_step(FAKE, 0, FAKE, 3, 8, 0, ref, None) == -1         # bad gfmt
+    assert lib.madd_plain_step(FAKE, 0, None, 0, 8, 0, ref, None) == -1         # null g
+    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, -2, 0, ref, None) == -1        # n < 0
+    assert lib.madd_plain_step(None, 0, None, 0, 0, 0, ref, None) == 0          # empty
+    bad, _h2 = _hp(r_max=1.5)
+    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, 8, 0, bad, None) == -1
+
+
 def test_init_and_encode_reject_bad_arguments():
     lib = B.lib()
     assert lib.madd_init_state(FAKE, FAKE, FAKE, 0, -1, None) == -1

@@ -55,6 +55,9 @@ MUTANTS = {
     "block compute copy without the scale": (
         "      if (copy) copy[i] = compute_copy((float)decode(wfmt, q[i]) * sf);",
         "      if (copy) copy[i] = compute_copy((float)decode(wfmt, q[i]));"),
+    "plain additive sign": ("  const float ua = -(lra * g);", "  const float ua = (lra * g);"),
+    "plain multiplicative without rho": ("  const float um = clampf(ut / rho, s->ULO, s->UHI);\n  const float wn = fmaf(w, um, w) + ua;\n  return",
+                                         "  const float um = clampf(ut, s->ULO, s->UHI);\n  const float wn = fmaf(w, um, w) + ua;\n  return"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }

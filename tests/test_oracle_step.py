@@ -424,3 +424,68 @@ def test_bf16_moments_are_fp32_step_then_nearest_rounding(wfmt):
         for a, b in zip(ms, f32):
             assert (a == to_bf16(b)).all()
         del w32
+
+
+# --------------------------------------------------------------------------
+# Appendix B's moment-free rules
+# --------------------------------------------------------------------------
+
+def test_plain_additive_rule_is_sgd_then_bf16_rounding():
+    rng = np.random.default_rng(20)
+    n = 8192
+    codes = oracle.encode_array("bf16", rng.normal(0, 0.5, n).astype(np.float32))
+    g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-4, 1, n)).astype(np.float32)
+    w = oracle.decode_array("bf16", codes).astype(np.float32)
+    oracle.plain_step("bf16", codes, g, hp(lr_add=0.01, lr_mul=0.0))
+    want = w + (-(np.float32(0.01) * g))  # fp32, as the rule is written
+    ref = torch.from_numpy(want.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+    assert (codes == ref.numpy().view(np.uint16)).all()
+
+
+def test_plain_multiplicative_rule_closed_form():
+    # u_m = clip(-eta_m ln2 w g / |w|) = clip(-eta_m ln2 g sign(w)) for |w| > tau
+    rng = np.random.default_rng(21)
+    n = 4096
+    w = rng.normal(0, 1, n).astype(np.float32)
+    w[:5] = [0.0, 1e-9, -2.0, 50.0, -1e-3]
+    g = rng.normal(0, 2, n).astype(np.float32)
+    codes = w.view(np.uint32).copy()
+    oracle.plain_step("fp32", codes, g, hp(lr_add=0.0, lr_mul=0.3))
+    wn = codes.view(np.float32).astype(np.float64)
+    w64, g64 = w.astype(np.float64), g.astype(np.float64)
+    um = np.clip(-0.3 * LN2 * w64 * g64 / np.maximum(np.abs(w64), 1e-8), -0.75, 0.75)
+    want = w64 * (1 + um)
+    assert np.allclose(wn, want, rtol=4e-7, atol=0)
+    assert wn[0] == 0.0 and (np.sign(wn) == np.sign(w64)).all()
+
+
+def test_plain_rules_on_appendix_b_regimes():
+    # Section 3.1 / Appendix B: the multiplicative rule cannot change a sign
+    # or leave exact zero; the additive rule can; at large magnitudes an
+    # additive step below half the BF16 spacing is rounded away while the
+    # multiplicative step, relative to |w|, is not.
+    from paper_2607_10611_amd import diagnostic as D
+    from paper_2607_10611_amd import workloads as W
+
+    def run(regime, rule, lr, steps=60):
+        ws, w0, c = W.toy_regime(regime)
+        codes = oracle.encode_array("bf16", w0)
+        rng = np.random.default_rng(0)
+        for t in range(1, steps + 1):
+            w = oracle.decode_array("bf16", codes).astype(np.float32)
+            cnt = np.bincount(rng.integers(0, W.TOY_N, W.TOY_N), minlength=W.TOY_N)
+            g = D.toy_gradient(w, ws, c, cnt.astype(np.float32), W.TOY_N).astype(np.float32)
+            oracle.plain_step("bf16", codes, g, D.rule_hparams(rule, lr, t))
+        return oracle.decode_array("bf16", codes), ws, w0
+
+    w, ws, w0 = run("sign_flip", "multiplicative", 10.0)
+    assert (np.sign(w) == np.sign(w0)).all()
+    w, ws, w0 = run("sign_flip", "combined", 10.0)
+    assert np.mean(np.sign(w) == np.sign(ws)) > 0.99
+    w, ws, w0 = run("zero_revival", "multiplicative", 10.0)
+    assert (w == 0).all()
+    w, ws, w0 = run("zero_revival", "additive", 10.0)
+    assert (w != 0).all()
+    w, ws, w0 = run("large", "additive", 1.0)
+    wm, _, _ = run("large", "multiplicative", 1.0)
+    assert np.mean(w == w0) > 0.5 > np.mean(wm == w0)
