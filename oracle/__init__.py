@@ -16,6 +16,9 @@ What each function follows in the paper:
                        FP32-step / BF16-storage round trip of Appendix B.
   * ``step_block``  -- the same step on FP8 payloads with FP16 block scales
                        (Section 4.2, FP8 master-weight setting).
+  * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
+                       E8M0 scale per 32 elements; the format stands in for
+                       the 4-bit master weights of Section 4.2).
   * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
                        storage formats' value grids.
   * ``philox`` / ``draw16`` -- the counter-based generator that keys
@@ -39,7 +42,7 @@ _SRC = os.path.join(_HERE, "madd_oracle.c")
 _LIB = os.path.join(_HERE, "libmadd_oracle.so")
 
 # format / rounding numbering of the oracle's C interface
-FMT = {"bf16": 0, "e4m3": 1, "e5m2": 2, "fp32": 3, "fp16": 4}
+FMT = {"bf16": 0, "e4m3": 1, "e5m2": 2, "fp32": 3, "fp16": 4, "e2m1": 5, "e8m0": 6}
 GFMT = {"fp32": 0, "bf16": 1}
 SFMT = {"fp32": 0, "bf16": 1}
 ROUND = {"rne": 0, "sr": 1}
@@ -86,6 +89,10 @@ def lib():
         L.oracle_encode_array.restype = I
         L.oracle_encode_block.argtypes = [I, P, P, P, I64]
         L.oracle_encode_block.restype = I
+        L.oracle_step_mx.argtypes = [P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_mx.restype = I
+        L.oracle_encode_mx.argtypes = [P, P, P, I64]
+        L.oracle_encode_mx.restype = I
         L.oracle_decode.argtypes = [I, U32]
         L.oracle_decode.restype = D
         L.oracle_encode.argtypes = [I, ctypes.c_float, I, U32]
@@ -177,6 +184,52 @@ def step_block(wfmt: str, q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: n
                                  int(index_base), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_block returned {rc}")
+
+
+def step_mx(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray,
+            ve: np.ndarray, hp: dict, gfmt: str = "fp32", index_base: int = 0,
+            gidx: np.ndarray | None = None, sfmt: str = "fp32", copy: np.ndarray | None = None):
+    """MXFP4 step: ``q`` holds n/2 bytes (element 2k in the low nibble),
+    ``scales`` one E8M0 code per 32 elements."""
+    n = 2 * q.size
+    if q.dtype != np.uint8 or scales.dtype != np.uint8 or scales.size * 32 != n:
+        raise OracleError("q must be n/2 packed bytes and scales uint8, one per 32 elements")
+    _check_state(n, g, m, v, ve, gfmt, sfmt)
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+        assert gidx.size == n
+    _check_copy(copy, n)
+    rc = lib().oracle_step_mx(_ptr(q), _ptr(scales), _ptr(copy), GFMT[gfmt], _ptr(g), SFMT[sfmt],
+                              _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx), int(index_base),
+                              *_hp_args(hp))
+    if rc != 0:
+        raise OracleError(f"oracle_step_mx returned {rc}")
+
+
+def encode_mx(x: np.ndarray):
+    """MXFP4 encoding (nearest-even): packed payload bytes and E8M0 scales."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.zeros(x.size // 2, dtype=np.uint8)
+    s = np.zeros(x.size // 32, dtype=np.uint8)
+    if lib().oracle_encode_mx(_ptr(x), _ptr(q), _ptr(s), x.size) != 0:
+        raise OracleError("oracle_encode_mx failed")
+    return q, s
+
+
+def unpack_e2m1(q: np.ndarray) -> np.ndarray:
+    """Element codes (one per element) of packed MXFP4 payload bytes."""
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    out = np.empty(2 * q.size, dtype=np.uint8)
+    out[0::2] = q & 0xF
+    out[1::2] = q >> 4
+    return out
+
+
+def mx_values(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Stored MXFP4 weights as float64 (payload x scale)."""
+    el = decode_array("e2m1", unpack_e2m1(q))
+    sc = decode_array("e8m0", scales)
+    return (el.reshape(-1, 32) * sc[:, None]).ravel()
 
 
 def plain_step(wfmt: str, w: np.ndarray, g: np.ndarray, hp: dict, gfmt: str = "fp32",

@@ -78,6 +78,9 @@
  *     0, the largest finite FP16 when it overflows, and FP16 NaN when any w'
  *     of the block is not finite; q' = encode(w'/s') with the block's
  *     rounding mode.
+ *   - 4-bit storage (the NVFP4/FP8 setting of Section 4.2; the paper does not
+ *     define the format): the OCP MX block format MXFP4 -- 32-element blocks
+ *     of E2M1 values with one E8M0 power-of-two scale; rule at oracle_step_mx.
  *
  * Codec implementation: values are decoded from the (sign, exponent,
  * mantissa) definition of each format; encoding searches the sorted table of
@@ -89,7 +92,10 @@
 #include <stdlib.h>
 #include <string.h>
 
-enum { OF_BF16 = 0, OF_E4M3 = 1, OF_E5M2 = 2, OF_FP32 = 3, OF_FP16 = 4, OF_NFMT = 5 };
+/* OF_E2M1 is the 4-bit MXFP4 element format; OF_E8M0 the MX block scale
+ * (a power of two, not a sign/exponent/mantissa format: decoded separately). */
+enum { OF_BF16 = 0, OF_E4M3 = 1, OF_E5M2 = 2, OF_FP32 = 3, OF_FP16 = 4, OF_E2M1 = 5, OF_NFMT = 6,
+       OF_E8M0 = 6 };
 enum { OG_FP32 = 0, OG_BF16 = 1 };
 enum { OS_FP32 = 0, OS_BF16 = 1 }; /* storage of the moments m, v, v_e */
 enum { OR_RNE = 0, OR_SR = 1 };
@@ -105,7 +111,8 @@ enum {
 
 typedef struct {
   int ebits, mbits, bias;
-  int ieee_special; /* all-ones exponent field: Inf (mantissa 0) or NaN        */
+  int specials;     /* SPEC_IEEE: all-ones exponent = Inf / NaN; SPEC_E4M3: only
+                       S.1111.111 is NaN; SPEC_NONE: every code is finite      */
   int satfinite;    /* finite overflow and Inf saturate to +-max                */
   uint32_t nan_code;
   uint32_t inf_code;
@@ -118,6 +125,8 @@ typedef struct {
   double beyond; /* next grid point above max if the exponent were unbounded */
 } ofmt;
 
+enum { SPEC_E4M3 = 0, SPEC_IEEE = 1, SPEC_NONE = 2 };
+
 static ofmt g_fmt[OF_NFMT];
 static int g_ready = 0;
 
@@ -128,9 +137,9 @@ static double decode_def(const ofmt *f, uint32_t c) {
   const uint32_t m = c & ((1u << f->mbits) - 1u);
   const uint32_t eall = (1u << f->ebits) - 1u, mall = (1u << f->mbits) - 1u;
   double mag;
-  if (f->ieee_special && e == eall) {
+  if (f->specials == SPEC_IEEE && e == eall) {
     mag = m ? NAN : INFINITY;
-  } else if (!f->ieee_special && e == eall && m == mall) {
+  } else if (f->specials == SPEC_E4M3 && e == eall && m == mall) {
     mag = NAN; /* E4M3: only S.1111.111 is special */
   } else if (e == 0) {
     mag = ldexp((double)m, 1 - f->bias - f->mbits); /* subnormal */
@@ -150,11 +159,12 @@ static int cmp_vc(const void *a, const void *b) {
   return (x > y) - (x < y);
 }
 
-static void fmt_init(ofmt *f, int ebits, int mbits, int bias, int ieee, int sat) {
+static void fmt_init(ofmt *f, int ebits, int mbits, int bias, int specials, int sat) {
   f->ebits = ebits;
   f->mbits = mbits;
   f->bias = bias;
-  f->ieee_special = ieee;
+  f->specials = specials;
+  f->inf_code = 0u;
   f->satfinite = sat;
   const int nb = ebits + mbits;
   const uint32_t ncodes = 1u << nb; /* codes with the sign bit clear */
@@ -187,15 +197,18 @@ static void fmt_init(ofmt *f, int ebits, int mbits, int bias, int ieee, int sat)
 
 static void init_formats(void) {
   if (g_ready) return;
-  fmt_init(&g_fmt[OF_BF16], 8, 7, 127, 1, 0);
-  fmt_init(&g_fmt[OF_E4M3], 4, 3, 7, 0, 1);
-  fmt_init(&g_fmt[OF_E5M2], 5, 2, 15, 1, 1);
-  fmt_init(&g_fmt[OF_FP16], 5, 10, 15, 1, 0);
+  fmt_init(&g_fmt[OF_BF16], 8, 7, 127, SPEC_IEEE, 0);
+  fmt_init(&g_fmt[OF_E4M3], 4, 3, 7, SPEC_E4M3, 1);
+  fmt_init(&g_fmt[OF_E5M2], 5, 2, 15, SPEC_IEEE, 1);
+  fmt_init(&g_fmt[OF_FP16], 5, 10, 15, SPEC_IEEE, 0);
+  /* OCP MX E2M1: bias 1, no Inf or NaN, largest magnitude 6 */
+  fmt_init(&g_fmt[OF_E2M1], 2, 1, 1, SPEC_NONE, 1);
   /* canonical NaN codes (positive) */
   g_fmt[OF_BF16].nan_code = 0x7FC0u;
   g_fmt[OF_FP16].nan_code = 0x7E00u;
   g_fmt[OF_E4M3].nan_code = 0x7Fu;
   g_fmt[OF_E5M2].nan_code = 0x7Fu;
+  g_fmt[OF_E2M1].nan_code = 0x0u; /* no NaN code: an MX block carries NaN in its scale */
   /* OF_FP32 is a passthrough and has no grid */
   g_ready = 1;
 }
@@ -207,6 +220,8 @@ static int fmt_bits(int fmt) {
   case OF_E4M3: return 8;
   case OF_E5M2: return 8;
   case OF_FP32: return 32;
+  case OF_E2M1: return 4;
+  case OF_E8M0: return 8;
   default: return 0;
   }
 }
@@ -223,21 +238,28 @@ static float f32_from_bits(uint32_t u) {
   return x;
 }
 
+/* E8M0: the value 2^(code - 127); code 255 is NaN (OCP MX scale format). */
+static double decode_e8m0(uint32_t code) {
+  code &= 0xFFu;
+  return code == 0xFFu ? NAN : ldexp(1.0, (int)code - 127);
+}
+
 /* Value of a stored code, as a double (exact). */
 static double decode(int fmt, uint32_t code) {
   if (fmt == OF_FP32) return (double)f32_from_bits(code);
+  if (fmt == OF_E8M0) return decode_e8m0(code);
   return decode_def(&g_fmt[fmt], code);
 }
 
-/* Round the fp32 value x into format fmt.  mode = OR_RNE (nearest, ties to the
- * code with an even last mantissa bit) or OR_SR (stochastic, draw r16). */
-static uint32_t encode(int fmt, float xf, int mode, uint32_t r16) {
-  if (fmt == OF_FP32) return isnan(xf) ? 0x7FC00000u : f32_bits(xf);
+/* Round the value x (exact, as a double) onto the grid of format fmt.
+ * mode = OR_RNE (nearest, ties to the code with an even last mantissa bit) or
+ * OR_SR (stochastic, draw r16). */
+static uint32_t encode_val(int fmt, double x, int mode, uint32_t r16) {
   const ofmt *f = &g_fmt[fmt];
   const int nb = f->ebits + f->mbits;
-  const uint32_t sign = signbit(xf) ? (1u << nb) : 0u;
-  if (isnan(xf)) return f->nan_code; /* the sign of a NaN carries no meaning */
-  const double a = fabs((double)xf);
+  const uint32_t sign = signbit(x) ? (1u << nb) : 0u;
+  if (isnan(x)) return f->nan_code; /* the sign of a NaN carries no meaning */
+  const double a = fabs(x);
   if (f->satfinite && a >= f->max) return sign | f->max_code;
   if (!f->satfinite && isinf(a)) return sign | f->inf_code;
 
@@ -274,6 +296,12 @@ static uint32_t encode(int fmt, float xf, int mode, uint32_t r16) {
     out = (k + (double)r16 >= 65536.0) ? hi_code : lo_code;
   }
   return sign | out;
+}
+
+/* Round the fp32 value xf into format fmt (FP32 is a passthrough). */
+static uint32_t encode(int fmt, float xf, int mode, uint32_t r16) {
+  if (fmt == OF_FP32) return isnan(xf) ? 0x7FC00000u : f32_bits(xf);
+  return encode_val(fmt, (double)xf, mode, r16);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -574,7 +602,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, uint16_t *copy, in
 /* Round fp32 values into a storage format with round-to-nearest-even. */
 int oracle_encode_array(int fmt, const float *x, void *codes, int64_t n) {
   init_formats();
-  if (fmt < 0 || fmt >= OF_NFMT || n < 0) return ORACLE_EINVAL;
+  if (fmt < 0 || fmt >= OF_NFMT || fmt == OF_E2M1 || n < 0) return ORACLE_EINVAL;
   for (int64_t i = 0; i < n; ++i) store_code(fmt, codes, i, encode(fmt, x[i], OR_RNE, 0u));
   return ORACLE_OK;
 }
@@ -589,6 +617,114 @@ int oracle_encode_block(int fmt, const float *x, uint8_t *q, uint16_t *scales, i
     for (int k = 0; k < BLOCK; ++k)
       q[b * BLOCK + k] = (uint8_t)encode(fmt, x[b * BLOCK + k] / sf, OR_RNE, 0u);
     scales[b] = sc;
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* MXFP4 storage (OCP Microscaling Formats v1.0)                             */
+/* ------------------------------------------------------------------------ */
+
+/* The paper trains with 4-bit block-scaled master weights (Section 4.2, its
+ * NVFP4/FP8 setting) without defining the format.  This oracle uses the MX
+ * block format of the OCP specification: blocks of 32 contiguous elements,
+ * each an E2M1 value, sharing one E8M0 scale X = 2^s; the weight is q * X.
+ * Two elements per byte, element 2k in the low nibble.
+ *
+ * Scale of a block of new weights w' (the specification's conversion rule):
+ *   s = floor(log2(max|w'|)) - emax, emax = exponent of E2M1's largest value
+ *   (6 = 1.5 * 2^2, so emax = 2), clamped to E8M0's range [-127, 127];
+ *   an all-zero block takes s = 0 (any scale represents it); a block holding
+ *   a non-finite w' takes the NaN scale and zero payloads.
+ * Payloads: q = round(w' / X) on the E2M1 grid with the step's rounding mode,
+ * saturating at +-6 (w' / X is exact: X is a power of two). */
+#define MX_BLOCK 32
+
+static uint32_t mx_get(const uint8_t *q, int64_t i) { return (q[i >> 1] >> (4 * (i & 1))) & 0xFu; }
+
+static void mx_put(uint8_t *q, int64_t i, uint32_t c) {
+  const int sh = 4 * (int)(i & 1);
+  q[i >> 1] = (uint8_t)((q[i >> 1] & ~(0xFu << sh)) | ((c & 0xFu) << sh));
+}
+
+/* Exponent s of the block scale for the values wn[0..31]; 128 marks NaN. */
+static int mx_scale_exp(const float *wn) {
+  double amax = 0.0;
+  for (int i = 0; i < MX_BLOCK; ++i) {
+    if (!isfinite(wn[i])) return 128;
+    if (fabs((double)wn[i]) > amax) amax = fabs((double)wn[i]);
+  }
+  if (amax == 0.0) return 0;
+  int e_amax, e_top;
+  (void)frexp(amax, &e_amax);                 /* amax = f 2^e, f in [0.5, 1) */
+  (void)frexp(g_fmt[OF_E2M1].max, &e_top);
+  int s = (e_amax - 1) - (e_top - 1);         /* floor(log2 amax) - emax */
+  if (s < -127) s = -127;
+  if (s > 127) s = 127;
+  return s;
+}
+
+static uint32_t mx_scale_code(int s) { return s == 128 ? 0xFFu : (uint32_t)(s + 127); }
+
+/* Payload code of w' in a block of scale exponent s. */
+static uint32_t mx_payload(float wn, int s, int mode, uint32_t r16) {
+  if (s == 128) return 0u;
+  return encode_val(OF_E2M1, ldexp((double)wn, -s), mode, r16);
+}
+
+/* The stored value q * X as the fp32 the step reads. */
+static float mx_value(uint32_t qcode, uint32_t scode) {
+  return (float)(decode(OF_E2M1, qcode) * decode_e8m0(scode));
+}
+
+/* M+Adam step on MXFP4 storage.  n must be a multiple of 32; q holds n/2
+ * bytes, scales n/32 E8M0 codes. */
+int oracle_step_mx(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const void *g, int sfmt,
+                   void *m, void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base,
+                   double lr_add, double lr_mul, double beta1, double beta2, double eps, double tau,
+                   double r_max, double eps0, double g_max, double d_mult_max, double w_max,
+                   int bias_correction, int rounding, uint64_t seed, int64_t step) {
+  init_formats();
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
+              w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
+  if (n < 0 || n % MX_BLOCK != 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  float wn[MX_BLOCK];
+  for (int64_t b = 0; b < n / MX_BLOCK; ++b) {
+    for (int k = 0; k < MX_BLOCK; ++k) {
+      const int64_t i = b * MX_BLOCK + k;
+      const float wv = mx_value(mx_get(q, i), scales[b]);
+      wn[k] = step_stored(wv, load_grad(gfmt, g, i), sfmt, m, v, ve, i, &s);
+    }
+    const int se = mx_scale_exp(wn);
+    const uint32_t sc = mx_scale_code(se);
+    for (int k = 0; k < MX_BLOCK; ++k) {
+      const int64_t i = b * MX_BLOCK + k;
+      const int64_t idx = gidx ? gidx[i] : index_base + i;
+      const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+      const uint32_t c = mx_payload(wn[k], se, h.rounding, r16);
+      mx_put(q, i, c);
+      if (copy) copy[i] = compute_copy(mx_value(c, sc));
+    }
+    scales[b] = (uint8_t)sc;
+  }
+  return ORACLE_OK;
+}
+
+/* MXFP4 encoding of fp32 values with round-to-nearest-even. */
+int oracle_encode_mx(const float *x, uint8_t *q, uint8_t *scales, int64_t n) {
+  init_formats();
+  if (n < 0 || n % MX_BLOCK != 0) return ORACLE_EINVAL;
+  for (int64_t b = 0; b < n / MX_BLOCK; ++b) {
+    const int se = mx_scale_exp(x + b * MX_BLOCK);
+    for (int k = 0; k < MX_BLOCK; ++k)
+      mx_put(q, b * MX_BLOCK + k, mx_payload(x[b * MX_BLOCK + k], se, OR_RNE, 0u));
+    scales[b] = (uint8_t)mx_scale_code(se);
   }
   return ORACLE_OK;
 }
@@ -648,6 +784,7 @@ double oracle_decode(int fmt, uint32_t code) {
 
 uint32_t oracle_encode(int fmt, float x, int rounding, uint32_t r16) {
   init_formats();
+  if (fmt < 0 || fmt >= OF_NFMT) return 0xFFFFFFFFu;
   return encode(fmt, x, rounding, r16 & 0xFFFFu);
 }
 

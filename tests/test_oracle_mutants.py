@@ -15,7 +15,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "madd_oracle.c")
 PINS = ["tests/test_oracle_step.py", "tests/test_oracle_block.py", "tests/test_oracle_sr_rng.py",
-        "tests/test_oracle_formats.py"]
+        "tests/test_oracle_formats.py", "tests/test_oracle_mx.py"]
 
 MUTANTS = {
     "additive sign": ("const float ua = -((s->SA * m) / den_a);",
@@ -58,6 +58,17 @@ MUTANTS = {
     "plain additive sign": ("  const float ua = -(lra * g);", "  const float ua = (lra * g);"),
     "plain multiplicative without rho": ("  const float um = clampf(ut / rho, s->ULO, s->UHI);\n  const float wn = fmaf(w, um, w) + ua;\n  return",
                                          "  const float um = clampf(ut, s->ULO, s->UHI);\n  const float wn = fmaf(w, um, w) + ua;\n  return"),
+    "MX scale exponent off by one": ("int s = (e_amax - 1) - (e_top - 1);",
+                                     "int s = (e_amax - 1) - (e_top - 2);"),
+    "MX nibble order": ("const int sh = 4 * (int)(i & 1);", "const int sh = 4 * (int)(1 - (i & 1));"),
+    "MX zero block scale": ("if (amax == 0.0) return 0;", "if (amax == 0.0) return -127;"),
+    "MX NaN block payload": ("if (s == 128) return 0u;", "if (s == 128) return 7u;"),
+    "MX scale exponent unclamped": ("  if (s < -127) s = -127;\n", ""),
+    "MX dequantize without the scale": (
+        "const float wv = mx_value(mx_get(q, i), scales[b]);",
+        "const float wv = (float)decode(OF_E2M1, mx_get(q, i));"),
+    "MX compute copy without the scale": ("if (copy) copy[i] = compute_copy(mx_value(c, sc));",
+                                          "if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, c));"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }
