@@ -32,11 +32,11 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
 
-WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1}
+WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5}
 SBYTES = {"fp32": 4, "bf16": 2}
 
 
-def bytes_per_param(wfmt: str, sfmt: str) -> int:
+def bytes_per_param(wfmt: str, sfmt: str) -> float:
     """Algorithmic bytes: read w, g (fp32), m, v, v_e; write w, m, v, v_e."""
     return 2 * WBYTES[wfmt] + 4 + 6 * SBYTES[sfmt]
 
@@ -53,7 +53,13 @@ def log(msg: str):
 
 
 def kernel_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    """Hash of the kernel source's code: comments and blank lines stripped, so
+    that documentation edits do not invalidate a counter summary."""
+    src = open(KERNEL_SRC).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    code = "\n".join(line.rstrip() for line in src.splitlines() if line.strip())
+    return hashlib.sha256(code.encode()).hexdigest()
 
 
 def traffic_from_profile():
@@ -62,7 +68,7 @@ def traffic_from_profile():
     if not os.path.exists(PMC_SUMMARY):
         return None
     text = open(PMC_SUMMARY).read()
-    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    sha = re.search(r"kernel_code_sha256:\s*([0-9a-f]{64})", text)
     val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not sha or not val or sha.group(1) != kernel_sha():
         return None
@@ -107,10 +113,11 @@ def main():
     ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
     ap.add_argument("--states", default="fp32", choices=["fp32", "bf16"],
                     help="storage of m, v, v_e (bf16: the paper's optimizer-state precision)")
-    ap.add_argument("--weights", default="list", choices=["list", "fp8-master"],
+    ap.add_argument("--weights", default="list", choices=["list", "fp8-master", "fp4-master"],
                     help="list: the configuration's weight format for every tensor; fp8-master: "
                          "linear layers block-scaled E4M3 with bf16 compute copies, embeddings, "
-                         "norms and head bf16 (the paper's FP8-master setting)")
+                         "norms and head bf16 (the paper's FP8-master setting); fp4-master: the "
+                         "same with MXFP4 linear layers (its 4-bit setting)")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
     ap.add_argument("--cpu-steps", type=int, default=None,
                     help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
@@ -158,8 +165,9 @@ def main():
             off += n
         return buf, views
 
-    if args.weights == "fp8-master":
-        plan = W.fp8_master_plan(cfg)
+    low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}.get(args.weights)
+    if low:
+        plan = W.low_precision_master_plan(cfg, low)
     else:
         plan = [(wfmt, False, False)] * len(specs)
 
@@ -181,9 +189,13 @@ def main():
         scales = copies = None
     else:
         wb16, w16 = flat_subset(torch.int16, lambda p: p[0] == "bf16")
-        wb8, w8 = flat_subset(torch.uint8, lambda p: p[0] != "bf16")
+        wb8, w8 = flat_subset(torch.uint8, lambda p: p[0] != "bf16",
+                              per_elem=2 if low == "mxfp4" else 1)
         ws = [a if a is not None else b for a, b in zip(w16, w8)]
-        sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
+        if low == "mxfp4":
+            sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=32)
+        else:
+            sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
         cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
     gbufs, grad_sets = [], []
     gb, gl = flat(torch.float32)
@@ -248,20 +260,21 @@ def main():
         log(f"copy probe: {nbytes} bytes read + {nbytes} bytes written")
         del src, dst
 
-    alg_bytes = 0
+    alg_bytes = 0.0
     for n, (wf, blk, cp) in zip(sizes, plan):
         alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
-        alg_bytes += (n // 128) * 4 if blk else 0  # FP16 scale read + written
+        if blk:  # scale read + written: FP16 per 128 (FP8) or E8M0 per 32 (MXFP4)
+            alg_bytes += (n // 32) * 2 if wf == "mxfp4" else (n // 128) * 4
     bpp = alg_bytes / nparam
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
     traffic = (traffic_from_profile()
                if (cfg == "c5" and args.states == "fp32" and args.weights == "list") else None)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "algorithmic_bytes_per_launch": alg_bytes,
+                "traffic": traffic, "algorithmic_bytes_per_launch": int(round(alg_bytes)),
                 "kernel": (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
                            f"{W.CONFIGS[cfg]['rounding'].upper()}>" if args.weights == "list" else
-                           "madd_step_block_kernel<e4m3> + madd_step_kernel<bf16> (two launches "
+                           f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches "
                            "per step; timed together)"),
                 "avg_launch_ms": round(avg_launch_ms, 4)}
 
@@ -286,7 +299,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[cfg], "params": nparam, "tensors": len(specs),
                    "weight_format": wfmt if args.weights == "list" else
-                   "e4m3 block-scaled linear layers + bf16 compute copies; bf16 embed/norms/head",
+                   f"{low} block-scaled linear layers + bf16 compute copies; bf16 "
+                   "embed/norms/head",
                    "grad_format": "fp32",
                    "state": f"{args.states} m, v, v_e",
                    "rounding": W.CONFIGS[cfg]["rounding"], "bytes_per_param": round(bpp, 4)},

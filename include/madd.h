@@ -52,7 +52,7 @@ extern "C" {
 typedef enum madd_status {
   MADD_OK = 0,
   MADD_EINVAL = -1,      /* invalid argument (NULL pointer, size, range, enum) */
-  MADD_EALIGN = -2,      /* block-scaled FP8 buffers not 16-byte aligned      */
+  MADD_EALIGN = -2,      /* block-scaled buffers not 16-byte aligned          */
   MADD_EUNSUPPORTED = -3,/* valid request the library does not implement      */
   MADD_EDEVICE = -4,     /* a HIP runtime call or kernel launch failed         */
   MADD_ENOMEM = -5       /* device allocation for the descriptor table failed  */
@@ -66,12 +66,22 @@ typedef enum madd_status {
  *              Both FP8 formats saturate finite overflow and Inf to +-max and
  *              store NaN as 0x7F.
  *   FP32     : passthrough (no rounding); for testing the unrounded step.
- *              NaN stored as 0x7FC00000. */
+ *              NaN stored as 0x7FC00000.
+ *   MXFP4    : 4-bit block-scaled storage, the OCP Microscaling (MX) v1.0
+ *              format MXFP4 -- the paper's 4-bit master-weight regime
+ *              (Section 4.2, the NVFP4/FP8 setting) names a 4-bit block
+ *              format without defining it.  Elements are OCP E2M1 (values
+ *              0, 0.5, 1, 1.5, 2, 3, 4, 6 and negatives), packed two per
+ *              byte, element 2k in the low nibble of byte k (w holds n/2
+ *              bytes).  Blocks of 32 contiguous elements share one E8M0
+ *              scale X = 2^(code - 127) (code 255 = NaN); the weight is
+ *              E2M1 value * X.  Always block-scaled (scales required). */
 typedef enum madd_wfmt {
   MADD_W_BF16 = 0,
   MADD_W_FP8_E4M3 = 1,
   MADD_W_FP8_E5M2 = 2,
-  MADD_W_FP32 = 3
+  MADD_W_FP32 = 3,
+  MADD_W_MXFP4 = 4
 } madd_wfmt;
 
 /* Gradient formats (decoded exactly to FP32). */
@@ -132,14 +142,21 @@ typedef struct madd_hparams {
 int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, void* stream);
 
 /* Round n fp32 values x into weight storage w with round-to-nearest-even.
- * w: device codes of format wfmt (2, 1, 1 or 4 bytes per element).
- * scales: NULL for unscaled storage; for block-scaled FP8 (wfmt E4M3 or
- *   E5M2 only) a device array of n/128 FP16 codes, n % 128 == 0: block b is
- *   elements [128b, 128b+128), its scale is RNE_fp16(max|x| / FMAX) (1.0 when
- *   the block is all zero, smallest FP16 subnormal on underflow, largest
- *   finite FP16 on overflow, FP16 NaN when the block holds a non-finite
- *   value) and its payloads are encode(x / scale). */
-int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* scales, int64_t n,
+ * w: device codes of format wfmt (2, 1, 1, 4 or 1/2 bytes per element).
+ * scales: NULL for unscaled storage, else a device array of block scales:
+ *   - block-scaled FP8 (wfmt E4M3 or E5M2): n/128 FP16 codes (uint16),
+ *     n % 128 == 0.  Block b is elements [128b, 128b+128); its scale is
+ *     RNE_fp16(max|x| / FMAX) (1.0 when the block is all zero, smallest FP16
+ *     subnormal on underflow, largest finite FP16 on overflow, FP16 NaN when
+ *     the block holds a non-finite value) and its payloads are
+ *     encode(x / scale).
+ *   - MXFP4 (required): n/32 E8M0 codes (uint8), n % 32 == 0.  Block b is
+ *     elements [32b, 32b+32); its scale is 2^s with s = floor(log2 max|x|)
+ *     - 2 (2 = exponent of E2M1's largest value 6), clamped to [-127, 127]
+ *     (the OCP MX conversion rule); s = 0 for an all-zero block; the NaN
+ *     scale, with zero payloads, for a block holding a non-finite value.
+ *     Payloads are x / 2^s rounded onto E2M1, saturating at +-6. */
+int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales, int64_t n,
                             void* stream);
 
 /* One M+Adam step on one tensor of n elements (Algorithm 1 with the optional
@@ -151,12 +168,13 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
  *           next step's GEMMs read, refreshed by dequantization after every
  *           update in the paper's FP8-master dataflow (Appendix figure), here
  *           written by the same pass.  16-byte aligned for the fast path.
- * scales  : NULL, or block-scaled FP8 as in madd_encode_weights: the weight
- *           is payload * scale (fp32 product); after the update each block's
+ * scales  : NULL, or the block scales of block-scaled FP8 or MXFP4 as in
+ *           madd_encode_weights (required for MXFP4): the weight is
+ *           payload * scale (fp32 product); after the update each block's
  *           scale is recomputed from the new weights by the same rule and the
- *           payloads re-encoded with hp->rounding.  Requires wfmt FP8,
- *           n % 128 == 0 and 16-byte-aligned w, g, m, v, ve (else
- *           MADD_EINVAL / MADD_EALIGN).
+ *           payloads re-encoded with hp->rounding.  Requires n % 128 == 0
+ *           (FP8) or n % 32 == 0 (MXFP4) and 16-byte-aligned w, g, m, v, ve
+ *           and copy (else MADD_EINVAL / MADD_EALIGN).
  * g       : device gradient of format gfmt (read only).
  * m, v, ve: device moments (first, second, multiplicative second) stored as
  *           sfmt (a madd_sfmt), updated in place.
@@ -166,7 +184,7 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
  *           any split of the index space (sharding).
  * Unaligned unscaled buffers are accepted and take a slower path with
  * identical results. */
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
                   int32_t gfmt, void* m, void* v, void* ve, int32_t sfmt, int64_t n,
                   int64_t index_base, const madd_hparams* hp, void* stream);
 
@@ -175,18 +193,18 @@ int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
  * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
  * block-scaled) or a host array whose entry i is NULL or tensor i's scale
- * array; copy: NULL (no compute copies) or a host array whose entry i is NULL
+ * array (never NULL for an MXFP4 tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
  * or tensor i's bf16 compute-copy array (as in madd_step).  Tensors of
  * different weight formats may be mixed -- e.g. block-scaled FP8 linear
- * layers with BF16 embeddings, norms and head, the paper's FP8-master
- * setting (Section 4.2).  Tensor i's elements have global
+ * layers (or MXFP4 ones) with BF16 embeddings, norms and head, the paper's
+ * FP8-master (4-bit-master) setting (Section 4.2).  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
  * The first call with a given list (same pointers and sizes) uploads a device
  * descriptor table (80 bytes per tensor) with a synchronous copy and caches it
  * (up to 32 lists per process; evicting one drains the device first).  Later
  * calls with the same list enqueue only the kernels. */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
-                               uint16_t* const* scales, uint16_t* const* copy,
+                               void* const* scales, uint16_t* const* copy,
                                const void* const* g, int32_t gfmt,
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
@@ -202,7 +220,8 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
  * No optimizer state.  w: device weight codes of format wfmt, in place;
  * g: device gradient of format gfmt; index_base, rounding and seed as in
  * madd_step; hp's beta1, beta2, eps, g_max and bias_correction are validated
- * but unused.  Errors as in madd_step. */
+ * but unused.  Unscaled formats only (MXFP4 is MADD_EINVAL).  Errors as in
+ * madd_step. */
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
                         int64_t index_base, const madd_hparams* hp, void* stream);
 

@@ -17,10 +17,12 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmadd.so")
 
 # enum values of madd.h
-W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32 = 0, 1, 2, 3
+W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32, W_MXFP4 = 0, 1, 2, 3, 4
 G_FP32, G_BF16 = 0, 1
 ROUND_RNE, ROUND_SR = 0, 1
-WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32}
+WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32,
+        "mxfp4": W_MXFP4}
+MX_BLOCK = 32  # elements per MXFP4 block (one E8M0 scale byte)
 GFMT = {"fp32": G_FP32, "bf16": G_BF16}
 S_FP32, S_BF16 = 0, 1
 SFMT = {"fp32": S_FP32, "bf16": S_BF16}
@@ -166,6 +168,7 @@ def madd_init_state(m, v, ve, sfmt: str | None = None, stream=None):
 
 
 def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
+    """Round fp32 ``x`` into the storage ``w`` (and its block ``scales``)."""
     _check("madd_encode_weights",
            lib().madd_encode_weights(_ptr(x), _ptr(w), WFMT[wfmt], _ptr(scales), x.numel(),
                                      _stream(stream)))
@@ -174,7 +177,8 @@ def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
 def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, index_base: int = 0,
               n: int | None = None, sfmt: str | None = None, copy=None, stream=None):
     """One step on one tensor.  ``w`` holds the weight codes (uint16 / uint8 /
-    int32 storage for bf16 / fp8 / fp32); the moments' storage follows their
+    int32 storage for bf16 / fp8 / fp32; n/2 packed bytes for mxfp4, whose
+    ``scales`` are n/32 uint8 E8M0 codes); the moments' storage follows their
     dtype unless ``sfmt`` is given; ``copy`` (16-bit tensor) receives the
     bf16 compute copy of the new weights."""
     h = _hp(hp)

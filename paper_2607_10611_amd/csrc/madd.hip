@@ -8,6 +8,9 @@
 // w + w u_m + u_a, and rounds the result back into the storage format (the
 // FP32-step / low-precision-storage round trip of Appendix B), to nearest-even
 // or stochastically with a Philox4x32-10 draw keyed by (seed, step, element).
+// Storage formats: bf16, FP8 E4M3 / E5M2 (optionally with FP16 scales per
+// 128-element block), and MXFP4 (E2M1 with an E8M0 scale per 32 elements)
+// for the 4-bit master-weight setting of Section 4.2.
 //
 // Layout of work: a launch covers a list of tensors.  The element space of
 // each tensor is cut into chunks; one workgroup (256 threads, four wave64s)
@@ -52,6 +55,7 @@ constexpr int kTile = 2 * kSub;              // sub-tiles A and B
 constexpr int kTilesPerChunk = 1;
 constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
 constexpr int kBlock = 128;                  // block-scaled FP8 block length
+constexpr int kMxBlock = 32;                 // MXFP4 block length (OCP MX)
 
 // ---------------------------------------------------------------------------
 // Scalars and descriptors
@@ -74,7 +78,7 @@ struct TensorDesc {
   void* m;   // moments: fp32, or bf16 codes
   void* v;
   void* ve;
-  uint16_t* scales;
+  void* scales;    // FP16 codes (block FP8) or E8M0 codes (MXFP4)
   uint16_t* copy;  // optional bf16 compute copy of the new weights
   int64_t n;       // elements
   int64_t gbase;   // global index of element 0
@@ -132,7 +136,7 @@ __device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s) {
 // Storage-format codecs (bit level)
 // ---------------------------------------------------------------------------
 
-enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3 };
+enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3, WF_MXFP4 = 4 };
 enum : int { GF_FP32 = 0, GF_BF16 = 1 };
 enum : int { SF_FP32 = 0, SF_BF16 = 1 };  // storage of the moments
 
@@ -230,6 +234,47 @@ __device__ __forceinline__ uint32_t enc_fp16_rne(float x) {
   return sign | c;
 }
 
+// MXFP4 (OCP Microscaling): E2M1 elements sharing an E8M0 power-of-two scale.
+// E2M1 magnitudes of codes 0..7, doubled (0 1 2 3 4 6 8 12), one per nibble.
+__device__ __forceinline__ float dec_e2m1(uint32_t c) {
+  const float mag = (float)((0xC8643210u >> (4u * (c & 7u))) & 0xFu) * 0.5f;
+  return (c & 8u) ? -mag : mag;
+}
+
+// x already divided by the block scale and finite; saturates at +-6.
+__device__ __forceinline__ uint32_t enc_e2m1(float x, bool sr, uint32_t r16) {
+  const uint32_t sign = (__float_as_uint(x) >> 28) & 0x8u;
+  const float a = fabsf(x);
+  if (a >= 6.0f) return sign | 0x7u;
+  uint32_t c = round_mini<1, 1, 0>(a, sr, r16);  // 1 mantissa bit, bias 1, min exponent 0
+  c = c > 0x7u ? 0x7u : c;
+  return sign | c;
+}
+
+// E8M0: 2^(c - 127); code 0 is the fp32 subnormal 2^-127; code 255 is NaN.
+__device__ __forceinline__ float dec_e8m0(uint32_t c) {
+  if (c == 0xFFu) return __uint_as_float(0x7FC00000u);
+  return __uint_as_float(c == 0u ? 0x00400000u : (c << 23));
+}
+
+// Scale code of a block whose largest |w'| has the raw bits amax_bits:
+// s = floor(log2 amax) - 2 clamped to [-127, 127] (code s + 127); 1.0 for an
+// all-zero block; NaN when the block holds a non-finite value.  For a normal
+// amax floor(log2 amax) is its unbiased exponent field, so the code is the
+// biased field minus 2; a subnormal amax clamps to code 0.
+__device__ __forceinline__ uint32_t mx_scale(uint32_t amax_bits) {
+  if (amax_bits >= 0x7F800000u) return 0xFFu;
+  if (amax_bits == 0u) return 127u;
+  const uint32_t ef = amax_bits >> 23;
+  return ef > 2u ? ef - 2u : 0u;
+}
+
+// 2^-s for a finite scale code (a normal float for every code the rule
+// produces, 0..252), so that w' * 2^-s is the exact quotient w' / 2^s.
+__device__ __forceinline__ float mx_inv_scale(uint32_t code) {
+  return __uint_as_float((code < 0xFFu ? 254u - code : 127u) << 23);
+}
+
 template <int WF>
 __device__ __forceinline__ uint32_t encode(float x, bool sr, uint32_t r16) {
   if constexpr (WF == WF_BF16) return enc_bf16(x, sr, r16);
@@ -241,6 +286,7 @@ template <int WF>
 __device__ __forceinline__ float decode(uint32_t c) {
   if constexpr (WF == WF_BF16) return dec_bf16(c);
   else if constexpr (WF == WF_FP32) return __uint_as_float(c);
+  else if constexpr (WF == WF_MXFP4) return dec_e2m1(c);  // payload value, before the scale
   else return dec_fp8<WF>(c);
 }
 
@@ -331,6 +377,18 @@ template <>
 struct WQuad<WF_E4M3> : WQuad8<WF_E4M3> {};
 template <>
 struct WQuad<WF_E5M2> : WQuad8<WF_E5M2> {};
+template <>
+struct WQuad<WF_MXFP4> {  // 4 x 4 bits: two bytes, element 2k in the low nibble of byte k
+  uint32_t raw;
+  __device__ __forceinline__ void load(const void* p, int64_t e) {
+    raw = ldg<uint16_t>((const uint8_t*)p + (e >> 1));
+  }
+  __device__ __forceinline__ uint32_t code(int k) const { return (raw >> (4 * k)) & 0xFu; }
+  __device__ __forceinline__ void set(int k, uint32_t c) { raw = (raw & ~(0xFu << (4 * k))) | (c << (4 * k)); }
+  __device__ __forceinline__ void store(void* p, int64_t e) const {
+    stg<uint16_t>((uint8_t*)p + (e >> 1), (uint16_t)raw);
+  }
+};
 template <>
 struct WQuad<WF_FP32> {  // 4 x 32 bits
   u4 raw;
@@ -602,18 +660,39 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
   }
 }
 
-// Block-scaled FP8: 32 consecutive lanes hold one 128-element block of a
-// sub-tile; the block's max |w'| is combined across them with lane shuffles.
-// The launch requires n % 128 == 0, so a block is never split and whole
-// 32-lane groups are active or inactive together; every lane runs the
+// Block-scaled storage: the kBlk / 4 consecutive lanes that hold one block of
+// a sub-tile (32 lanes for a 128-element FP8 block, 8 for a 32-element MXFP4
+// block) combine the block's max |w'| with lane shuffles.  The launch
+// requires n to be a multiple of the block length, so a block is never split
+// and whole lane groups are active or inactive together; every lane runs the
 // shuffles and the draw exchange.
-__device__ __forceinline__ uint32_t block_amax32(uint32_t a) {
+template <int WF>
+constexpr int block_len() { return WF == WF_MXFP4 ? kMxBlock : kBlock; }
+
+template <int LANES>
+__device__ __forceinline__ uint32_t block_amax(uint32_t a) {
 #pragma unroll
-  for (int off = 16; off >= 1; off >>= 1) {
-    const uint32_t o = (uint32_t)__shfl_xor((int)a, off, 32);
+  for (int off = LANES / 2; off >= 1; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)a, off, LANES);
     a = o > a ? o : a;
   }
   return a;
+}
+
+template <int WF>
+__device__ __forceinline__ float scale_value(uint32_t code) {
+  if constexpr (WF == WF_MXFP4) return dec_e8m0(code);
+  else return dec_fp16(code);
+}
+template <int WF>
+__device__ __forceinline__ uint32_t load_scale(const void* scales, int64_t b) {
+  if constexpr (WF == WF_MXFP4) return ((const uint8_t*)scales)[b];
+  else return ((const uint16_t*)scales)[b];
+}
+template <int WF>
+__device__ __forceinline__ void store_scale(void* scales, int64_t b, uint32_t code) {
+  if constexpr (WF == WF_MXFP4) ((uint8_t*)scales)[b] = (uint8_t)code;
+  else ((uint16_t*)scales)[b] = (uint16_t)code;
 }
 
 template <int WF, bool SR, bool CLAMP>
@@ -636,16 +715,26 @@ __device__ __forceinline__ uint32_t step_quad_unrounded(Quad<WF>& q, float sold,
 template <int WF, bool SR>
 __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[4], uint32_t amax,
                                                  const uint32_t (&r)[4]) {
-  const uint32_t sc = block_scale<WF>(amax);
-  const float sf = dec_fp16(sc);
+  if constexpr (WF == WF_MXFP4) {
+    const uint32_t sc = mx_scale(amax);
+    const float inv = mx_inv_scale(sc);
 #pragma unroll
-  for (int k = 0; k < 4; ++k) q.w.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
-  return sc;
+    for (int k = 0; k < 4; ++k) q.w.set(k, sc == 0xFFu ? 0u : enc_e2m1(wn[k] * inv, SR, r[k]));
+    return sc;
+  } else {
+    const uint32_t sc = block_scale<WF>(amax);
+    const float sf = dec_fp16(sc);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) q.w.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
+    return sc;
+  }
 }
 
 template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
+  constexpr int kBlk = block_len<WF>();
+  constexpr int kLanes = kBlk / kQuad;
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const int64_t c0 = (chunk - d.chunk0) * kChunk;
@@ -655,7 +744,7 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     const int64_t tb = c0 + (int64_t)tile * kTile;
     if (tb >= cend) break;
     const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
-    const bool actA = eA < cend, actB = eB < cend;  // whole 32-lane groups agree
+    const bool actA = eA < cend, actB = eB < cend;  // whole lane groups of a block agree
     Quad<WF> qa, qb;
     float wa[4], wb[4];
     uint32_t amaxA = 0u, amaxB = 0u;
@@ -668,21 +757,25 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
       draws_any<SR>((uint64_t)(d.gbase + eA), s, rA);
       draws_any<SR>((uint64_t)(d.gbase + eB), s, rB);
     }
-    if (actA) amaxA = step_quad_unrounded<WF, SR, CLAMP>(qa, dec_fp16(d.scales[eA / kBlock]), wa, s);
-    if (actB) amaxB = step_quad_unrounded<WF, SR, CLAMP>(qb, dec_fp16(d.scales[eB / kBlock]), wb, s);
-    amaxA = block_amax32(amaxA);
-    amaxB = block_amax32(amaxB);
+    if (actA)
+      amaxA = step_quad_unrounded<WF, SR, CLAMP>(
+          qa, scale_value<WF>(load_scale<WF>(d.scales, eA / kBlk)), wa, s);
+    if (actB)
+      amaxB = step_quad_unrounded<WF, SR, CLAMP>(
+          qb, scale_value<WF>(load_scale<WF>(d.scales, eB / kBlk)), wb, s);
+    amaxA = block_amax<kLanes>(amaxA);
+    amaxB = block_amax<kLanes>(amaxB);
     if (actA) {
       const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA);
       store_quad<WF, SF>(qa, d, eA);
-      if (COPY && d.copy) store_copy<WF>(qa.w, dec_fp16(sc), d.copy, eA);
-      if ((threadIdx.x & 31u) == 0u) d.scales[eA / kBlock] = (uint16_t)sc;
+      if (COPY && d.copy) store_copy<WF>(qa.w, scale_value<WF>(sc), d.copy, eA);
+      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, eA / kBlk, sc);
     }
     if (actB) {
       const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB);
       store_quad<WF, SF>(qb, d, eB);
-      if (COPY && d.copy) store_copy<WF>(qb.w, dec_fp16(sc), d.copy, eB);
-      if ((threadIdx.x & 31u) == 0u) d.scales[eB / kBlock] = (uint16_t)sc;
+      if (COPY && d.copy) store_copy<WF>(qb.w, scale_value<WF>(sc), d.copy, eB);
+      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, eB / kBlk, sc);
     }
   }
 }
@@ -770,6 +863,29 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
   }
 }
 
+// One thread per 32-element MXFP4 block.
+__global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __restrict__ x,
+                                                             uint8_t* q, uint8_t* scales,
+                                                             int64_t nblocks) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < nblocks; b += stride) {
+    const float* xb = x + b * kMxBlock;
+    uint32_t amax = 0u;
+    for (int k = 0; k < kMxBlock; ++k) {
+      const uint32_t ab = __float_as_uint(xb[k]) & 0x7FFFFFFFu;
+      amax = ab > amax ? ab : amax;
+    }
+    const uint32_t sc = mx_scale(amax);
+    const float inv = mx_inv_scale(sc);
+    for (int k = 0; k < kMxBlock; k += 2) {
+      const uint32_t lo = sc == 0xFFu ? 0u : enc_e2m1(xb[k] * inv, false, 0u);
+      const uint32_t hi = sc == 0xFFu ? 0u : enc_e2m1(xb[k + 1] * inv, false, 0u);
+      q[b * (kMxBlock / 2) + k / 2] = (uint8_t)(lo | (hi << 4));
+    }
+    scales[b] = (uint8_t)sc;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
@@ -778,15 +894,21 @@ typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
 
 template <int WF, int GF, int SF, bool SR, bool CLAMP>
 step_fn pick_copy(bool copy, bool blk) {
-  if constexpr (WF == WF_E4M3 || WF == WF_E5M2) {
-    if (blk)
-      return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
-                  : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
+  if constexpr (WF == WF_MXFP4) {
+    if (!blk) return nullptr;  // MXFP4 is always block-scaled
+    return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
+                : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
   } else {
-    if (blk) return nullptr;  // block scaling exists for FP8 payloads only
+    if constexpr (WF == WF_E4M3 || WF == WF_E5M2) {
+      if (blk)
+        return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
+                    : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
+    } else {
+      if (blk) return nullptr;  // no block-scaled form of BF16 or FP32
+    }
+    return copy ? madd_step_kernel<WF, GF, SF, SR, CLAMP, true>
+                : madd_step_kernel<WF, GF, SF, SR, CLAMP, false>;
   }
-  return copy ? madd_step_kernel<WF, GF, SF, SR, CLAMP, true>
-              : madd_step_kernel<WF, GF, SF, SR, CLAMP, false>;
 }
 template <int WF, int GF, int SF, bool SR>
 step_fn pick_clamp(bool clamp, bool copy, bool blk) {
@@ -818,6 +940,7 @@ step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool copy, bool
     case WF_E4M3: return pick_gf<WF_E4M3>(gf, sf, sr, clamp, copy, blk);
     case WF_E5M2: return pick_gf<WF_E5M2>(gf, sf, sr, clamp, copy, blk);
     case WF_FP32: return pick_gf<WF_FP32>(gf, sf, sr, clamp, copy, blk);
+    case WF_MXFP4: return pick_gf<WF_MXFP4>(gf, sf, sr, clamp, copy, blk);
     default: return nullptr;
   }
 }
@@ -826,11 +949,9 @@ bool needs_clamp(const madd_hparams& hp) {
   return !(std::isinf(hp.g_max) && hp.g_max > 0) || !(std::isinf(hp.w_max) && hp.w_max > 0);
 }
 
-bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_FP32; }
+bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_MXFP4; }
 bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
 bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16; }
-int wbytes(int32_t f) { return f == MADD_W_BF16 ? 2 : (f == MADD_W_FP32 ? 4 : 1); }
-int gbytes(int32_t f) { return f == MADD_G_FP32 ? 4 : 2; }
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int32_t check_hparams(const madd_hparams* hp) {
@@ -940,7 +1061,7 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-TensorDesc make_desc(void* w, uint16_t* scales, uint16_t* copy, const void* g, void* m, void* v,
+TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void* m, void* v,
                      void* ve, int64_t n, int64_t gbase) {
   TensorDesc d;
   memset(&d, 0, sizeof(d));
@@ -959,15 +1080,21 @@ TensorDesc make_desc(void* w, uint16_t* scales, uint16_t* copy, const void* g, v
   return d;
 }
 
-int32_t check_tensor(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+bool block_scaled_fmt(int32_t f) {
+  return f == MADD_W_FP8_E4M3 || f == MADD_W_FP8_E5M2 || f == MADD_W_MXFP4;
+}
+int64_t block_len_of(int32_t f) { return f == MADD_W_MXFP4 ? kMxBlock : kBlock; }
+
+int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
                      void* m, void* v, void* ve, int64_t n) {
   if (n < 0) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
   if (!valid_wfmt(wfmt)) return MADD_EINVAL;
+  if (wfmt == MADD_W_MXFP4 && !scales) return MADD_EINVAL;
   if (scales) {
-    if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
-    if (n % kBlock != 0) return MADD_EINVAL;
+    if (!block_scaled_fmt(wfmt)) return MADD_EINVAL;
+    if (n % block_len_of(wfmt) != 0) return MADD_EINVAL;
     if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy))))
       return MADD_EALIGN;
   }
@@ -1012,12 +1139,22 @@ int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, voi
   return MADD_OK;
 }
 
-int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* scales, int64_t n,
+int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales, int64_t n,
                             void* stream) {
   if (n < 0 || !valid_wfmt(wfmt)) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!x || !w) return MADD_EINVAL;
+  if (wfmt == MADD_W_MXFP4 && !scales) return MADD_EINVAL;
   hipStream_t st = (hipStream_t)stream;
+  if (wfmt == MADD_W_MXFP4) {
+    if (n % kMxBlock != 0) return MADD_EINVAL;
+    const int64_t nb = n / kMxBlock;
+    const int64_t want = (nb + kThreads - 1) / kThreads;
+    const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+    hipLaunchKernelGGL(encode_mx_kernel, dim3(grid), dim3(kThreads), 0, st, x, (uint8_t*)w,
+                       (uint8_t*)scales, nb);
+    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  }
   if (scales) {
     if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
     if (n % kBlock != 0) return MADD_EINVAL;
@@ -1026,10 +1163,10 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
     if (wfmt == MADD_W_FP8_E4M3)
       hipLaunchKernelGGL(encode_block_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), 0, st, x,
-                         (uint8_t*)w, scales, nb);
+                         (uint8_t*)w, (uint16_t*)scales, nb);
     else
       hipLaunchKernelGGL(encode_block_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), 0, st, x,
-                         (uint8_t*)w, scales, nb);
+                         (uint8_t*)w, (uint16_t*)scales, nb);
     return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
   }
   const int64_t want = (n + kThreads - 1) / kThreads;
@@ -1043,7 +1180,7 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, uint16_t* sca
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
-int32_t madd_step(void* w, int32_t wfmt, uint16_t* scales, uint16_t* copy, const void* g,
+int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
                   int32_t gfmt, void* m, void* v, void* ve, int32_t sfmt, int64_t n,
                   int64_t index_base, const madd_hparams* hp, void* stream) {
   int32_t rc = check_hparams(hp);
@@ -1067,6 +1204,7 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
   if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0 || n < 0) return MADD_EINVAL;
+  if (wfmt == MADD_W_MXFP4) return MADD_EINVAL;  // block-scaled: no scale argument here
   if (n == 0) return MADD_OK;
   if (!w || !g) return MADD_EINVAL;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
@@ -1087,7 +1225,7 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
 }
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
-                               uint16_t* const* scales, uint16_t* const* copy,
+                               void* const* scales, uint16_t* const* copy,
                                const void* const* g, int32_t gfmt,
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
@@ -1118,7 +1256,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
     int64_t nchunks;
   };
   std::vector<Group> groups;
-  for (int wf = MADD_W_BF16; wf <= MADD_W_FP32; ++wf) {
+  for (int wf = MADD_W_BF16; wf <= MADD_W_MXFP4; ++wf) {
     for (int blk = 0; blk <= 1; ++blk) {
       std::vector<TensorDesc> descs;
       int64_t gbase = index_base, nch = 0;

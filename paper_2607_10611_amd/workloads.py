@@ -208,16 +208,24 @@ def grad_fp32_device_(cfg: str, i: int, step: int, out, sigma: float | None = No
     return out
 
 
-def fp8_master_plan(cfg: str):
-    """Per-tensor storage for the FP8-master setting of Section 4.2: attention
-    and MLP linear weights as block-scaled E4M3 (FP16 scale per 128 elements)
-    with a bf16 compute copy; embeddings, norms and the LM head in bf16.
-    Returns (weight format, block-scaled, compute copy) per tensor."""
+def low_precision_master_plan(cfg: str, linear_fmt: str = "e4m3"):
+    """Per-tensor storage for the low-precision master settings of Section 4.2:
+    attention and MLP linear weights block-scaled in ``linear_fmt`` -- "e4m3"
+    (FP16 scale per 128 elements; the FP8/FP8 setting) or "mxfp4" (E2M1 with
+    an E8M0 scale per 32 elements; standing in for the 4-bit NVFP4/FP8
+    setting) -- each with a bf16 compute copy; embeddings, norms and the LM
+    head in bf16.  Returns (weight format, block-scaled, compute copy) per
+    tensor."""
     plan = []
     for s in specs(cfg):
         linear = s.kind == "matrix" and s.name not in ("embed", "lm_head", "wte", "wpe")
-        plan.append(("e4m3", True, True) if linear else ("bf16", False, False))
+        plan.append((linear_fmt, True, True) if linear else ("bf16", False, False))
     return plan
+
+
+def fp8_master_plan(cfg: str):
+    """The FP8-master setting: low_precision_master_plan with E4M3."""
+    return low_precision_master_plan(cfg, "e4m3")
 
 
 # ---------------------------------------------------------------------------

@@ -6,8 +6,10 @@ import torch
 import oracle
 from paper_2607_10611_amd import binding as B
 
-CODE_NP = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32}
-CODE_T = {"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8, "fp32": torch.int32}
+CODE_NP = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,
+           "mxfp4": np.uint8}  # mxfp4: packed bytes, two elements each
+CODE_T = {"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8, "fp32": torch.int32,
+          "mxfp4": torch.uint8}
 SIGNED_NP = {np.uint16: np.int16, np.uint32: np.int32, np.uint8: np.uint8}
 
 
@@ -90,7 +92,10 @@ class HostState:
 
 
 def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
-    if hs.scales is not None:
+    if wfmt == "mxfp4":
+        oracle.step_mx(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
+                       index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
+    elif hs.scales is not None:
         oracle.step_block(wfmt, hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
                           index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
     else:

@@ -81,6 +81,21 @@ def test_step_rejects_bad_arguments():
     assert call(None, 0, None, None, 0, None, None, None, 0, 0, 0) == 0            # empty: no-op
 
 
+def test_mxfp4_argument_rules():
+    lib = B.lib()
+    ref, _h = _hp()
+    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_MXFP4, sc, cp, FAKE, 0, FAKE, FAKE,  # noqa: E731
+                                                   FAKE, 0, n, 0, ref, None)
+    assert call(FAKE, None, 64) == -1            # MXFP4 needs its scales
+    assert call(FAKE, FAKE, 48) == -1            # n % 32
+    assert call(FAKE + 2, FAKE, 64) == -2        # unaligned payload bytes
+    assert call(FAKE, FAKE, 64, FAKE + 4) == -2  # unaligned compute copy
+    assert lib.madd_plain_step(FAKE, B.W_MXFP4, FAKE, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, None, 64, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, FAKE, 40, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, 5, FAKE, 64, None) == -1   # no such format
+
+
 def test_multi_tensor_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
@@ -103,6 +118,9 @@ def test_multi_tensor_rejects_bad_arguments():
     assert mt(2, w, fm, None, None, g, 0, m, v, ve, 0, ne_bad, 0, ref, None) == -1
     sc = arr(None, FAKE)  # second tensor block-scaled but bf16
     assert mt(2, w, fm, sc, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
+    fm_mx = (ctypes.c_int32 * 2)(4, 4)
+    sc_one = arr(FAKE, None)  # second MXFP4 tensor without scales
+    assert mt(2, w, fm_mx, sc_one, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
 
 
 def test_plain_step_rejects_bad_arguments():

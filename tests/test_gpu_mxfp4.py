@@ -1,0 +1,256 @@
+"""Parity of the HIP step on MXFP4 storage (E2M1 payloads, one E8M0 scale per
+32 elements) with the CPU oracle, through the C ABI.  Bar: packed payload
+bytes, scale codes and bf16 compute copies bit-exact; fp32 moments within
+2 ulp; bf16 moment codes bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_10611_amd import binding as B
+from paper_2607_10611_amd import workloads as W
+from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
+                             gpu_step, oracle_step, to_dev, to_host)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def hp(**kw):
+    h = dict(W.DEFAULT_HPARAMS)
+    h.update(kw)
+    return h
+
+
+def mx_weights(rng, n):
+    """N(0, 0.02) with zeros, outliers and tiny values; whole special blocks
+    (all zero, tiny, huge) at the front when there is room."""
+    x = rng.normal(0, 0.02, n).astype(np.float32)
+    x[rng.random(n) < 0.02] = 0.0
+    big = rng.random(n) < 0.01
+    x[big] = rng.normal(0, 3.0, big.sum())
+    if n >= 4 * 32:
+        x[:32] = 0.0
+        x[32:64] = rng.normal(0, 1e-39, 32).astype(np.float32)  # subnormal block
+        x[64:96] = rng.normal(0, 1e37, 32).astype(np.float32)   # near the top of fp32
+    return x
+
+
+def mx_grad(rng, n):
+    g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-6, -1, n)).astype(np.float32)
+    g[rng.random(n) < 0.05] = 0.0
+    return g
+
+
+def encode_mx_both(x):
+    q_ref, s_ref = oracle.encode_mx(x)
+    q = torch.empty(x.size // 2, dtype=torch.uint8, device="cuda")
+    s = torch.empty(x.size // 32, dtype=torch.uint8, device="cuda")
+    B.madd_encode_weights(torch.from_numpy(x).cuda(), q, "mxfp4", scales=s)
+    torch.cuda.synchronize()
+    bad = np.nonzero(to_host(q) != q_ref)[0]
+    assert bad.size == 0, f"encode payload bytes differ at {bad[:5]}"
+    assert (to_host(s) == s_ref).all(), "encode scales differ"
+    return q_ref, s_ref
+
+
+def check(tag, ds, hs):
+    w_g, m_g, v_g, ve_g = ds.host()
+    assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+    bad = np.nonzero(to_host(ds.scales) != hs.scales)[0]
+    assert bad.size == 0, f"{tag}: scales differ at blocks {bad[:5]}"
+    assert_copy_equal(tag, ds, hs)
+
+
+def run_mx(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
+           grad=mx_grad):
+    rng = np.random.default_rng(seed)
+    q, s = encode_mx_both(mx_weights(rng, n))
+    ds = DevState("mxfp4", q, n, s, sfmt=sfmt, copy=copy)
+    hs = HostState(q, n, s, sfmt=sfmt, copy=copy)
+    for t in range(1, steps + 1):
+        g = grad(rng, n)
+        if gfmt == "bf16":
+            g = oracle.encode_array("bf16", g)
+        h = hp(step=t, **hpkw)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
+        oracle_step("mxfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
+        torch.cuda.synchronize()
+        check(f"mxfp4 n={n} t={t}", ds, hs)
+    return ds, hs
+
+
+def test_encode_matches_oracle():
+    rng = np.random.default_rng(1)
+    x = mx_weights(rng, 32 * 4000)
+    x[200:232] = 0.0
+    x[300] = np.nan
+    x[400] = -np.inf
+    x[500] = 3.4e38
+    encode_mx_both(x)
+
+
+@pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
+                                                 ("sr", "bf16", True), ("rne", "bf16", False)])
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+    # five whole 2048-element tiles, then 3 blocks of a sixth
+    run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
+
+
+@pytest.mark.parametrize("n", [32, 64, 992, 2048 + 32, 4096 + 1024 + 96])
+def test_small_and_partial_tiles(n):
+    run_mx(n, 3, 12 + n, dict(rounding="sr", seed=77, lr_add=1e-2), copy=True)
+
+
+def test_bf16_gradients_unaligned_index_base():
+    # index base not a multiple of 8: the per-element draw path
+    run_mx(3 * 8192 + 32, 3, 13, dict(rounding="sr", seed=5), gfmt="bf16", index_base=3,
+           copy=True)
+
+
+def test_algorithm2_clamps():
+    run_mx(2 * 8192, 3, 14, dict(rounding="sr", g_max=2.0, w_max=0.5, d_mult_max=0.25,
+                                 eps0=0.1, bias_correction=0, lr_mul=0.05))
+
+
+def test_nonfinite_gradients_poison_their_blocks():
+    def grad(rng, n):
+        g = mx_grad(rng, n)
+        g[[40, 1000, 5000]] = [np.nan, np.inf, -np.inf]
+        return g
+    ds, hs = run_mx(4 * 2048, 2, 15, dict(rounding="sr"), grad=grad, copy=True)
+    sc = to_host(ds.scales)
+    assert (sc[[40 // 32, 1000 // 32, 5000 // 32]] == 0xFF).all()
+
+
+def test_multi_tensor_list_with_mxfp4():
+    rng = np.random.default_rng(16)
+    layout = [("mxfp4", 4096 + 64), ("bf16", 1000), ("mxfp4", 96), ("e4m3", 1024),
+              ("mxfp4", 0), ("mxfp4", 20480)]
+    devs, singles, hosts = [], [], []
+    for wfmt, n in layout:
+        if wfmt == "mxfp4":
+            q, s = encode_mx_both(mx_weights(rng, n)) if n else (np.zeros(0, np.uint8),
+                                                                  np.zeros(0, np.uint8))
+            args = (q, n, s)
+        elif wfmt == "e4m3":
+            q, s = oracle.encode_block("e4m3", mx_weights(rng, n))
+            args = (q, n, s)
+        else:
+            args = (oracle.encode_array("bf16", mx_weights(rng, n)), n, None)
+        cp = wfmt != "bf16"
+        devs.append(DevState(wfmt, *args, copy=cp))
+        singles.append(DevState(wfmt, *args, copy=cp))
+        hosts.append(HostState(*args, copy=cp))
+    base = 4000
+    for t in range(1, 4):
+        gs = [mx_grad(rng, n) for _, n in layout]
+        gds = [to_dev(g) for g in gs]
+        h = hp(step=t, rounding="sr", seed=2718)
+        tl = B.TensorList([d.w for d in devs], [d.wfmt for d in devs], gds, [d.m for d in devs],
+                          [d.v for d in devs], [d.ve for d in devs],
+                          scales=[d.scales for d in devs], copies=[d.copy for d in devs])
+        B.madd_multi_tensor_step(tl, h, index_base=base)
+        off = base
+        for (wfmt, n), d1, hs, g, gd in zip(layout, singles, hosts, gs, gds):
+            if n:
+                gpu_step(d1, gd, h, index_base=off)
+                oracle_step(wfmt, hs, g, h, index_base=off)
+            off += n
+        torch.cuda.synchronize()
+        for (wfmt, n), d, d1, hs in zip(layout, devs, singles, hosts):
+            if not n:
+                continue
+            tag = f"multi {wfmt} n={n} t={t}"
+            w_g, m_g, v_g, ve_g = d.host()
+            assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+            assert_copy_equal(tag, d, hs)
+            for a, b in zip(d.host(), d1.host()):
+                assert a.tobytes() == b.tobytes(), tag
+            if hs.scales is not None:
+                sn = np.uint8 if wfmt == "mxfp4" else np.uint16
+                assert (to_host(d.scales, sn) == hs.scales).all(), tag
+
+
+def test_fp4_master_llama7b_sampled():
+    """The 4-bit master setting on the full 7B list: attention and MLP linear
+    weights in MXFP4 with bf16 compute copies, embeddings / norms / head in
+    bf16, one multi-tensor call per step; the oracle follows sampled whole
+    32-element blocks (their global indices key the draws)."""
+    cfg = "c5"
+    specs = W.specs(cfg)
+    plan = W.low_precision_master_plan(cfg, "mxfp4")
+    free, _ = torch.cuda.mem_get_info()
+    need = sum(s.numel for s in specs) * 19 + (1 << 30)
+    assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
+    rng = np.random.default_rng(17)
+    offsets = np.cumsum([0] + [s.numel for s in specs])
+    dev = dict(w=[], sc=[], cp=[], m=[], v=[], ve=[], g=[])
+    samples, hosts = [], []
+    for i, (s, (wfmt, blk, cp)) in enumerate(zip(specs, plan)):
+        x = W.init_fp32_device(cfg, i)
+        if blk:
+            w = torch.empty(s.numel // 2, dtype=torch.uint8, device="cuda")
+            sc = torch.empty(s.numel // 32, dtype=torch.uint8, device="cuda")
+        else:
+            w = torch.empty(s.numel, dtype=torch.int16, device="cuda")
+            sc = None
+        B.madd_encode_weights(x, w, wfmt, scales=sc)
+        blen = 32 if blk else 128
+        nb = s.numel // blen
+        bidx = np.unique(np.concatenate([np.arange(4), np.arange(nb - 4, nb),
+                                         rng.choice(nb, size=min(nb, 48), replace=False)]))
+        idx = (bidx[:, None] * blen + np.arange(blen)[None, :]).ravel()
+        idx_t = torch.from_numpy(idx).cuda()
+        x_s = to_host(x[idx_t])
+        if blk:
+            byte_t = torch.from_numpy((bidx[:, None] * 16 + np.arange(16)[None, :]).ravel()).cuda()
+            q_ref, s_ref = oracle.encode_mx(x_s)
+            assert (to_host(w[byte_t]) == q_ref).all(), s.name
+            assert (to_host(sc[torch.from_numpy(bidx).cuda()]) == s_ref).all(), s.name
+            hs = HostState(q_ref, idx.size, s_ref, copy=cp)
+        else:
+            byte_t = None
+            codes = oracle.encode_array(wfmt, x_s)
+            assert (to_host(w[idx_t], np.uint16) == codes).all(), s.name
+            hs = HostState(codes, idx.size, copy=cp)
+        del x
+        dev["w"].append(w)
+        dev["sc"].append(sc)
+        dev["cp"].append(torch.zeros(s.numel, dtype=torch.int16, device="cuda") if cp else None)
+        for k in ("m", "v", "ve"):
+            dev[k].append(torch.zeros(s.numel, device="cuda"))
+        dev["g"].append(torch.empty(s.numel, device="cuda"))
+        samples.append((idx, idx_t, bidx, byte_t))
+        hosts.append(hs)
+    tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
+                      scales=dev["sc"], copies=dev["cp"])
+    for t in (1, 2, 3):
+        for i in range(len(specs)):
+            W.grad_fp32_device_(cfg, i, t, dev["g"][i])
+        h = W.hparams(cfg, step=t)
+        B.madd_multi_tensor_step(tl, h)
+        for i, (idx, idx_t, bidx, byte_t) in enumerate(samples):
+            oracle_step(plan[i][0], hosts[i], to_host(dev["g"][i][idx_t]), h,
+                        gidx=idx + offsets[i])
+        torch.cuda.synchronize()
+        for i, (idx, idx_t, bidx, byte_t) in enumerate(samples):
+            hs, (wfmt, blk, cp) = hosts[i], plan[i]
+            tag = f"fp4-master {specs[i].name} t={t}"
+            w_got = to_host(dev["w"][i][byte_t]) if blk else to_host(dev["w"][i][idx_t], np.uint16)
+            assert_state_equal(tag, w_got, hs.w, to_host(dev["m"][i][idx_t]), hs.m,
+                               to_host(dev["v"][i][idx_t]), hs.v, to_host(dev["ve"][i][idx_t]),
+                               hs.ve)
+            if blk:
+                got = to_host(dev["sc"][i][torch.from_numpy(bidx).cuda()])
+                assert (got == hs.scales).all(), tag
+            if cp:
+                assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag
