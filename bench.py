@@ -21,6 +21,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -75,9 +76,23 @@ def traffic_from_profile():
     return float(val.group(1))
 
 
-def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32") -> dict:
-    """The CPU oracle (single thread) on a bounded sample of the workload: the
-    first `sample` elements of the list, `steps` steps."""
+def cpu_threads() -> int:
+    """Host threads for the oracle: this process's CPU set, at most 16 (one
+    GPU's share of the host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads: int = 1) -> dict:
+    """The CPU oracle on a bounded sample of the workload: the first `sample`
+    elements of the list, `steps` steps.  With several threads each runs the
+    unchanged oracle on a contiguous index range (the step is elementwise and
+    its draws are keyed by global index, so the split changes no result)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     import oracle
@@ -96,13 +111,24 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32") -> dict:
     codes = oracle.encode_array(wfmt, np.concatenate(xs))
     grads = [np.concatenate([g[t] for g in gs]) for t in range(steps)]
     m, v, ve = (np.zeros(sample, np.float32 if sfmt == "fp32" else np.uint16) for _ in range(3))
-    t0 = time.perf_counter()
-    for t in range(1, steps + 1):
-        oracle.step(wfmt, codes, grads[t - 1], m, v, ve, W.hparams(cfg, step=t), sfmt=sfmt)
-    dt = time.perf_counter() - t0
-    return {"value": sample * steps / dt / 1e9, "unit": "Gparam/s", "cores": 1, "kind": "oracle",
+    bounds = [(sample * k // threads) // 8 * 8 for k in range(threads)] + [sample]
+
+    def part(k, t, h):
+        lo, hi = bounds[k], bounds[k + 1]
+        oracle.step(wfmt, codes[lo:hi], grads[t - 1][lo:hi], m[lo:hi], v[lo:hi], ve[lo:hi], h,
+                    sfmt=sfmt, index_base=lo)
+
+    with ThreadPoolExecutor(threads) as ex:
+        t0 = time.perf_counter()
+        for t in range(1, steps + 1):
+            h = W.hparams(cfg, step=t)
+            list(ex.map(lambda k: part(k, t, h), range(threads)))
+        dt = time.perf_counter() - t0
+    return {"value": sample * steps / dt / 1e9, "unit": "Gparam/s", "cores": threads,
+            "kind": "oracle",
             "sample": f"first {sample:,} parameters of the list, {steps} steps "
-                      f"({dt:.1f} s, single-threaded scalar C)"}
+                      f"({dt:.1f} s on {threads} thread(s), scalar C, one contiguous index "
+                      "range per thread)"}
 
 
 def main():
@@ -122,7 +148,14 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=None,
                     help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
                          "whose encoding makes the oracle slower)")
+    ap.add_argument("--cpu-threads", type=int, default=None,
+                    help="host threads for the oracle (default: this process's CPUs, at most 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the streaming-ceiling probe (same buffers and bytes, no arithmetic)")
+    ap.add_argument("--shard", default=None, metavar="K/P",
+                    help="time only rank K's contiguous 1/P of the flat list, index base = its "
+                         "first element: one GPU's share under P-way optimizer-state sharding")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="after timing, run one plain device copy of this many GiB (a known "
                          "byte count that calibrates HBM traffic counters in a profiler run)")
@@ -142,6 +175,12 @@ def main():
 
     B.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    shard = None
+    if args.shard:
+        k, p = (int(x) for x in args.shard.split("/"))
+        if not (p >= 1 and 0 <= k < p) or args.weights != "list":
+            sys.exit("--shard K/P needs 0 <= K < P and the plain list (--weights list)")
+        shard = (k, p)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = args.config
@@ -223,11 +262,24 @@ def main():
                           copies=copies) for gl in grad_sets]
     stream = torch.cuda.current_stream()
     step_no = 0
+    lo, hi = 0, nparam
+    if shard:
+        # In the flat layout the global index of an element is its offset, so
+        # a contiguous range is one madd_step call with that offset as base.
+        per = (nparam // shard[1]) // 128 * 128
+        lo = shard[0] * per
+        hi = nparam if shard[0] == shard[1] - 1 else lo + per
+        log(f"shard {shard[0]}/{shard[1]}: elements [{lo:,}, {hi:,})")
 
     def one_step():
         nonlocal step_no
         step_no += 1
-        B.madd_multi_tensor_step(lists[step_no % 2], W.hparams(cfg, step=step_no), stream=stream)
+        h = W.hparams(cfg, step=step_no)
+        if shard:
+            B.madd_step(wbuf[lo:hi], wfmt, gbufs[step_no % 2][lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+                        vebuf[lo:hi], h, index_base=lo, stream=stream)
+        else:
+            B.madd_multi_tensor_step(lists[step_no % 2], h, stream=stream)
 
     for _ in range(args.warmup):
         one_step()
@@ -247,8 +299,30 @@ def main():
     total_ms = ev[0].elapsed_time(ev[-1])
     ms_per_step = total_ms / args.steps
     avg_launch_ms = sum(per_launch_ms) / len(per_launch_ms)
+    median_ms = statistics.median(per_launch_ms)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})"
-        f", launches min {min(per_launch_ms):.3f} max {max(per_launch_ms):.3f} ms")
+        f", launches min {min(per_launch_ms):.3f} median {median_ms:.3f} "
+        f"max {max(per_launch_ms):.3f} ms")
+
+    n_step = hi - lo
+    alg_bytes = 0.0
+    if shard:
+        alg_bytes = n_step * bytes_per_param(wfmt, args.states)
+    else:
+        for n, (wf, blk, cp) in zip(sizes, plan):
+            alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
+            if blk:  # scale read + written: FP16 per 128 (FP8) or E8M0 per 32 (MXFP4)
+                alg_bytes += (n // 32) * 2 if wf == "mxfp4" else (n // 128) * 4
+    bpp = alg_bytes / n_step
+    achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
+
+    ceiling = None
+    if not args.no_ceiling and args.weights == "list" and wfmt == "bf16":
+        ceiling = stream_ceiling(wbuf[lo:hi], gbufs[1][lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+                                 vebuf[lo:hi], 4 if args.states == "fp32" else 2, args.steps,
+                                 stream, alg_bytes, achieved)
+        log(f"streaming ceiling: {ceiling['achieved']:.1f} GB/s; the step reaches "
+            f"{ceiling['step_frac_of_ceiling'] * 100:.1f}% of it")
 
     if args.copy_probe_gib > 0:
         nbytes = int(args.copy_probe_gib * 2**30) // 4 * 4
@@ -260,44 +334,50 @@ def main():
         log(f"copy probe: {nbytes} bytes read + {nbytes} bytes written")
         del src, dst
 
-    alg_bytes = 0.0
-    for n, (wf, blk, cp) in zip(sizes, plan):
-        alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
-        if blk:  # scale read + written: FP16 per 128 (FP8) or E8M0 per 32 (MXFP4)
-            alg_bytes += (n // 32) * 2 if wf == "mxfp4" else (n // 128) * 4
-    bpp = alg_bytes / nparam
-    achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
     traffic = (traffic_from_profile()
-               if (cfg == "c5" and args.states == "fp32" and args.weights == "list") else None)
+               if (cfg == "c5" and args.states == "fp32" and args.weights == "list" and not shard)
+               else None)
+    if shard:
+        kname = (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
+                 f"{W.CONFIGS[cfg]['rounding'].upper()}> on one shard")
+    elif args.weights == "list":
+        kname = (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
+                 f"{W.CONFIGS[cfg]['rounding'].upper()}>")
+    else:
+        low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}[args.weights]
+        kname = (f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches per "
+                 "step; timed together)")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": int(round(alg_bytes)),
-                "kernel": (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
-                           f"{W.CONFIGS[cfg]['rounding'].upper()}>" if args.weights == "list" else
-                           f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches "
-                           "per step; timed together)"),
-                "avg_launch_ms": round(avg_launch_ms, 4)}
+                "kernel": kname, "avg_launch_ms": round(avg_launch_ms, 4)}
 
     cpu = None
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle on a sample")
+        threads = args.cpu_threads or cpu_threads()
+        log(f"timing the CPU oracle on a sample ({threads} threads)")
         steps = args.cpu_steps or (10 if args.states == "fp32" else 4)
-        cpu = cpu_baseline(cfg, args.cpu_sample, steps, args.states)
+        cpu = cpu_baseline(cfg, args.cpu_sample, steps, args.states, threads)
 
+    workload = WORKLOAD_NAMES[cfg]
+    if shard:
+        workload = f"rank {shard[0]} of {shard[1]} contiguous shards of the {workload}"
+    low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}.get(args.weights)
     out = {
         "metric": METRIC,
-        "value": round(nparam / (ms_per_step / 1e3) / 1e9, 3),
+        "value": round(n_step / (ms_per_step / 1e3) / 1e9, 3),
         "unit": "Gparam/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_median": round(median_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": WORKLOAD_NAMES[cfg], "params": nparam, "tensors": len(specs),
+        "config": {"workload": workload, "params": n_step, "tensors": len(specs),
                    "weight_format": wfmt if args.weights == "list" else
                    f"{low} block-scaled linear layers + bf16 compute copies; bf16 "
                    "embed/norms/head",
@@ -306,9 +386,43 @@ def main():
                    "rounding": W.CONFIGS[cfg]["rounding"], "bytes_per_param": round(bpp, 4)},
         "hbm_gbps": round(alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
         "roofline": roofline,
+        "ceiling": ceiling,
         "cpu_baseline": cpu,
     }
+    if shard:
+        out["config"]["index_base"] = lo
     print(json.dumps(out), flush=True)
+
+
+def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_gbs) -> dict:
+    """Time the streaming-ceiling probe (libmadd_ceiling.so) on the step's own
+    buffers: the same bytes and access pattern without the arithmetic."""
+    import ctypes
+
+    import torch
+
+    from paper_2607_10611_amd import _build
+
+    lib = ctypes.CDLL(_build.CEIL_LIB)
+    lib.madd_ceiling_stream.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64,
+                                                                ctypes.c_void_p]
+    lib.madd_ceiling_stream.restype = ctypes.c_int32
+    args = [t.data_ptr() for t in (w, g, m, v, ve)] + [state_bytes, m.numel(), stream.cuda_stream]
+    for _ in range(2):
+        assert lib.madd_ceiling_stream(*args) == 0
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for k in range(steps):
+        assert lib.madd_ceiling_stream(*args) == 0
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[-1]) / steps
+    gbs = alg_bytes / (ms / 1e3) / 1e9
+    return {"kernel": "madd_ceiling_stream (same buffers and bytes, no arithmetic)",
+            "avg_launch_ms": round(ms, 4), "achieved": round(gbs, 1), "unit": "GB/s",
+            "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "step_frac_of_ceiling": round(step_gbs / gbs, 4)}
 
 
 if __name__ == "__main__":

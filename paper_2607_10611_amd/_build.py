@@ -1,4 +1,7 @@
-"""Build of the HIP library ``libmadd.so`` (gfx950), in-tree.
+"""Build of the HIP libraries (gfx950), in-tree: ``libmadd.so`` (the
+optimizer step, include/madd.h) and ``libmadd_ceiling.so`` (the streaming
+ceiling probe the benchmark reports beside the HBM peak,
+include/madd_ceiling.h).
 
 The flags are part of the numerical contract of the kernels:
   * ``-ffp-contract=off``: only the fmaf calls written in the source fuse;
@@ -17,6 +20,10 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "madd.hip")
 HDR = os.path.join(ROOT, "include", "madd.h")
 LIB = os.path.join(PKG, "libmadd.so")
+CEIL_SRC = os.path.join(PKG, "csrc", "stream_ceiling.hip")
+CEIL_HDR = os.path.join(ROOT, "include", "madd_ceiling.h")
+CEIL_LIB = os.path.join(PKG, "libmadd_ceiling.so")
+TARGETS = ((SRC, HDR, LIB), (CEIL_SRC, CEIL_HDR, CEIL_LIB))
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -35,21 +42,25 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile csrc/madd.hip into libmadd.so next to this file; returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    """Compile every library next to this file; returns libmadd.so's path."""
+    for src, _hdr, lib in TARGETS:
+        tmp = lib + ".tmp"
+        cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, src]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, lib)
     return LIB
 
 
 def is_stale() -> bool:
-    if not os.path.exists(LIB):
-        return True
-    t = os.path.getmtime(LIB)
-    return any(os.path.getmtime(p) > t for p in (SRC, HDR))
+    for src, hdr, lib in TARGETS:
+        if not os.path.exists(lib):
+            return True
+        t = os.path.getmtime(lib)
+        if any(os.path.getmtime(p) > t for p in (src, hdr)):
+            return True
+    return False
 
 
 if __name__ == "__main__":

@@ -1,0 +1,114 @@
+// Streaming-ceiling probe for the M+Adam step (declared in
+// include/madd_ceiling.h): the step kernel's bytes and work mapping without
+// its arithmetic.  A workgroup of 256 threads owns 2048 elements; thread t
+// moves elements [4t, 4t+4) of both 1024-element sub-tiles, all loads of a
+// tile issued before any store, every access non-temporal.  Values are
+// XORed with gradient bits masked by a runtime zero, so the stores write
+// back what was read while the compiler must keep every load and store.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "madd_ceiling.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kQuad = 4;
+constexpr int kSub = kThreads * kQuad;
+constexpr int kTile = 2 * kSub;
+
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+#define GLOBAL __attribute__((address_space(1)))
+
+template <typename T>
+__device__ __forceinline__ T ldg(const void* p) {
+  return __builtin_nontemporal_load((const GLOBAL T*)p);
+}
+template <typename T>
+__device__ __forceinline__ void stg(void* p, T x) {
+  __builtin_nontemporal_store(x, (GLOBAL T*)p);
+}
+
+// State lanes of four elements: fp32 (u4) or bf16 codes (u2).
+template <int SB>
+struct StateT;
+template <>
+struct StateT<4> {
+  typedef u4 T;
+  static __device__ __forceinline__ T mix(T x, u4 g, uint32_t mask) { return x ^ (g & mask); }
+};
+template <>
+struct StateT<2> {
+  typedef u2 T;
+  static __device__ __forceinline__ T mix(T x, u4 g, uint32_t mask) {
+    return x ^ (u2{g.x ^ g.y, g.z ^ g.w} & mask);
+  }
+};
+
+template <int SB>
+__global__ __launch_bounds__(kThreads) void ceiling_kernel(void* w, const float* g, void* m,
+                                                           void* v, void* ve, int64_t n,
+                                                           uint32_t mask) {
+  typedef typename StateT<SB>::T S;
+  const int64_t tb = (int64_t)blockIdx.x * kTile;
+  const int64_t eA = tb + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
+  if (eB + kQuad <= n) {
+    u2 wa = ldg<u2>((const uint16_t*)w + eA), wb = ldg<u2>((const uint16_t*)w + eB);
+    const u4 ga = ldg<u4>(g + eA), gb = ldg<u4>(g + eB);
+    S ma = ldg<S>((const uint8_t*)m + eA * SB), mb = ldg<S>((const uint8_t*)m + eB * SB);
+    S va = ldg<S>((const uint8_t*)v + eA * SB), vb = ldg<S>((const uint8_t*)v + eB * SB);
+    S ea = ldg<S>((const uint8_t*)ve + eA * SB), eb = ldg<S>((const uint8_t*)ve + eB * SB);
+    wa ^= u2{ga.x, ga.z} & mask;
+    wb ^= u2{gb.x, gb.z} & mask;
+    stg<u2>((uint16_t*)w + eA, wa);
+    stg<S>((uint8_t*)m + eA * SB, StateT<SB>::mix(ma, ga, mask));
+    stg<S>((uint8_t*)v + eA * SB, StateT<SB>::mix(va, ga, mask));
+    stg<S>((uint8_t*)ve + eA * SB, StateT<SB>::mix(ea, ga, mask));
+    stg<u2>((uint16_t*)w + eB, wb);
+    stg<S>((uint8_t*)m + eB * SB, StateT<SB>::mix(mb, gb, mask));
+    stg<S>((uint8_t*)v + eB * SB, StateT<SB>::mix(vb, gb, mask));
+    stg<S>((uint8_t*)ve + eB * SB, StateT<SB>::mix(eb, gb, mask));
+    return;
+  }
+  // the last, partial tile: element by element
+  for (int half = 0; half < 2; ++half) {
+    const int64_t e0 = half ? eB : eA;
+    for (int64_t i = e0; i < e0 + kQuad && i < n; ++i) {
+      const uint32_t gi = __float_as_uint(g[i]) & mask;
+      ((uint16_t*)w)[i] ^= (uint16_t)gi;
+      if (SB == 4) {
+        ((uint32_t*)m)[i] ^= gi;
+        ((uint32_t*)v)[i] ^= gi;
+        ((uint32_t*)ve)[i] ^= gi;
+      } else {
+        ((uint16_t*)m)[i] ^= (uint16_t)gi;
+        ((uint16_t*)v)[i] ^= (uint16_t)gi;
+        ((uint16_t*)ve)[i] ^= (uint16_t)gi;
+      }
+    }
+  }
+}
+
+bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" int32_t madd_ceiling_stream(void* w, const float* g, void* m, void* v, void* ve,
+                                       int32_t state_bytes, int64_t n, void* stream) {
+  if (n < 0 || (state_bytes != 2 && state_bytes != 4)) return -1;
+  if (n == 0) return 0;
+  if (!w || !g || !m || !v || !ve) return -1;
+  if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve))) return -2;
+  const int64_t tiles = (n + kTile - 1) / kTile;
+  if (tiles > 0x7FFFFFFFll) return -1;
+  hipStream_t st = (hipStream_t)stream;
+  if (state_bytes == 4)
+    hipLaunchKernelGGL(ceiling_kernel<4>, dim3((unsigned)tiles), dim3(kThreads), 0, st, w, g, m,
+                       v, ve, n, 0u);
+  else
+    hipLaunchKernelGGL(ceiling_kernel<2>, dim3((unsigned)tiles), dim3(kThreads), 0, st, w, g, m,
+                       v, ve, n, 0u);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}

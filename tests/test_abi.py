@@ -23,6 +23,33 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(B.EXPORTS)
 
 
+def test_every_header_symbol_is_exported_by_its_library():
+    from paper_2607_10611_amd import _build
+    libs = {"madd.h": _build.LIB, "madd_ceiling.h": _build.CEIL_LIB}
+    headers = sorted(os.listdir(os.path.join(ROOT, "include")))
+    assert sorted(h for h in headers if h.endswith(".h")) == sorted(libs)
+    for h, so in libs.items():
+        text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", h)).read(), flags=re.S)
+        names = set(re.findall(r"\b(madd_\w+)\s*\(", text))
+        assert names, h
+        nm = os.popen(f"nm -D --defined-only {so}").read()
+        for name in names:
+            assert re.search(rf"\bT {name}\b", nm), (h, name)
+
+
+def test_ceiling_probe_rejects_bad_arguments():
+    from paper_2607_10611_amd import _build
+    L = ctypes.CDLL(_build.CEIL_LIB)
+    f = L.madd_ceiling_stream
+    f.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p]
+    f.restype = ctypes.c_int32
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 4, -1, None) == -1
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, 3, 64, None) == -1
+    assert f(None, FAKE, FAKE, FAKE, FAKE, 4, 64, None) == -1
+    assert f(FAKE, FAKE + 4, FAKE, FAKE, FAKE, 4, 64, None) == -2
+    assert f(None, None, None, None, None, 2, 0, None) == 0
+
+
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     for name in declared_functions():
