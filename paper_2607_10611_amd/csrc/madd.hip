@@ -142,13 +142,39 @@ enum : int { SF_FP32 = 0, SF_BF16 = 1 };  // storage of the moments
 
 __device__ __forceinline__ float dec_bf16(uint32_t c) { return __uint_as_float(c << 16); }
 
+// BF16 encoding with gfx950's conversion instructions.  v_cvt_pk_bf16_f32
+// rounds to nearest-even; v_cvt_sr_bf16_f32 adds the high 16 bits of its
+// random operand to the 16 discarded bits and truncates, which with the draw
+// placed there is the stochastic rule above (carry into the kept half with
+// probability low16 / 2^16).  Both match the integer definitions bit for bit
+// on every non-NaN fp32 (checked exhaustively on the device) and turn a NaN
+// into a quieted truncation of it, so a NaN is first replaced by the
+// canonical 0x7FC00000, whose conversion is the canonical code 0x7FC0.
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef short s2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float canon_nan(float x) {
+  return (x == x) ? x : __uint_as_float(0x7FC00000u);
+}
+
+// Two values, `a` in the low half.
+__device__ __forceinline__ uint32_t enc_bf16x2(float a, float b, bool sr, uint32_t ra,
+                                               uint32_t rb) {
+  if (sr) {
+    s2v r = __builtin_amdgcn_cvt_sr_bf16_f32(s2v{0, 0}, canon_nan(a), ra << 16, false);
+    r = __builtin_amdgcn_cvt_sr_bf16_f32(r, canon_nan(b), rb << 16, true);
+    return __builtin_bit_cast(uint32_t, r);
+  }
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{canon_nan(a), canon_nan(b)}, bf2v));
+}
+
 __device__ __forceinline__ uint32_t enc_bf16(float x, bool sr, uint32_t r16) {
-  const uint32_t u = __float_as_uint(x);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
-  // SR: carry into the kept half with probability low16 / 2^16.
-  // RNE: add half an ulp minus one, plus the kept lsb (ties to even).
-  const uint32_t add = sr ? r16 : (0x7FFFu + ((u >> 16) & 1u));
-  return (u + add) >> 16;
+  if (sr) {
+    const s2v r = __builtin_amdgcn_cvt_sr_bf16_f32(s2v{0, 0}, canon_nan(x), r16 << 16, false);
+    return __builtin_bit_cast(uint32_t, r) & 0xFFFFu;
+  }
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)canon_nan(x));
 }
 
 // Minifloat description: M mantissa bits, exponent bias, minimum normal
@@ -160,39 +186,41 @@ struct Mini<WF_E4M3> {
   static constexpr int M = 3, BIAS = 7, EMIN = -6;
   static constexpr float MAXV = 448.0f;
   static constexpr uint32_t MAXCODE = 0x7Eu, NANCODE = 0x7Fu;
+  static constexpr uint32_t RESCALE_BITS = (127u + 127u - 7u) << 23;  // 2^(127 - BIAS)
 };
 template <>
 struct Mini<WF_E5M2> {
   static constexpr int M = 2, BIAS = 15, EMIN = -14;
   static constexpr float MAXV = 57344.0f;
   static constexpr uint32_t MAXCODE = 0x7Bu, NANCODE = 0x7Fu;
+  static constexpr uint32_t RESCALE_BITS = (127u + 127u - 15u) << 23;
 };
 
+// Branch-free decode: the code's exponent and mantissa fields, placed at the
+// top of an fp32's exponent and mantissa fields, read as 2^(E-127) (1.M) for
+// E > 0 and as the fp32 subnormal M 2^(-149+23-M) for E = 0; one multiply by
+// 2^(127 - BIAS) rescales both exactly (fp32 denormals are kept).
 template <int WF>
 __device__ __forceinline__ float dec_fp8(uint32_t c) {
   using F = Mini<WF>;
-  const uint32_t sign = (c & 0x80u) << 24;
-  const uint32_t e = (c >> F::M) & ((0x80u >> F::M) - 1u);
-  const uint32_t mant = c & ((1u << F::M) - 1u);
-  float mag;
-  if (WF == WF_E4M3 && (c & 0x7Fu) == 0x7Fu) {
-    mag = __uint_as_float(0x7FC00000u);
-  } else if (WF == WF_E5M2 && e == 31u) {
-    mag = __uint_as_float(mant ? 0x7FC00000u : 0x7F800000u);
-  } else if (e == 0u) {
-    mag = ldexpf((float)mant, F::EMIN - F::M);
-  } else {
-    mag = __uint_as_float(((e + 127u - F::BIAS) << 23) | (mant << (23 - F::M)));
+  const uint32_t mag = c & 0x7Fu;
+  float v = __uint_as_float(mag << (23 - F::M)) * __uint_as_float(F::RESCALE_BITS);
+  if constexpr (WF == WF_E4M3) {
+    v = (mag == 0x7Fu) ? __uint_as_float(0x7FC00000u) : v;
+  } else {  // E5M2: all-ones exponent is Inf (mantissa 0) or NaN
+    v = (mag >= 0x7Cu) ? __uint_as_float((mag & 3u) ? 0x7FC00000u : 0x7F800000u) : v;
   }
-  return __uint_as_float(__float_as_uint(mag) | sign);
+  return __uint_as_float(__float_as_uint(v) | ((c & 0x80u) << 24));
 }
 
 // Value-domain rounding onto a minifloat grid: scale |x| so that the grid
 // spacing of its binade is 1, round to an integer k (ties to even, or
 // stochastically), and assemble the code from the spacing exponent and k.
 // A k that reaches the next power of two lands on the next binade's code.
+// `val` receives the rounded magnitude k 2^se (exact), for callers that need
+// the stored value as well as its code.
 template <int M, int BIAS, int EMIN>
-__device__ __forceinline__ uint32_t round_mini(float a, bool sr, uint32_t r16) {
+__device__ __forceinline__ uint32_t round_mini(float a, bool sr, uint32_t r16, float& val) {
   const int e = (int)((__float_as_uint(a) >> 23) & 0xFFu) - 127;
   const int se = (e > EMIN ? e : EMIN) - M;  // exponent of the grid spacing
   const float q = ldexpf(a, -se);            // exact; q < 2^(M+1)
@@ -204,19 +232,36 @@ __device__ __forceinline__ uint32_t round_mini(float a, bool sr, uint32_t r16) {
   } else {
     k = rintf(q);
   }
+  val = ldexpf(k, se);
   return ((uint32_t)(se + M + BIAS - 1) << M) + (uint32_t)k;
 }
+template <int M, int BIAS, int EMIN>
+__device__ __forceinline__ uint32_t round_mini(float a, bool sr, uint32_t r16) {
+  float unused;
+  return round_mini<M, BIAS, EMIN>(a, sr, r16, unused);
+}
 
+// Branch-free: |x| is first clamped to the largest finite value (Inf and
+// finite overflow saturate; a NaN takes the clamp's value and is replaced by
+// the NaN code at the end).  The largest value is a grid point of its binade,
+// whose spacing then bounds every rounding of a clamped |x| by it, so no
+// code beyond the largest finite one can arise.
+// `val` receives the value of the returned code.
 template <int WF>
-__device__ __forceinline__ uint32_t enc_fp8(float x, bool sr, uint32_t r16) {
+__device__ __forceinline__ uint32_t enc_fp8(float x, bool sr, uint32_t r16, float& val) {
   using F = Mini<WF>;
   const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
-  const float a = fabsf(x);
-  if (!(a == a)) return F::NANCODE;
-  if (a >= F::MAXV) return sign | F::MAXCODE;  // saturate (Inf included)
-  uint32_t c = round_mini<F::M, F::BIAS, F::EMIN>(a, sr, r16);
-  c = c > F::MAXCODE ? F::MAXCODE : c;
-  return sign | c;
+  float a = fabsf(x);
+  a = a < F::MAXV ? a : F::MAXV;
+  float mag;
+  const uint32_t c = round_mini<F::M, F::BIAS, F::EMIN>(a, sr, r16, mag);
+  val = (x == x) ? __uint_as_float(__float_as_uint(mag) | (sign << 24)) : x;
+  return (x == x) ? (sign | c) : F::NANCODE;
+}
+template <int WF>
+__device__ __forceinline__ uint32_t enc_fp8(float x, bool sr, uint32_t r16) {
+  float unused;
+  return enc_fp8<WF>(x, sr, r16, unused);
 }
 
 // FP16 codes of the block scales (IEEE: RNE, overflow to Inf).
@@ -241,14 +286,21 @@ __device__ __forceinline__ float dec_e2m1(uint32_t c) {
   return (c & 8u) ? -mag : mag;
 }
 
-// x already divided by the block scale and finite; saturates at +-6.
-__device__ __forceinline__ uint32_t enc_e2m1(float x, bool sr, uint32_t r16) {
+// x already divided by the block scale and finite; saturates at +-6 (6 is a
+// grid point, so rounding a clamped |x| never passes code 7).
+// `val` receives the value of the returned code.
+__device__ __forceinline__ uint32_t enc_e2m1(float x, bool sr, uint32_t r16, float& val) {
   const uint32_t sign = (__float_as_uint(x) >> 28) & 0x8u;
-  const float a = fabsf(x);
-  if (a >= 6.0f) return sign | 0x7u;
-  uint32_t c = round_mini<1, 1, 0>(a, sr, r16);  // 1 mantissa bit, bias 1, min exponent 0
-  c = c > 0x7u ? 0x7u : c;
+  float a = fabsf(x);
+  a = a < 6.0f ? a : 6.0f;
+  float mag;
+  const uint32_t c = round_mini<1, 1, 0>(a, sr, r16, mag);  // 1 mantissa bit, bias 1, min exponent 0
+  val = __uint_as_float(__float_as_uint(mag) | (sign << 28));
   return sign | c;
+}
+__device__ __forceinline__ uint32_t enc_e2m1(float x, bool sr, uint32_t r16) {
+  float unused;
+  return enc_e2m1(x, sr, r16, unused);
 }
 
 // E8M0: 2^(c - 127); code 0 is the fp32 subnormal 2^-127; code 255 is NaN.
@@ -445,8 +497,7 @@ __device__ __forceinline__ void st4s(void* p, int64_t e, f4 x) {
   if constexpr (SF == SF_FP32) {
     stg<f4>((float*)p + e, x);
   } else {
-    const u2 r = u2{enc_bf16(x.x, false, 0u) | (enc_bf16(x.y, false, 0u) << 16),
-                    enc_bf16(x.z, false, 0u) | (enc_bf16(x.w, false, 0u) << 16)};
+    const u2 r = u2{enc_bf16x2(x.x, x.y, false, 0u, 0u), enc_bf16x2(x.z, x.w, false, 0u, 0u)};
     stg<u2>((uint16_t*)p + e, r);
   }
 }
@@ -487,13 +538,19 @@ __device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& 
 
 // The bf16 compute copy of four new stored weights (value x scale for
 // block-scaled FP8), rounded to nearest-even.
+// The bf16 compute copy from the four new stored values (block-scaled: payload
+// value already multiplied by the block scale).
+__device__ __forceinline__ void store_copy_values(const float (&v)[4], uint16_t* copy, int64_t e) {
+  stg<u2>(copy + e, u2{enc_bf16x2(v[0], v[1], false, 0u, 0u), enc_bf16x2(v[2], v[3], false, 0u, 0u)});
+}
+
 template <int WF>
 __device__ __forceinline__ void store_copy(const WQuad<WF>& w, float scale, uint16_t* copy,
                                            int64_t e) {
-  uint32_t c[4];
+  float v[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) c[k] = enc_bf16(decode<WF>(w.code(k)) * scale, false, 0u);
-  stg<u2>(copy + e, u2{c[0] | (c[1] << 16), c[2] | (c[3] << 16)});
+  for (int k = 0; k < 4; ++k) v[k] = decode<WF>(w.code(k)) * scale;
+  store_copy_values(v, copy, e);
 }
 
 // Swap a value with the neighbouring lane (DPP quad_perm [1,0,3,2]).
@@ -550,14 +607,20 @@ __device__ __forceinline__ void draws_any(uint64_t g0, const Scalars& s, uint32_
 
 template <int WF, bool SR, bool CLAMP>
 __device__ __forceinline__ void step_quad(Quad<WF>& q, const uint32_t (&r)[4], const Scalars& s) {
+  float wn[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     float m = q.m[k], v = q.v[k], ve = q.ve[k];
-    const float wn = step_elem<CLAMP>(decode<WF>(q.w.code(k)), q.g[k], m, v, ve, s);
+    wn[k] = step_elem<CLAMP>(decode<WF>(q.w.code(k)), q.g[k], m, v, ve, s);
     q.m[k] = m;
     q.v[k] = v;
     q.ve[k] = ve;
-    q.w.set(k, encode<WF>(wn, SR, r[k]));
+  }
+  if constexpr (WF == WF_BF16) {  // two codes per conversion
+    q.w.raw = u2{enc_bf16x2(wn[0], wn[1], SR, r[0], r[1]), enc_bf16x2(wn[2], wn[3], SR, r[2], r[3])};
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) q.w.set(k, encode<WF>(wn[k], SR, r[k]));
   }
 }
 
@@ -669,11 +732,27 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
 template <int WF>
 constexpr int block_len() { return WF == WF_MXFP4 ? kMxBlock : kBlock; }
 
+// Max over aligned groups of LANES lanes (8, or 32): lane swaps within quads
+// (DPP quad_perm [1,0,3,2] and [2,3,0,1]), the mirrored quad of each half row
+// (row_half_mirror), the mirrored half of each row (row_mirror) and the
+// other row of each 32-lane half (ds_swizzle, xor 16).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, false);
+}
 template <int LANES>
 __device__ __forceinline__ uint32_t block_amax(uint32_t a) {
-#pragma unroll
-  for (int off = LANES / 2; off >= 1; off >>= 1) {
-    const uint32_t o = (uint32_t)__shfl_xor((int)a, off, LANES);
+  static_assert(LANES == 8 || LANES == 32, "block lane groups are 8 or 32 lanes");
+  uint32_t o = dpp_u32<0xB1>(a);
+  a = o > a ? o : a;
+  o = dpp_u32<0x4E>(a);
+  a = o > a ? o : a;
+  o = dpp_u32<0x141>(a);
+  a = o > a ? o : a;
+  if constexpr (LANES == 32) {
+    o = dpp_u32<0x140>(a);
+    a = o > a ? o : a;
+    o = (uint32_t)__builtin_amdgcn_ds_swizzle((int)a, 0x401F);  // and 0x1F, xor 0x10
     a = o > a ? o : a;
   }
   return a;
@@ -712,20 +791,31 @@ __device__ __forceinline__ uint32_t step_quad_unrounded(Quad<WF>& q, float sold,
   return amax;
 }
 
+// Re-quantize four new weights of one block; `cv` receives their stored
+// values (payload value x scale) for the compute copy.
 template <int WF, bool SR>
 __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[4], uint32_t amax,
-                                                 const uint32_t (&r)[4]) {
+                                                 const uint32_t (&r)[4], float (&cv)[4]) {
   if constexpr (WF == WF_MXFP4) {
     const uint32_t sc = mx_scale(amax);
-    const float inv = mx_inv_scale(sc);
+    const float inv = mx_inv_scale(sc), X = dec_e8m0(sc);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) q.w.set(k, sc == 0xFFu ? 0u : enc_e2m1(wn[k] * inv, SR, r[k]));
+    for (int k = 0; k < 4; ++k) {
+      float v;
+      const uint32_t c = enc_e2m1(wn[k] * inv, SR, r[k], v);
+      q.w.set(k, sc == 0xFFu ? 0u : c);
+      cv[k] = (sc == 0xFFu ? 0.0f : v) * X;
+    }
     return sc;
   } else {
     const uint32_t sc = block_scale<WF>(amax);
     const float sf = dec_fp16(sc);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) q.w.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k]));
+    for (int k = 0; k < 4; ++k) {
+      float v;
+      q.w.set(k, enc_fp8<WF>(wn[k] / sf, SR, r[k], v));
+      cv[k] = v * sf;
+    }
     return sc;
   }
 }
@@ -759,23 +849,24 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     }
     if (actA)
       amaxA = step_quad_unrounded<WF, SR, CLAMP>(
-          qa, scale_value<WF>(load_scale<WF>(d.scales, eA / kBlk)), wa, s);
+          qa, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk))), wa, s);
     if (actB)
       amaxB = step_quad_unrounded<WF, SR, CLAMP>(
-          qb, scale_value<WF>(load_scale<WF>(d.scales, eB / kBlk)), wb, s);
+          qb, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk))), wb, s);
     amaxA = block_amax<kLanes>(amaxA);
     amaxB = block_amax<kLanes>(amaxB);
+    float cv[4];
     if (actA) {
-      const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA);
+      const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA, cv);
       store_quad<WF, SF>(qa, d, eA);
-      if (COPY && d.copy) store_copy<WF>(qa.w, scale_value<WF>(sc), d.copy, eA);
-      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, eA / kBlk, sc);
+      if (COPY && d.copy) store_copy_values(cv, d.copy, eA);
+      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk), sc);
     }
     if (actB) {
-      const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB);
+      const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB, cv);
       store_quad<WF, SF>(qb, d, eB);
-      if (COPY && d.copy) store_copy<WF>(qb.w, scale_value<WF>(sc), d.copy, eB);
-      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, eB / kBlk, sc);
+      if (COPY && d.copy) store_copy_values(cv, d.copy, eB);
+      if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk), sc);
     }
   }
 }
