@@ -395,7 +395,7 @@ def main():
 
 
 def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_gbs) -> dict:
-    """Time the streaming-ceiling probe (libmadd_ceiling.so) on the step's own
+    """Time the streaming-ceiling probe (libmadd_probes.so) on the step's own
     buffers: the same bytes and access pattern without the arithmetic."""
     import ctypes
 
@@ -403,7 +403,7 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
 
     from paper_2607_10611_amd import _build
 
-    lib = ctypes.CDLL(_build.CEIL_LIB)
+    lib = ctypes.CDLL(_build.PROBE_LIB)
     lib.madd_ceiling_stream.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64,
                                                                 ctypes.c_void_p]
     lib.madd_ceiling_stream.restype = ctypes.c_int32

@@ -1,7 +1,7 @@
 """Build of the HIP libraries (gfx950), in-tree: ``libmadd.so`` (the
-optimizer step, include/madd.h) and ``libmadd_ceiling.so`` (the streaming
-ceiling probe the benchmark reports beside the HBM peak,
-include/madd_ceiling.h).
+optimizer step, include/madd.h) and ``libmadd_probes.so`` (device probes:
+the streaming ceiling the benchmark reports beside the HBM peak, and the
+exhaustive check of the bf16 conversion instructions; include/madd_probes.h).
 
 The flags are part of the numerical contract of the kernels:
   * ``-ffp-contract=off``: only the fmaf calls written in the source fuse;
@@ -20,10 +20,10 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "madd.hip")
 HDR = os.path.join(ROOT, "include", "madd.h")
 LIB = os.path.join(PKG, "libmadd.so")
-CEIL_SRC = os.path.join(PKG, "csrc", "stream_ceiling.hip")
-CEIL_HDR = os.path.join(ROOT, "include", "madd_ceiling.h")
-CEIL_LIB = os.path.join(PKG, "libmadd_ceiling.so")
-TARGETS = ((SRC, HDR, LIB), (CEIL_SRC, CEIL_HDR, CEIL_LIB))
+PROBE_SRC = os.path.join(PKG, "csrc", "probes.hip")
+PROBE_HDR = os.path.join(ROOT, "include", "madd_probes.h")
+PROBE_LIB = os.path.join(PKG, "libmadd_probes.so")
+TARGETS = ((SRC, HDR, LIB), (PROBE_SRC, PROBE_HDR, PROBE_LIB))
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

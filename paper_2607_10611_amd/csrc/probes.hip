@@ -1,6 +1,7 @@
-// Streaming-ceiling probe for the M+Adam step (declared in
-// include/madd_ceiling.h): the step kernel's bytes and work mapping without
-// its arithmetic.  A workgroup of 256 threads owns 2048 elements; thread t
+// Device probes declared in include/madd_probes.h.
+//
+// Streaming-ceiling probe for the M+Adam step: the step kernel's bytes and
+// work mapping without its arithmetic.  A workgroup of 256 threads owns 2048 elements; thread t
 // moves elements [4t, 4t+4) of both 1024-element sub-tiles, all loads of a
 // tile issued before any store, every access non-temporal.  Values are
 // XORed with gradient bits masked by a runtime zero, so the stores write
@@ -8,7 +9,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "madd_ceiling.h"
+#include "madd_probes.h"
 
 namespace {
 
@@ -93,7 +94,59 @@ __global__ __launch_bounds__(kThreads) void ceiling_kernel(void* w, const float*
 
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// bf16 conversion instructions against the integer definitions.
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef short s2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t hash32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7FEB352Du;
+  x ^= x >> 15;
+  x *= 0x846CA68Bu;
+  x ^= x >> 16;
+  return x;
+}
+
+// 65536 workgroups x 256 threads x 256 inputs = 2^32 inputs.
+__global__ __launch_bounds__(256) void bf16_rounding_kernel(unsigned long long* c) {
+  const uint32_t base = ((uint32_t)blockIdx.x * 256u + threadIdx.x) * 256u;
+  unsigned long long rne_bad = 0, sr_bad = 0, nan_bad = 0;
+  for (uint32_t j = 0; j < 256u; ++j) {
+    const uint32_t u = base + j;
+    const float x = __uint_as_float(u);
+    const uint32_t r16 = hash32(u) & 0xFFFFu;
+    const uint32_t hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{x, x}, bf2v)) & 0xFFFFu;
+    const uint32_t hs = __builtin_bit_cast(
+        uint32_t, __builtin_amdgcn_cvt_sr_bf16_f32(s2v{0, 0}, x, r16 << 16, false)) & 0xFFFFu;
+    if ((u & 0x7FFFFFFFu) <= 0x7F800000u) {
+      rne_bad += hw != ((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+      sr_bad += hs != ((u + r16) >> 16);
+    }
+  }
+  if (blockIdx.x == 0) {  // the canonical NaN under every 16-bit draw
+    const float q = __uint_as_float(0x7FC00000u);
+    for (uint32_t r = threadIdx.x; r < 65536u; r += 256u) {
+      const uint32_t hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{q, q}, bf2v)) & 0xFFFFu;
+      const uint32_t hs = __builtin_bit_cast(
+          uint32_t, __builtin_amdgcn_cvt_sr_bf16_f32(s2v{0, 0}, q, r << 16, false)) & 0xFFFFu;
+      nan_bad += (hw != 0x7FC0u) + (hs != 0x7FC0u);
+    }
+  }
+  if (rne_bad) atomicAdd(&c[0], rne_bad);
+  if (sr_bad) atomicAdd(&c[1], sr_bad);
+  if (nan_bad) atomicAdd(&c[2], nan_bad);
+  if (threadIdx.x == 0) atomicAdd(&c[3], 256ull * 256ull);  // this workgroup's inputs
+}
+
 }  // namespace
+
+extern "C" int32_t madd_probe_bf16_rounding(uint64_t* counters, void* stream) {
+  if (!counters) return -1;
+  hipLaunchKernelGGL(bf16_rounding_kernel, dim3(65536), dim3(256), 0, (hipStream_t)stream,
+                     (unsigned long long*)counters);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
 
 extern "C" int32_t madd_ceiling_stream(void* w, const float* g, void* m, void* v, void* ve,
                                        int32_t state_bytes, int64_t n, void* stream) {

@@ -25,7 +25,7 @@ def test_header_declares_the_boundary():
 
 def test_every_header_symbol_is_exported_by_its_library():
     from paper_2607_10611_amd import _build
-    libs = {"madd.h": _build.LIB, "madd_ceiling.h": _build.CEIL_LIB}
+    libs = {"madd.h": _build.LIB, "madd_probes.h": _build.PROBE_LIB}
     headers = sorted(os.listdir(os.path.join(ROOT, "include")))
     assert sorted(h for h in headers if h.endswith(".h")) == sorted(libs)
     for h, so in libs.items():
@@ -39,7 +39,7 @@ def test_every_header_symbol_is_exported_by_its_library():
 
 def test_ceiling_probe_rejects_bad_arguments():
     from paper_2607_10611_amd import _build
-    L = ctypes.CDLL(_build.CEIL_LIB)
+    L = ctypes.CDLL(_build.PROBE_LIB)
     f = L.madd_ceiling_stream
     f.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p]
     f.restype = ctypes.c_int32
@@ -48,6 +48,9 @@ def test_ceiling_probe_rejects_bad_arguments():
     assert f(None, FAKE, FAKE, FAKE, FAKE, 4, 64, None) == -1
     assert f(FAKE, FAKE + 4, FAKE, FAKE, FAKE, 4, 64, None) == -2
     assert f(None, None, None, None, None, 2, 0, None) == 0
+    L.madd_probe_bf16_rounding.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    L.madd_probe_bf16_rounding.restype = ctypes.c_int32
+    assert L.madd_probe_bf16_rounding(None, None) == -1
 
 
 def test_library_exports_every_declared_symbol():

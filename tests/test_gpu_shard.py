@@ -91,7 +91,7 @@ def test_eight_shards_equal_one_call_llama_1b():
 
 
 def _ceiling():
-    L = ctypes.CDLL(_build.CEIL_LIB)
+    L = ctypes.CDLL(_build.PROBE_LIB)
     f = L.madd_ceiling_stream
     f.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p]
     f.restype = ctypes.c_int32
