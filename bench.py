@@ -34,7 +34,7 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
 
 WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5}
-SBYTES = {"fp32": 4, "bf16": 2}
+SBYTES = {"fp32": 4, "bf16": 2, "bf16-sr": 2}
 
 
 def bytes_per_param(wfmt: str, sfmt: str) -> float:
@@ -137,8 +137,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c5", choices=sorted(WORKLOAD_NAMES))
-    ap.add_argument("--states", default="fp32", choices=["fp32", "bf16"],
-                    help="storage of m, v, v_e (bf16: the paper's optimizer-state precision)")
+    ap.add_argument("--states", default="fp32", choices=["fp32", "bf16", "bf16-sr"],
+                    help="storage of m, v, v_e (bf16: the paper's optimizer-state precision, "
+                         "rounded to nearest; bf16-sr: rounded stochastically)")
     ap.add_argument("--weights", default="list", choices=["list", "fp8-master", "fp4-master"],
                     help="list: the configuration's weight format for every tensor; fp8-master: "
                          "linear layers block-scaled E4M3 with bf16 compute copies, embeddings, "
@@ -258,8 +259,9 @@ def main():
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
         f"{time.perf_counter() - t0:.1f} s")
 
+    sfmt = args.states.replace("-", "_")
     lists = [B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
-                          copies=copies) for gl in grad_sets]
+                          copies=copies, sfmt=sfmt) for gl in grad_sets]
     stream = torch.cuda.current_stream()
     step_no = 0
     lo, hi = 0, nparam
@@ -277,7 +279,7 @@ def main():
         h = W.hparams(cfg, step=step_no)
         if shard:
             B.madd_step(wbuf[lo:hi], wfmt, gbufs[step_no % 2][lo:hi], mbuf[lo:hi], vbuf[lo:hi],
-                        vebuf[lo:hi], h, index_base=lo, stream=stream)
+                        vebuf[lo:hi], h, index_base=lo, sfmt=sfmt, stream=stream)
         else:
             B.madd_multi_tensor_step(lists[step_no % 2], h, stream=stream)
 
@@ -357,7 +359,7 @@ def main():
         threads = args.cpu_threads or cpu_threads()
         log(f"timing the CPU oracle on a sample ({threads} threads)")
         steps = args.cpu_steps or (10 if args.states == "fp32" else 4)
-        cpu = cpu_baseline(cfg, args.cpu_sample, steps, args.states, threads)
+        cpu = cpu_baseline(cfg, args.cpu_sample, steps, sfmt, threads)
 
     workload = WORKLOAD_NAMES[cfg]
     if shard:

@@ -88,13 +88,18 @@ typedef enum madd_wfmt {
 typedef enum madd_gfmt { MADD_G_FP32 = 0, MADD_G_BF16 = 1 } madd_gfmt;
 
 /* Storage of the moments m, v, v_e.
- *   FP32 : float arrays.
- *   BF16 : bfloat16 codes -- the precision of the optimizer states in the
- *          paper's per-parameter memory accounting (Appendix, memory
- *          comparison table).  A step decodes them exactly, computes in FP32,
- *          uses the FP32 results within the step and stores them rounded to
- *          nearest (ties to even). */
-typedef enum madd_sfmt { MADD_S_FP32 = 0, MADD_S_BF16 = 1 } madd_sfmt;
+ *   FP32    : float arrays.
+ *   BF16    : bfloat16 codes -- the precision of the optimizer states in the
+ *             paper's per-parameter memory accounting (Appendix, memory
+ *             comparison table).  A step decodes them exactly, computes in
+ *             FP32, uses the FP32 results within the step and stores them
+ *             rounded to nearest (ties to even).
+ *   BF16_SR : bfloat16 codes as BF16, stored with stochastic rounding (the
+ *             rule of madd_round) instead; m, v and v_e of the element with
+ *             global index i draw from Philox streams 1, 2 and 3 (counter
+ *             word 3) at the step's seed and t, independently of the weight's
+ *             stream 0 and of hp->rounding. */
+typedef enum madd_sfmt { MADD_S_FP32 = 0, MADD_S_BF16 = 1, MADD_S_BF16_SR = 2 } madd_sfmt;
 
 /* Rounding of the new weight into its storage format.
  *   RNE : round to nearest, ties to even.

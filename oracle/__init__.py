@@ -44,7 +44,7 @@ _LIB = os.path.join(_HERE, "libmadd_oracle.so")
 # format / rounding numbering of the oracle's C interface
 FMT = {"bf16": 0, "e4m3": 1, "e5m2": 2, "fp32": 3, "fp16": 4, "e2m1": 5, "e8m0": 6}
 GFMT = {"fp32": 0, "bf16": 1}
-SFMT = {"fp32": 0, "bf16": 1}
+SFMT = {"fp32": 0, "bf16": 1, "bf16_sr": 2}
 ROUND = {"rne": 0, "sr": 1}
 
 _CODE_DTYPE = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,

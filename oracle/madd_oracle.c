@@ -70,7 +70,8 @@
  *     optimizer states in the paper's memory accounting table).  With bf16
  *     storage the step decodes them exactly, computes in fp32 as above, uses
  *     the fp32 results within the step and stores them rounded to nearest
- *     (ties to even).
+ *     (ties to even), or stochastically by the rule above with the draws of
+ *     streams 1 (m), 2 (v) and 3 (v_e) of the same generator.
  *   - Block-scaled FP8: contiguous blocks of 128 elements, one FP16 scale s
  *     per block, weight = q * s (fp32 product).  After the update,
  *     amax = max|w'| over the block; s' = RNE_fp16(amax / FMAX) with
@@ -97,7 +98,9 @@
 enum { OF_BF16 = 0, OF_E4M3 = 1, OF_E5M2 = 2, OF_FP32 = 3, OF_FP16 = 4, OF_E2M1 = 5, OF_NFMT = 6,
        OF_E8M0 = 6 };
 enum { OG_FP32 = 0, OG_BF16 = 1 };
-enum { OS_FP32 = 0, OS_BF16 = 1 }; /* storage of the moments m, v, v_e */
+/* storage of the moments m, v, v_e: fp32, bf16 rounded to nearest-even, or
+ * bf16 rounded stochastically (draws on streams 1, 2, 3 for m, v, v_e) */
+enum { OS_FP32 = 0, OS_BF16 = 1, OS_BF16_SR = 2 };
 enum { OR_RNE = 0, OR_SR = 1 };
 
 enum {
@@ -445,20 +448,25 @@ static float load_state(int sfmt, const void *a, int64_t i) {
   return (float)decode(OF_BF16, ((const uint16_t *)a)[i]);
 }
 
-/* Store a moment: fp32 as is, or rounded to bf16 (nearest, ties to even). */
-static void store_state(int sfmt, void *a, int64_t i, float x) {
+/* Store a moment: fp32 as is, or rounded to bf16 -- to nearest (ties to
+ * even), or stochastically with the 16-bit draw r16. */
+static void store_state(int sfmt, void *a, int64_t i, float x, uint32_t r16) {
   if (sfmt == OS_FP32) ((float *)a)[i] = x;
-  else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);
+  else if (sfmt == OS_BF16) ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);
+  else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, r16);
 }
 
-/* One element: load the three moments, step, store them back. */
+/* One element: load the three moments, step, store them back.  With
+ * stochastically rounded bf16 moments, moment k (m, v, v_e) of the element
+ * with global index idx draws from stream 1 + k at the step's (seed, t). */
 static float step_stored(float w, float g, int sfmt, void *m, void *v, void *ve, int64_t i,
-                         const oscal *s) {
+                         const oscal *s, const ohp *h, int64_t idx) {
   float mi = load_state(sfmt, m, i), vi = load_state(sfmt, v, i), vei = load_state(sfmt, ve, i);
   const float wn = oracle_step_elem(w, g, &mi, &vi, &vei, s);
-  store_state(sfmt, m, i, mi);
-  store_state(sfmt, v, i, vi);
-  store_state(sfmt, ve, i, vei);
+  const int sr = sfmt == OS_BF16_SR;
+  store_state(sfmt, m, i, mi, sr ? draw16(h->seed, h->step, 1u, idx) : 0u);
+  store_state(sfmt, v, i, vi, sr ? draw16(h->seed, h->step, 2u, idx) : 0u);
+  store_state(sfmt, ve, i, vei, sr ? draw16(h->seed, h->step, 3u, idx) : 0u);
   return wn;
 }
 
@@ -519,15 +527,15 @@ int oracle_step(int wfmt, void *w, uint16_t *copy, int gfmt, const void *g, int 
     return ORACLE_EINVAL;
   if (wfmt != OF_BF16 && wfmt != OF_E4M3 && wfmt != OF_E5M2 && wfmt != OF_FP32) return ORACLE_EINVAL;
   if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
-  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
   if (n < 0) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
   for (int64_t i = 0; i < n; ++i) {
     const float wv = (float)decode(wfmt, load_code(wfmt, w, i));
     const float gv = load_grad(gfmt, g, i);
-    const float wn = step_stored(wv, gv, sfmt, m, v, ve, i, &s);
     const int64_t idx = gidx ? gidx[i] : index_base + i;
+    const float wn = step_stored(wv, gv, sfmt, m, v, ve, i, &s, &h, idx);
     const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
     const uint32_t code = encode(wfmt, wn, h.rounding, r16);
     store_code(wfmt, w, i, code);
@@ -572,7 +580,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, uint16_t *copy, in
     return ORACLE_EINVAL;
   if (wfmt != OF_E4M3 && wfmt != OF_E5M2) return ORACLE_EINVAL;
   if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
-  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
   if (n < 0 || n % BLOCK != 0) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
@@ -583,7 +591,7 @@ int oracle_step_block(int wfmt, uint8_t *q, uint16_t *scales, uint16_t *copy, in
       const int64_t i = b * BLOCK + k;
       const float wv = (float)decode(wfmt, q[i]) * sold;
       const float gv = load_grad(gfmt, g, i);
-      wn[k] = step_stored(wv, gv, sfmt, m, v, ve, i, &s);
+      wn[k] = step_stored(wv, gv, sfmt, m, v, ve, i, &s, &h, gidx ? gidx[i] : index_base + i);
     }
     const uint16_t snew = block_scale(wfmt, wn);
     const float sf = (float)decode(OF_FP16, snew);
@@ -690,7 +698,7 @@ int oracle_step_mx(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const 
               w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
     return ORACLE_EINVAL;
   if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
-  if (sfmt != OS_FP32 && sfmt != OS_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
   if (n < 0 || n % MX_BLOCK != 0) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
@@ -699,7 +707,8 @@ int oracle_step_mx(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const 
     for (int k = 0; k < MX_BLOCK; ++k) {
       const int64_t i = b * MX_BLOCK + k;
       const float wv = mx_value(mx_get(q, i), scales[b]);
-      wn[k] = step_stored(wv, load_grad(gfmt, g, i), sfmt, m, v, ve, i, &s);
+      wn[k] = step_stored(wv, load_grad(gfmt, g, i), sfmt, m, v, ve, i, &s, &h,
+                          gidx ? gidx[i] : index_base + i);
     }
     const int se = mx_scale_exp(wn);
     const uint32_t sc = mx_scale_code(se);

@@ -24,8 +24,8 @@ WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32,
         "mxfp4": W_MXFP4}
 MX_BLOCK = 32  # elements per MXFP4 block (one E8M0 scale byte)
 GFMT = {"fp32": G_FP32, "bf16": G_BF16}
-S_FP32, S_BF16 = 0, 1
-SFMT = {"fp32": S_FP32, "bf16": S_BF16}
+S_FP32, S_BF16, S_BF16_SR = 0, 1, 2
+SFMT = {"fp32": S_FP32, "bf16": S_BF16, "bf16_sr": S_BF16_SR}
 ROUND = {"rne": ROUND_RNE, "sr": ROUND_SR}
 
 STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPORTED",
@@ -151,7 +151,8 @@ def _hp(hp) -> madd_hparams:
 
 def state_format(t) -> str:
     """Moment storage of a torch tensor: float32 -> "fp32"; bfloat16 (or its
-    16-bit integer view) -> "bf16"."""
+    16-bit integer view) -> "bf16" (pass sfmt="bf16_sr" explicitly for
+    stochastically rounded bf16 moments)."""
     import torch
     if t.dtype == torch.float32:
         return "fp32"

@@ -117,9 +117,11 @@ __device__ __forceinline__ u4 philox10(u4 c, uint32_t k0, uint32_t k1) {
   return c;
 }
 
-// 128 random bits for the group of eight elements j = idx >> 3.
-__device__ __forceinline__ u4 draw_group(uint64_t j, const Scalars& s) {
-  return philox10(u4{(uint32_t)j, (uint32_t)(j >> 32), s.t, 0u}, s.key0, s.key1);
+// 128 random bits for the group of eight elements j = idx >> 3 on a stream:
+// 0 rounds the weights, 1, 2, 3 the stochastically rounded bf16 moments
+// m, v, v_e.
+__device__ __forceinline__ u4 draw_group(uint64_t j, const Scalars& s, uint32_t stream = 0u) {
+  return philox10(u4{(uint32_t)j, (uint32_t)(j >> 32), s.t, stream}, s.key0, s.key1);
 }
 
 __device__ __forceinline__ uint32_t lane16(u4 r, uint32_t lane) {
@@ -128,8 +130,8 @@ __device__ __forceinline__ uint32_t lane16(u4 r, uint32_t lane) {
 }
 
 // 16-bit draw of a single element.
-__device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s) {
-  return lane16(draw_group(idx >> 3, s), (uint32_t)(idx & 7u));
+__device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s, uint32_t stream = 0u) {
+  return lane16(draw_group(idx >> 3, s, stream), (uint32_t)(idx & 7u));
 }
 
 // ---------------------------------------------------------------------------
@@ -138,7 +140,9 @@ __device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s) {
 
 enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3, WF_MXFP4 = 4 };
 enum : int { GF_FP32 = 0, GF_BF16 = 1 };
-enum : int { SF_FP32 = 0, SF_BF16 = 1 };  // storage of the moments
+// storage of the moments: fp32, bf16 rounded to nearest-even, bf16 rounded
+// stochastically (streams 1, 2, 3)
+enum : int { SF_FP32 = 0, SF_BF16 = 1, SF_BF16_SR = 2 };
 
 __device__ __forceinline__ float dec_bf16(uint32_t c) { return __uint_as_float(c << 16); }
 
@@ -481,7 +485,7 @@ __device__ __forceinline__ void st1w(void* p, int64_t e, uint32_t c) {
 }
 
 // Moments as stored: fp32, or bf16 codes (decoded exactly; stored rounded to
-// nearest, ties to even).
+// nearest, ties to even, or stochastically with the given draws).
 template <int SF>
 __device__ __forceinline__ f4 ld4s(const void* p, int64_t e) {
   if constexpr (SF == SF_FP32) {
@@ -493,11 +497,13 @@ __device__ __forceinline__ f4 ld4s(const void* p, int64_t e) {
   }
 }
 template <int SF>
-__device__ __forceinline__ void st4s(void* p, int64_t e, f4 x) {
+__device__ __forceinline__ void st4s(void* p, int64_t e, f4 x, const uint32_t (&r16)[4]) {
   if constexpr (SF == SF_FP32) {
     stg<f4>((float*)p + e, x);
   } else {
-    const u2 r = u2{enc_bf16x2(x.x, x.y, false, 0u, 0u), enc_bf16x2(x.z, x.w, false, 0u, 0u)};
+    constexpr bool sr = SF == SF_BF16_SR;
+    const u2 r = u2{enc_bf16x2(x.x, x.y, sr, r16[0], r16[1]),
+                    enc_bf16x2(x.z, x.w, sr, r16[2], r16[3])};
     stg<u2>((uint16_t*)p + e, r);
   }
 }
@@ -507,10 +513,15 @@ __device__ __forceinline__ float ld1s(const void* p, int64_t e) {
   else return dec_bf16(((const uint16_t*)p)[e]);
 }
 template <int SF>
-__device__ __forceinline__ void st1s(void* p, int64_t e, float x) {
+__device__ __forceinline__ void st1s(void* p, int64_t e, float x, uint32_t r16) {
   if constexpr (SF == SF_FP32) ((float*)p)[e] = x;
-  else ((uint16_t*)p)[e] = (uint16_t)enc_bf16(x, false, 0u);
+  else ((uint16_t*)p)[e] = (uint16_t)enc_bf16(x, SF == SF_BF16_SR, r16);
 }
+
+// The draws of the three moments of four elements (stochastic bf16 moments).
+struct MDraws {
+  uint32_t m[4], v[4], ve[4];
+};
 
 // One sub-tile's worth of a thread's inputs: four consecutive elements.
 template <int WF>
@@ -529,11 +540,12 @@ __device__ __forceinline__ void load_quad(Quad<WF>& q, const TensorDesc& d, int6
 }
 
 template <int WF, int SF>
-__device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& d, int64_t e) {
+__device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& d, int64_t e,
+                                           const MDraws& md) {
   q.w.store(d.w, e);
-  st4s<SF>(d.m, e, q.m);
-  st4s<SF>(d.v, e, q.v);
-  st4s<SF>(d.ve, e, q.ve);
+  st4s<SF>(d.m, e, q.m, md.m);
+  st4s<SF>(d.v, e, q.v, md.v);
+  st4s<SF>(d.ve, e, q.ve, md.ve);
 }
 
 // The bf16 compute copy of four new stored weights (value x scale for
@@ -564,13 +576,13 @@ __device__ __forceinline__ uint32_t swap_lane_pair(uint32_t x) {
 // Every lane of the wave must call this (lane swap).
 template <bool SR>
 __device__ __forceinline__ void draws_aligned(uint64_t gA, const Scalars& s, uint32_t (&rA)[4],
-                                              uint32_t (&rB)[4]) {
+                                              uint32_t (&rB)[4], uint32_t stream = 0u) {
   if constexpr (!SR) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) rA[k] = rB[k] = 0u;
   } else {
     const bool odd = (threadIdx.x & 1u) != 0u;
-    const u4 P = draw_group((gA >> 3) + (odd ? (uint64_t)(kSub / 8) : 0u), s);
+    const u4 P = draw_group((gA >> 3) + (odd ? (uint64_t)(kSub / 8) : 0u), s, stream);
     // even lane keeps words x,y of its A block and sends z,w; odd lane keeps
     // z,w of its B block and sends x,y
     const uint32_t r0 = swap_lane_pair(odd ? P.x : P.z);
@@ -584,24 +596,44 @@ __device__ __forceinline__ void draws_aligned(uint64_t gA, const Scalars& s, uin
 
 // Draws of four consecutive elements starting at an arbitrary global index.
 template <bool SR>
-__device__ __forceinline__ void draws_any(uint64_t g0, const Scalars& s, uint32_t (&r)[4]) {
+__device__ __forceinline__ void draws_any(uint64_t g0, const Scalars& s, uint32_t (&r)[4],
+                                          uint32_t stream = 0u) {
   if constexpr (!SR) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) r[k] = 0u;
   } else {
     const uint32_t off = (uint32_t)(g0 & 7u);
-    const u4 a = draw_group(g0 >> 3, s);
+    const u4 a = draw_group(g0 >> 3, s, stream);
     if (off <= 4u) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) r[k] = lane16(a, off + (uint32_t)k);
     } else {
-      const u4 b = draw_group((g0 >> 3) + 1u, s);
+      const u4 b = draw_group((g0 >> 3) + 1u, s, stream);
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const uint32_t l = off + (uint32_t)k;
         r[k] = l < 8u ? lane16(a, l) : lane16(b, l - 8u);
       }
     }
+  }
+}
+
+// Moment draws of a lane pair's A and B groups (see draws_aligned; every lane
+// of the pair must call), or of four elements at any index.
+template <int SF>
+__device__ __forceinline__ void mdraws_aligned(uint64_t gA, const Scalars& s, MDraws& a, MDraws& b) {
+  if constexpr (SF == SF_BF16_SR) {
+    draws_aligned<true>(gA, s, a.m, b.m, 1u);
+    draws_aligned<true>(gA, s, a.v, b.v, 2u);
+    draws_aligned<true>(gA, s, a.ve, b.ve, 3u);
+  }
+}
+template <int SF>
+__device__ __forceinline__ void mdraws_any(uint64_t g0, const Scalars& s, MDraws& a) {
+  if constexpr (SF == SF_BF16_SR) {
+    draws_any<true>(g0, s, a.m, 1u);
+    draws_any<true>(g0, s, a.v, 2u);
+    draws_any<true>(g0, s, a.ve, 3u);
   }
 }
 
@@ -649,13 +681,15 @@ __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b
     const float w = decode<WF>(ld1w<WF>(d.w, i));
     const float g = ld1g<GF>(d.g, i);
     const float wn = step_elem<CLAMP>(w, g, m, v, ve, s);
-    const uint32_t r16 = SR ? draw_one((uint64_t)(d.gbase + i), s) : 0u;
+    const uint64_t gi = (uint64_t)(d.gbase + i);
+    const uint32_t r16 = SR ? draw_one(gi, s) : 0u;
     const uint32_t code = encode<WF>(wn, SR, r16);
     st1w<WF>(d.w, i, code);
     if (COPY && d.copy) d.copy[i] = (uint16_t)enc_bf16(decode<WF>(code), false, 0u);
-    st1s<SF>(d.m, i, m);
-    st1s<SF>(d.v, i, v);
-    st1s<SF>(d.ve, i, ve);
+    constexpr bool ssr = SF == SF_BF16_SR;
+    st1s<SF>(d.m, i, m, ssr ? draw_one(gi, s, 1u) : 0u);
+    st1s<SF>(d.v, i, v, ssr ? draw_one(gi, s, 2u) : 0u);
+    st1s<SF>(d.ve, i, ve, ssr ? draw_one(gi, s, 3u) : 0u);
   }
 }
 
@@ -677,8 +711,13 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
       if (eB < cend) step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
       continue;
     }
-    const bool fullA = eA + kQuad <= cend, fullB = eB + kQuad <= cend;
+    // Whole quads, decided per lane pair: lanes 2k and 2k+1 exchange halves of
+    // their Philox blocks over a DPP swap, so both must take the same branch.
+    const int64_t pA = tb + 2 * kQuad * (int64_t)(threadIdx.x >> 1), pB = pA + kSub;
+    const bool fullA = pA + 2 * kQuad <= cend, fullB = pB + 2 * kQuad <= cend;
+    const uint64_t gpair = (uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1);
     Quad<WF> qa, qb;
+    MDraws mA, mB;
     if (fullA && fullB) {
       // Both sub-tiles whole (every tile but a tensor's last): loads grouped
       // by array, so a wave's two requests to one array are adjacent spans.
@@ -693,29 +732,31 @@ __global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* _
       qa.ve = ld4s<SF>(d.ve, eA);
       qb.ve = ld4s<SF>(d.ve, eB);
       uint32_t rA[4], rB[4];
-      draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+      draws_aligned<SR>(gpair, s, rA, rB);
+      mdraws_aligned<SF>(gpair, s, mA, mB);
       step_quad<WF, SR, CLAMP>(qa, rA, s);
-      store_quad<WF, SF>(qa, d, eA);
+      store_quad<WF, SF>(qa, d, eA, mA);
       if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
       step_quad<WF, SR, CLAMP>(qb, rB, s);
-      store_quad<WF, SF>(qb, d, eB);
+      store_quad<WF, SF>(qb, d, eB, mB);
       if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
       continue;
     }
     if (fullA) load_quad<WF, GF, SF>(qa, d, eA);
     if (fullB) load_quad<WF, GF, SF>(qb, d, eB);
     uint32_t rA[4], rB[4];
-    draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+    draws_aligned<SR>(gpair, s, rA, rB);
+    mdraws_aligned<SF>(gpair, s, mA, mB);
     if (fullA) {
       step_quad<WF, SR, CLAMP>(qa, rA, s);
-      store_quad<WF, SF>(qa, d, eA);
+      store_quad<WF, SF>(qa, d, eA, mA);
       if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
     } else if (eA < cend) {
       step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
     }
     if (fullB) {
       step_quad<WF, SR, CLAMP>(qb, rB, s);
-      store_quad<WF, SF>(qb, d, eB);
+      store_quad<WF, SF>(qb, d, eB, mB);
       if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
     } else if (eB < cend) {
       step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
@@ -841,11 +882,16 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     if (actA) load_quad<WF, GF, SF>(qa, d, eA);
     if (actB) load_quad<WF, GF, SF>(qb, d, eB);
     uint32_t rA[4], rB[4];
+    MDraws mA, mB;
     if (d.vec_ok) {  // uniform: index base a multiple of 8
-      draws_aligned<SR>((uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1), s, rA, rB);
+      const uint64_t gpair = (uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1);
+      draws_aligned<SR>(gpair, s, rA, rB);
+      mdraws_aligned<SF>(gpair, s, mA, mB);
     } else {
       draws_any<SR>((uint64_t)(d.gbase + eA), s, rA);
       draws_any<SR>((uint64_t)(d.gbase + eB), s, rB);
+      mdraws_any<SF>((uint64_t)(d.gbase + eA), s, mA);
+      mdraws_any<SF>((uint64_t)(d.gbase + eB), s, mB);
     }
     if (actA)
       amaxA = step_quad_unrounded<WF, SR, CLAMP>(
@@ -858,13 +904,13 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     float cv[4];
     if (actA) {
       const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA, cv);
-      store_quad<WF, SF>(qa, d, eA);
+      store_quad<WF, SF>(qa, d, eA, mA);
       if (COPY && d.copy) store_copy_values(cv, d.copy, eA);
       if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk), sc);
     }
     if (actB) {
       const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB, cv);
-      store_quad<WF, SF>(qb, d, eB);
+      store_quad<WF, SF>(qb, d, eB, mB);
       if (COPY && d.copy) store_copy_values(cv, d.copy, eB);
       if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk), sc);
     }
@@ -1013,8 +1059,12 @@ step_fn pick_sr(bool sr, bool clamp, bool copy, bool blk) {
 }
 template <int WF, int GF>
 step_fn pick_sf(int sf, bool sr, bool clamp, bool copy, bool blk) {
-  return sf == SF_FP32 ? pick_sr<WF, GF, SF_FP32>(sr, clamp, copy, blk)
-                       : pick_sr<WF, GF, SF_BF16>(sr, clamp, copy, blk);
+  switch (sf) {
+    case SF_FP32: return pick_sr<WF, GF, SF_FP32>(sr, clamp, copy, blk);
+    case SF_BF16: return pick_sr<WF, GF, SF_BF16>(sr, clamp, copy, blk);
+    case SF_BF16_SR: return pick_sr<WF, GF, SF_BF16_SR>(sr, clamp, copy, blk);
+    default: return nullptr;
+  }
 }
 template <int WF>
 step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
@@ -1042,7 +1092,7 @@ bool needs_clamp(const madd_hparams& hp) {
 
 bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_MXFP4; }
 bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
-bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16; }
+bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16 || f == MADD_S_BF16_SR; }
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int32_t check_hparams(const madd_hparams* hp) {

@@ -55,8 +55,8 @@ def assert_state_equal(tag, w_gpu, w_ref, m_gpu, m_ref, v_gpu, v_ref, ve_gpu, ve
         assert d.max() <= max_ulp, f"{tag}: {name} max ulp {d.max()} at {np.argmax(d)}"
 
 
-STATE_T = {"fp32": torch.float32, "bf16": torch.int16}
-STATE_NP = {"fp32": np.float32, "bf16": np.uint16}
+STATE_T = {"fp32": torch.float32, "bf16": torch.int16, "bf16_sr": torch.int16}
+STATE_NP = {"fp32": np.float32, "bf16": np.uint16, "bf16_sr": np.uint16}
 
 
 class DevState:

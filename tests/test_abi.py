@@ -103,7 +103,7 @@ def test_step_rejects_bad_arguments():
     assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 0, 8, 0) == -1           # null v
     assert call(FAKE, 9, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad wfmt
     assert call(FAKE, 0, None, FAKE, 5, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad gfmt
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 2, 8, 0) == -1           # bad sfmt
+    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 3, 8, 0) == -1           # bad sfmt
     assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, -3) == -1          # base < 0
     assert call(FAKE, 0, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0) == -1         # scales + bf16
     assert call(FAKE, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 100, 0) == -1         # n % 128

@@ -99,7 +99,8 @@ def test_encode_matches_oracle():
 
 
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
-                                                 ("sr", "bf16", True), ("rne", "bf16", False)])
+                                                 ("sr", "bf16", True), ("rne", "bf16", False),
+                                                 ("sr", "bf16_sr", True)])
 def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
     # five whole 2048-element tiles, then 3 blocks of a sixth
     run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)

@@ -160,6 +160,33 @@ def test_bf16_moments(wfmt, n):
     run_pair(wfmt, n, 4, 43 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16", index_base=16)
 
 
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3"])
+@pytest.mark.parametrize("n,base", [(1036, 0), (2047, 8), (4095, 2 ** 33 + 16),
+                                    (3 * 2048 + 1024 + 20, 64)])
+def test_aligned_ragged_tails_split_lane_pairs(wfmt, n, base):
+    """Aligned index bases with a last tile that ends inside a lane pair's
+    group of sub-tile B: the pair must take the per-element path together
+    (the two lanes share Philox blocks)."""
+    run_pair(wfmt, n, 3, 70 + n, dict(rounding="sr", seed=91), index_base=base)
+
+
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "fp32"])
+@pytest.mark.parametrize("n,base", [(9, 16), (2047, 16), (3 * 8192 + 24, 16), (5000, 3)])
+def test_bf16_sr_moments(wfmt, n, base):
+    run_pair(wfmt, n, 4, 60 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16_sr", index_base=base)
+
+
+def test_bf16_sr_moments_with_nearest_weights_and_bf16_gradients():
+    run_pair("bf16", 3 * 8192 + 100, 3, 62, dict(rounding="rne", seed=5), gfmt="bf16",
+             sfmt="bf16_sr", index_base=8)
+
+
+@pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
+def test_block_scaled_fp8_bf16_sr_moments(wfmt):
+    run_pair(wfmt, 2 * 8192 + 5 * 128, 3, 63, dict(rounding="sr"), block=True, copy=True,
+             sfmt="bf16_sr")
+
+
 @pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "e5m2", "fp32"])
 @pytest.mark.parametrize("n", [13, 2048 + 4, 2 * 8192 + 40])
 def test_compute_copy(wfmt, n):
@@ -209,6 +236,27 @@ def test_unaligned_buffers_take_the_scalar_path():
                            to_host(mbuf)[1:], hs.m, to_host(vbuf)[1:], hs.v, to_host(vebuf)[1:],
                            hs.ve)
         assert to_host(mbuf)[0] == 0.0  # untouched neighbour
+
+
+def test_unaligned_buffers_bf16_sr_moments():
+    # the per-element path's moment draws (streams 1-3)
+    n = 3000
+    rng = np.random.default_rng(62)
+    codes = encode_both("bf16", random_weights(rng, n + 1, "bf16"))
+    wbuf = to_dev(codes)
+    mbuf, vbuf, vebuf = (torch.zeros(n + 1, dtype=torch.int16, device="cuda") for _ in range(3))
+    hs = HostState(codes[1:], n, sfmt="bf16_sr")
+    for t in range(1, 4):
+        g = random_grad(rng, n + 1)
+        gd = to_dev(g)
+        h = hp(step=t, rounding="sr", seed=99)
+        B.madd_step(wbuf[1:], "bf16", gd[1:], mbuf[1:], vbuf[1:], vebuf[1:], h, index_base=8,
+                    sfmt="bf16_sr")
+        oracle_step("bf16", hs, np.ascontiguousarray(g[1:]), h, index_base=8)
+        torch.cuda.synchronize()
+        assert_state_equal(f"unaligned bf16_sr t={t}", to_host(wbuf, np.uint16)[1:], hs.w,
+                           to_host(mbuf, np.uint16)[1:], hs.m, to_host(vbuf, np.uint16)[1:], hs.v,
+                           to_host(vebuf, np.uint16)[1:], hs.ve)
 
 
 def test_nonfinite_gradients():
@@ -335,7 +383,7 @@ def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096, sfmt="fp32"):
         gs.append(torch.empty(s.numel, device="cuda"))
         samples.append((idx, idx_t))
         hosts.append(HostState(codes_ref, idx.size, sfmt=sfmt))
-    tl = B.TensorList(ws, [wfmt] * len(ws), gs, ms, vs, ves)
+    tl = B.TensorList(ws, [wfmt] * len(ws), gs, ms, vs, ves, sfmt=sfmt)
     for t in range(1, steps + 1):
         for i in range(len(specs)):
             W.grad_fp32_device_(cfg, i, t, gs[i])
@@ -371,6 +419,10 @@ def test_config4_llama_1b_fp8_sampled(wfmt):
 
 def test_config3_llama_1b_bf16_moments_sampled():
     assert run_list_sampled("c3", 5, sfmt="bf16") == 1_100_048_384
+
+
+def test_config3_llama_1b_bf16_sr_moments_sampled():
+    assert run_list_sampled("c3", 4, sfmt="bf16_sr") == 1_100_048_384
 
 
 def test_config5_llama_7b_sampled():

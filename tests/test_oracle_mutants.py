@@ -47,8 +47,12 @@ MUTANTS = {
     "eps0 sign": ("double ulo = -(h->r_max - h->eps0)", "double ulo = -(h->r_max + h->eps0)"),
     "block scale constant": ("const float ratio = (float)amax / fp8_max(fmt);",
                              "const float ratio = (float)amax / 256.0f;"),
-    "bf16 moments truncated": ("else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);",
-                               "else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, 0u);"),
+    "bf16 moments truncated": (
+        "else if (sfmt == OS_BF16) ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, 0u);",
+        "else if (sfmt == OS_BF16) ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, 0u);"),
+    "stochastic bf16 moments rounded to nearest": (
+        "else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_SR, r16);",
+        "else ((uint16_t *)a)[i] = (uint16_t)encode(OF_BF16, x, OR_RNE, r16);"),
     "compute copy of the unrounded weight": (
         "    if (copy) copy[i] = compute_copy((float)decode(wfmt, code));",
         "    if (copy) copy[i] = compute_copy(wn);"),
@@ -69,6 +73,10 @@ MUTANTS = {
         "const float wv = (float)decode(OF_E2M1, mx_get(q, i));"),
     "MX compute copy without the scale": ("if (copy) copy[i] = compute_copy(mx_value(c, sc));",
                                           "if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, c));"),
+    "moment draws on the weight stream": ("sr ? draw16(h->seed, h->step, 1u, idx) : 0u",
+                                          "sr ? draw16(h->seed, h->step, 0u, idx) : 0u"),
+    "v and v_e share a stream": ("sr ? draw16(h->seed, h->step, 3u, idx) : 0u",
+                                 "sr ? draw16(h->seed, h->step, 2u, idx) : 0u"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }

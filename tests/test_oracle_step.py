@@ -426,6 +426,59 @@ def test_bf16_moments_are_fp32_step_then_nearest_rounding(wfmt):
         del w32
 
 
+def _bf16_sr_bits(x: np.ndarray, r16: np.ndarray) -> np.ndarray:
+    """bf16 stochastic rounding at the bit level: add the 16-bit draw to the
+    16 bits that are cut off, then truncate (finite inputs)."""
+    u = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + r16.astype(np.uint64)) >> 16).astype(np.uint16)
+
+
+def test_bf16_sr_moments_use_streams_1_2_3_and_the_bit_level_rule():
+    # Weights as with fp32 moments; each new moment is the fp32 moment rounded
+    # stochastically with the draw of stream 1 (m), 2 (v), 3 (v_e) at the
+    # element's global index.
+    rng = np.random.default_rng(9)
+    n, base, seed = 4000, 777, 12345
+    codes = oracle.encode_array("bf16", rng.normal(0, 0.02, n).astype(np.float32))
+    ms = [np.zeros(n, np.uint16) for _ in range(3)]
+    for t in range(1, 4):
+        g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-5, -2, n)).astype(np.float32)
+        h = hp(step=t, rounding="sr", seed=seed)
+        c32 = codes.copy()
+        f32 = [oracle.decode_array("bf16", a).astype(np.float32) for a in ms]
+        oracle.step("bf16", c32, g, *f32, h, index_base=base)
+        oracle.step("bf16", codes, g, *ms, h, sfmt="bf16_sr", index_base=base)
+        assert (codes == c32).all()
+        for k, (a, b) in enumerate(zip(ms, f32)):
+            r16 = np.array([oracle.draw16(seed, t, 1 + k, base + i) for i in range(n)], np.uint32)
+            assert (a == _bf16_sr_bits(b, r16)).all(), (t, k)
+
+
+def test_bf16_sr_moments_are_unbiased_and_independent_across_streams():
+    rng = np.random.default_rng(10)
+    n = 60000
+    codes = oracle.encode_array("bf16", rng.normal(0, 0.02, n).astype(np.float32))
+    g = (rng.normal(0, 1, n) * 1e-3).astype(np.float32)
+    ms = [np.zeros(n, np.uint16) for _ in range(3)]
+    f32 = [np.zeros(n, np.float32) for _ in range(3)]
+    oracle.step("bf16", codes.copy(), g, *f32, hp(rounding="sr", seed=4))
+    oracle.step("bf16", codes, g, *ms, hp(rounding="sr", seed=4), sfmt="bf16_sr")
+    ups = []
+    for a, b in zip(ms, f32):
+        lo = b.view(np.uint32) >> 16                        # truncation (finite, >= 0 here)
+        frac = (b.view(np.uint32) & 0xFFFF) / 65536.0       # position between the neighbours
+        up = a.astype(np.uint32) == lo + 1
+        assert ((a == lo) | up).all()
+        inexact = frac > 0
+        # E[up] = frac: the mean of (up - frac) is within 5 sigma of 0
+        d = up[inexact] - frac[inexact]
+        sd = np.sqrt(np.sum(frac[inexact] * (1 - frac[inexact]))) / inexact.sum()
+        assert abs(d.mean()) < 5 * sd
+        ups.append(up)
+    # the three streams make different decisions
+    assert (ups[0] != ups[1]).mean() > 0.2 and (ups[1] != ups[2]).mean() > 0.2
+
+
 # --------------------------------------------------------------------------
 # Appendix B's moment-free rules
 # --------------------------------------------------------------------------
