@@ -14,6 +14,8 @@ from __future__ import annotations
 
 import os
 import subprocess
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -41,15 +43,30 @@ def hipcc() -> str:
     return "hipcc"
 
 
+NPARTS = 8  # csrc/madd.hip is compiled as parts 0..7 (-DMADD_PART=k), in parallel
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
 def build(verbose: bool = False) -> str:
     """Compile every library next to this file; returns libmadd.so's path."""
-    for src, _hdr, lib in TARGETS:
-        tmp = lib + ".tmp"
-        cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, src]
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True)
-        os.replace(tmp, lib)
+    inc = ["-I", os.path.join(ROOT, "include")]
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    with tempfile.TemporaryDirectory(prefix="madd_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, f"madd_part{k}.o") for k in range(NPARTS)]
+        cmds = [[hipcc(), *compile_flags, *inc, f"-DMADD_PART={k}", "-c", "-o", objs[k], SRC]
+                for k in range(NPARTS)]
+        cmds.append([hipcc(), *HIPCC_FLAGS, *inc, "-o", PROBE_LIB + ".tmp", PROBE_SRC])
+        workers = max(1, min(len(cmds), os.cpu_count() or 1))
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(lambda c: _run(c, verbose), cmds))
+        _run([hipcc(), *HIPCC_FLAGS, "-o", LIB + ".tmp", *objs], verbose)
+    os.replace(LIB + ".tmp", LIB)
+    os.replace(PROBE_LIB + ".tmp", PROBE_LIB)
     return LIB
 
 

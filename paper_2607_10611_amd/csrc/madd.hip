@@ -46,7 +46,17 @@
 
 #include "madd.h"
 
-namespace {
+// The library is built from this one source compiled as several parts
+// (-DMADD_PART=k, in parallel): part 0 holds the host code, the ABI and the
+// set-up kernels; parts 1-7 each instantiate the step kernels of one weight
+// format (block-scaled FP8 separately from unscaled).  Without MADD_PART
+// everything is compiled as one unit.
+#ifndef MADD_PART
+#define MADD_PART -1
+#endif
+#define MADD_IN_PART(k) (MADD_PART < 0 || MADD_PART == (k))
+
+namespace madd_detail {
 
 constexpr int kThreads = 256;
 constexpr int kQuad = 4;                     // consecutive elements per thread and sub-tile
@@ -693,8 +703,15 @@ __device__ __forceinline__ void step_scalar_range(const TensorDesc& d, int64_t b
   }
 }
 
+// Waves per SIMD the step kernel asks the compiler for: with bf16 moments
+// (rounded to nearest, no compute copy) the step is bound by VALU issue and
+// fits a fifth wave (at most 96 VGPRs) without spilling; elsewhere the
+// compiler's own choice stands (a tighter bound spills).
+template <int SF, bool COPY>
+constexpr int kStepWaves = (SF == SF_BF16 && !COPY) ? 5 : 1;
+
 template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
-__global__ __launch_bounds__(kThreads) void madd_step_kernel(const TensorDesc* __restrict__ table,
+__global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_kernel(const TensorDesc* __restrict__ table,
                                                              int ntab, TensorDesc single,
                                                              Scalars s) {
   const int64_t chunk = blockIdx.x;
@@ -1000,6 +1017,7 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
   }
 }
 
+#if MADD_IN_PART(0)
 // One thread per 32-element MXFP4 block.
 __global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __restrict__ x,
                                                              uint8_t* q, uint8_t* scales,
@@ -1022,6 +1040,7 @@ __global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __rest
     scales[b] = (uint8_t)sc;
   }
 }
+#endif  // MADD_IN_PART(0)
 
 // ---------------------------------------------------------------------------
 // Host side
@@ -1029,59 +1048,100 @@ __global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __rest
 
 typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
 
-template <int WF, int GF, int SF, bool SR, bool CLAMP>
-step_fn pick_copy(bool copy, bool blk) {
-  if constexpr (WF == WF_MXFP4) {
-    if (!blk) return nullptr;  // MXFP4 is always block-scaled
+// Kernel instantiation for (weight format, block-scaled; gradient and moment
+// formats, rounding, optional clamps present, compute copies present).
+template <int WF, bool BLK, int GF, int SF, bool SR, bool CLAMP>
+step_fn pick_copy(bool copy) {
+  if constexpr (BLK)
     return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
                 : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
-  } else {
-    if constexpr (WF == WF_E4M3 || WF == WF_E5M2) {
-      if (blk)
-        return copy ? madd_step_block_kernel<WF, GF, SF, SR, CLAMP, true>
-                    : madd_step_block_kernel<WF, GF, SF, SR, CLAMP, false>;
-    } else {
-      if (blk) return nullptr;  // no block-scaled form of BF16 or FP32
-    }
+  else
     return copy ? madd_step_kernel<WF, GF, SF, SR, CLAMP, true>
                 : madd_step_kernel<WF, GF, SF, SR, CLAMP, false>;
-  }
 }
-template <int WF, int GF, int SF, bool SR>
-step_fn pick_clamp(bool clamp, bool copy, bool blk) {
-  return clamp ? pick_copy<WF, GF, SF, SR, true>(copy, blk)
-               : pick_copy<WF, GF, SF, SR, false>(copy, blk);
+template <int WF, bool BLK, int GF, int SF, bool SR>
+step_fn pick_clamp(bool clamp, bool copy) {
+  return clamp ? pick_copy<WF, BLK, GF, SF, SR, true>(copy)
+               : pick_copy<WF, BLK, GF, SF, SR, false>(copy);
 }
-template <int WF, int GF, int SF>
-step_fn pick_sr(bool sr, bool clamp, bool copy, bool blk) {
-  return sr ? pick_clamp<WF, GF, SF, true>(clamp, copy, blk)
-            : pick_clamp<WF, GF, SF, false>(clamp, copy, blk);
+template <int WF, bool BLK, int GF, int SF>
+step_fn pick_sr(bool sr, bool clamp, bool copy) {
+  return sr ? pick_clamp<WF, BLK, GF, SF, true>(clamp, copy)
+            : pick_clamp<WF, BLK, GF, SF, false>(clamp, copy);
 }
-template <int WF, int GF>
-step_fn pick_sf(int sf, bool sr, bool clamp, bool copy, bool blk) {
+template <int WF, bool BLK, int GF>
+step_fn pick_sf(int sf, bool sr, bool clamp, bool copy) {
   switch (sf) {
-    case SF_FP32: return pick_sr<WF, GF, SF_FP32>(sr, clamp, copy, blk);
-    case SF_BF16: return pick_sr<WF, GF, SF_BF16>(sr, clamp, copy, blk);
-    case SF_BF16_SR: return pick_sr<WF, GF, SF_BF16_SR>(sr, clamp, copy, blk);
+    case SF_FP32: return pick_sr<WF, BLK, GF, SF_FP32>(sr, clamp, copy);
+    case SF_BF16: return pick_sr<WF, BLK, GF, SF_BF16>(sr, clamp, copy);
+    case SF_BF16_SR: return pick_sr<WF, BLK, GF, SF_BF16_SR>(sr, clamp, copy);
     default: return nullptr;
   }
 }
-template <int WF>
-step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
-  return gf == GF_FP32 ? pick_sf<WF, GF_FP32>(sf, sr, clamp, copy, blk)
-                       : pick_sf<WF, GF_BF16>(sf, sr, clamp, copy, blk);
+template <int WF, bool BLK>
+step_fn pick_gf(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return gf == GF_FP32 ? pick_sf<WF, BLK, GF_FP32>(sf, sr, clamp, copy)
+                       : pick_sf<WF, BLK, GF_BF16>(sf, sr, clamp, copy);
 }
 
-// Kernel instantiation for (weight, gradient and moment formats, rounding,
+// One entry point per part; each instantiates one (weight format, scaled)
+// family of step kernels.
+step_fn pick_part1(int gf, int sf, bool sr, bool clamp, bool copy);  // bf16
+step_fn pick_part2(int gf, int sf, bool sr, bool clamp, bool copy);  // e4m3
+step_fn pick_part3(int gf, int sf, bool sr, bool clamp, bool copy);  // e4m3, block-scaled
+step_fn pick_part4(int gf, int sf, bool sr, bool clamp, bool copy);  // e5m2
+step_fn pick_part5(int gf, int sf, bool sr, bool clamp, bool copy);  // e5m2, block-scaled
+step_fn pick_part6(int gf, int sf, bool sr, bool clamp, bool copy);  // fp32 passthrough
+step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy);  // mxfp4 (block-scaled)
+
+#if MADD_IN_PART(1)
+step_fn pick_part1(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_BF16, false>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(2)
+step_fn pick_part2(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_E4M3, false>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(3)
+step_fn pick_part3(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_E4M3, true>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(4)
+step_fn pick_part4(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_E5M2, false>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(5)
+step_fn pick_part5(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_E5M2, true>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(6)
+step_fn pick_part6(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_FP32, false>(gf, sf, sr, clamp, copy);
+}
+#endif
+#if MADD_IN_PART(7)
+step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_MXFP4, true>(gf, sf, sr, clamp, copy);
+}
+#endif
+
+#if MADD_IN_PART(0)
+// The step kernel for (weight, gradient and moment formats, rounding,
 // optional clamps present, compute copies present, block-scaled); nullptr for
-// combinations that do not exist.
+// combinations that do not exist (block scaling is for FP8 and MXFP4 only,
+// and MXFP4 is always block-scaled).
 step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
   switch (wf) {
-    case WF_BF16: return pick_gf<WF_BF16>(gf, sf, sr, clamp, copy, blk);
-    case WF_E4M3: return pick_gf<WF_E4M3>(gf, sf, sr, clamp, copy, blk);
-    case WF_E5M2: return pick_gf<WF_E5M2>(gf, sf, sr, clamp, copy, blk);
-    case WF_FP32: return pick_gf<WF_FP32>(gf, sf, sr, clamp, copy, blk);
-    case WF_MXFP4: return pick_gf<WF_MXFP4>(gf, sf, sr, clamp, copy, blk);
+    case WF_BF16: return blk ? nullptr : pick_part1(gf, sf, sr, clamp, copy);
+    case WF_E4M3: return blk ? pick_part3(gf, sf, sr, clamp, copy) : pick_part2(gf, sf, sr, clamp, copy);
+    case WF_E5M2: return blk ? pick_part5(gf, sf, sr, clamp, copy) : pick_part4(gf, sf, sr, clamp, copy);
+    case WF_FP32: return blk ? nullptr : pick_part6(gf, sf, sr, clamp, copy);
+    case WF_MXFP4: return blk ? pick_part7(gf, sf, sr, clamp, copy) : nullptr;
     default: return nullptr;
   }
 }
@@ -1242,11 +1302,15 @@ int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const 
   return MADD_OK;
 }
 
-}  // namespace
+#endif  // MADD_IN_PART(0)
+}  // namespace madd_detail
 
+#if MADD_IN_PART(0)
 // ---------------------------------------------------------------------------
 // C ABI
 // ---------------------------------------------------------------------------
+
+using namespace madd_detail;
 
 extern "C" {
 
@@ -1434,3 +1498,4 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
 }
 
 }  // extern "C"
+#endif  // MADD_IN_PART(0)
