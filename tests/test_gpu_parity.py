@@ -211,9 +211,27 @@ def test_block_scaled_fp8_bf16_moments(wfmt):
 
 @pytest.mark.parametrize("kw", [dict(g_max=0.5), dict(d_mult_max=0.05), dict(w_max=0.03),
                                 dict(eps0=0.2), dict(bias_correction=0),
-                                dict(lr_add=0.0), dict(lr_mul=0.0), dict(beta1=0.0, beta2=0.0)])
+                                dict(lr_add=0.0), dict(lr_mul=0.0), dict(lr_add=0.0, lr_mul=0.0),
+                                dict(beta1=0.0, beta2=0.0)])
 def test_algorithm2_options(kw):
     run_pair("bf16", 10000, 3, 51, {**dict(rounding="sr", lr_mul=5e-3), **kw})
+
+
+def test_last_step_counters():
+    """t = 2^32 - 2 and 2^32 - 1, the largest step counters: the bias
+    corrections are 1 in fp32 and the Philox counter's step word is all ones."""
+    n = 2 * 8192 + 40
+    rng = np.random.default_rng(64)
+    codes = encode_both("bf16", random_weights(rng, n, "bf16"))
+    ds, hs = DevState("bf16", codes, n), HostState(codes, n)
+    for t in (2 ** 32 - 2, 2 ** 32 - 1):
+        g = random_grad(rng, n)
+        h = hp(step=t, rounding="sr", seed=2 ** 63 + 11)
+        gpu_step(ds, to_dev(g), h, index_base=8)
+        oracle_step("bf16", hs, g, h, index_base=8)
+        torch.cuda.synchronize()
+        w_g, m_g, v_g, ve_g = ds.host()
+        assert_state_equal(f"t={t}", w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
 
 
 def test_unaligned_buffers_take_the_scalar_path():
@@ -402,6 +420,36 @@ def run_list_sampled(cfg, steps, wfmt=None, per_tensor=4096, sfmt="fp32"):
                                    to_host(ms[i][idx_t], sn), hs.m, to_host(vs[i][idx_t], sn),
                                    hs.v, to_host(ves[i][idx_t], sn), hs.ve)
     return offsets[-1]
+
+
+def test_one_tensor_past_2pow32_elements():
+    """Maximum sizes: one madd_step call over 2^32 + 4196 elements (byte offsets
+    past 16 GiB, chunk indices past 2^21), checked on samples at the start,
+    across element 2^32 and at the ragged end."""
+    n = 2 ** 32 + 4196
+    free, _ = torch.cuda.mem_get_info()
+    assert free > n * 24 + (1 << 30), "needs about 100 GiB of device memory"
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    w = torch.empty(n, dtype=torch.int16, device="cuda")
+    x = torch.randn(n, device="cuda", generator=gen).mul_(0.02)
+    B.madd_encode_weights(x, w, "bf16")
+    del x
+    m, v, ve = (torch.zeros(n, device="cuda") for _ in range(3))
+    idx = np.concatenate([np.arange(0, 3000), np.arange(2 ** 32 - 1500, 2 ** 32 + 1500),
+                          np.arange(n - 3000, n)])
+    idx_t = torch.from_numpy(idx).cuda()
+    hs = HostState(to_host(w[idx_t], np.uint16), idx.size)
+    base = 2 ** 20
+    for t in (1, 2):
+        g = torch.randn(n, device="cuda", generator=gen).mul_(1e-3)
+        h = hp(step=t, rounding="sr", seed=17)
+        B.madd_step(w, "bf16", g, m, v, ve, h, index_base=base)
+        oracle_step("bf16", hs, to_host(g[idx_t]), h, gidx=idx + base)
+        torch.cuda.synchronize()
+        assert_state_equal(f"2^32+ t={t}", to_host(w[idx_t], np.uint16), hs.w, to_host(m[idx_t]),
+                           hs.m, to_host(v[idx_t]), hs.v, to_host(ve[idx_t]), hs.ve)
+        del g
 
 
 def test_config2_gpt2_small_100_steps_sampled():

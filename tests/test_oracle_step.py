@@ -479,6 +479,25 @@ def test_bf16_sr_moments_are_unbiased_and_independent_across_streams():
     assert (ups[0] != ups[1]).mean() > 0.2 and (ups[1] != ups[2]).mean() > 0.2
 
 
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "e5m2"])
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_zero_learning_rates_keep_every_finite_weight(wfmt, rounding):
+    # eta_a = eta_m = 0: both updates are zero, w' = w exactly (a stored
+    # value is on the grid, so either rounding returns it); the moments still
+    # follow the gradients.
+    rng = np.random.default_rng(11)
+    n = 4000
+    x = rng.normal(0, 0.5, n).astype(np.float32)
+    x[:5] = [0.0, -0.0, 1e-30, -3.0, 2.0 ** -20]
+    codes = oracle.encode_array(wfmt, x)
+    before = oracle.decode_array(wfmt, codes)
+    m, v, ve = (np.zeros(n, np.float32) for _ in range(3))
+    g = rng.normal(0, 1e-2, n).astype(np.float32)
+    oracle.step(wfmt, codes, g, m, v, ve, hp(lr_add=0.0, lr_mul=0.0, rounding=rounding, seed=3))
+    assert (oracle.decode_array(wfmt, codes) == before).all()
+    assert np.allclose(m, np.float32(0.1) * g, rtol=1e-6) and (v > 0).mean() > 0.99
+
+
 # --------------------------------------------------------------------------
 # Appendix B's moment-free rules
 # --------------------------------------------------------------------------
