@@ -341,6 +341,42 @@ def test_multi_tensor_mixed_list_matches_oracle_and_single_calls():
                 assert (to_host(d.scales, np.uint16) == hs.scales).all()
 
 
+def test_descriptor_table_cache_eviction():
+    """More distinct tensor lists than the library caches (32): each new list
+    uploads a table, the least recently used one is evicted after the device
+    drains, and a list whose table was evicted is uploaded again on its next
+    call.  Every step must still match single calls."""
+    rng = np.random.default_rng(83)
+    lists = []
+    for k in range(40):
+        sizes = (256 + 8 * k, 1000 + k)
+        devs, singles = [], []
+        for j, n in enumerate(sizes):
+            codes = oracle.encode_array("bf16", random_weights(rng, n, "bf16"))
+            devs.append(DevState("bf16", codes, n))
+            singles.append(DevState("bf16", codes, n))
+        gs = [to_dev(random_grad(rng, n)) for n in sizes]
+        tl = B.TensorList([d.w for d in devs], ["bf16"] * 2, gs, [d.m for d in devs],
+                          [d.v for d in devs], [d.ve for d in devs])
+        lists.append((sizes, devs, singles, gs, tl))
+    order = list(range(40)) + [0, 1, 39, 5]
+    steps = {}
+    for k in order:
+        sizes, devs, singles, gs, tl = lists[k]
+        t = steps[k] = steps.get(k, 0) + 1
+        h = hp(step=t, rounding="sr", seed=k)
+        B.madd_multi_tensor_step(tl, h, index_base=64)
+        off = 64
+        for d1, g, n in zip(singles, gs, sizes):
+            gpu_step(d1, g, h, index_base=off)
+            off += n
+    torch.cuda.synchronize()
+    for sizes, devs, singles, gs, tl in lists:
+        for d, d1 in zip(devs, singles):
+            for a, b in zip(d.host(), d1.host()):
+                assert a.tobytes() == b.tobytes()
+
+
 def test_init_state_zeroes():
     n = 70001
     ts = [torch.full((n + 1,), 3.0, device="cuda") for _ in range(3)]
