@@ -170,9 +170,10 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
  * copy    : NULL, or a device array of n bf16 codes that receives the compute
  *           copy of the new weights: each new stored value (payload x scale
  *           when block-scaled) rounded to nearest-even -- the BF16 copy the
- *           next step's GEMMs read, refreshed by dequantization after every
- *           update in the paper's FP8-master dataflow (Appendix figure), here
- *           written by the same pass.  16-byte aligned for the fast path.
+ *           next step's GEMMs read, which the paper's FP8-master dataflow
+ *           (Appendix figure) rebuilds from the stored weights after every
+ *           update; here the same pass writes it.  16-byte aligned for the
+ *           fast path.
  * scales  : NULL, or the block scales of block-scaled FP8 or MXFP4 as in
  *           madd_encode_weights (required for MXFP4): the weight is
  *           payload * scale (fp32 product); after the update each block's

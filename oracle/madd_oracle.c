@@ -64,8 +64,9 @@
  *     as 0x7FC00000.
  *   - Compute copy (optional): after the update, the BF16 value of each stored
  *     weight (payload x scale for block-scaled FP8), rounded to nearest-even,
- *     for the GEMMs of the next step (the FP8-master dataflow figure refreshes
- *     a BF16 compute copy by dequantization each step).
+ *     for the GEMMs of the next step (in the FP8-master dataflow figure the
+ *     BF16 copy the GEMMs read is rebuilt from the stored FP8 weights after
+ *     every step).
  *   - Moments m, v, v_e are stored in fp32, or in bf16 (the precision of the
  *     optimizer states in the paper's memory accounting table).  With bf16
  *     storage the step decodes them exactly, computes in fp32 as above, uses
