@@ -84,6 +84,16 @@
  *     define the format): the OCP MX block format MXFP4 -- 32-element blocks
  *     of E2M1 values with one E8M0 power-of-two scale; rule at oracle_step_mx.
  *
+ * Pin status (tests/test_oracle_*.py; a mutation test checks the pins catch
+ * planted mistakes): the real-number update is pinned by closed forms, the
+ * Adam limit, limits and invariants; the codecs by library conversions, the
+ * OCP value tables and brute force; Philox by published known-answer vectors.
+ * Parity unpinned against the paper, because the paper does not fix them:
+ * the exact fp32 operation order (a contract shared with the kernel), the
+ * block-scaled FP8 block length and scale rule, the 4-bit format (MXFP4,
+ * pinned to the OCP specification instead), and the stochastic-rounding rule
+ * and its generator (pinned to their own definitions).
+ *
  * Codec implementation: values are decoded from the (sign, exponent,
  * mantissa) definition of each format; encoding searches the sorted table of
  * decoded grid values for the neighbours of |x| and decides with exact double
