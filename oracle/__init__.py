@@ -19,6 +19,8 @@ What each function follows in the paper:
   * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
                        E8M0 scale per 32 elements; the format stands in for
                        the 4-bit master weights of Section 4.2).
+  * ``step_nv``     -- the same step on NVFP4 storage (E2M1 payloads, one E4M3
+                       scale per 16 elements, one fp32 scale per tensor).
   * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
                        storage formats' value grids.
   * ``philox`` / ``draw16`` -- the counter-based generator that keys
@@ -97,6 +99,10 @@ def lib():
         L.oracle_step_mx.restype = I
         L.oracle_encode_mx.argtypes = [P, P, P, I64]
         L.oracle_encode_mx.restype = I
+        L.oracle_step_nv.argtypes = [P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_nv.restype = I
+        L.oracle_encode_nv.argtypes = [P, P, P, I64]
+        L.oracle_encode_nv.restype = I
         L.oracle_decode.argtypes = [I, U32]
         L.oracle_decode.restype = D
         L.oracle_encode.argtypes = [I, ctypes.c_float, I, U32]
@@ -218,6 +224,45 @@ def encode_mx(x: np.ndarray):
     if lib().oracle_encode_mx(_ptr(x), _ptr(q), _ptr(s), x.size) != 0:
         raise OracleError("oracle_encode_mx failed")
     return q, s
+
+
+def step_nv(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray,
+            ve: np.ndarray, hp: dict, gfmt: str = "fp32", index_base: int = 0,
+            gidx: np.ndarray | None = None, sfmt: str = "fp32", copy: np.ndarray | None = None):
+    """NVFP4 step: ``q`` holds n/2 bytes, ``scales`` 4 + n/16 bytes (the fp32
+    per-tensor scale, then one E4M3 code per 16 elements)."""
+    n = 2 * q.size
+    if q.dtype != np.uint8 or scales.dtype != np.uint8 or scales.size != 4 + n // 16:
+        raise OracleError("q must be n/2 packed bytes and scales 4 + n/16 bytes")
+    _check_state(n, g, m, v, ve, gfmt, sfmt)
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+        assert gidx.size == n
+    _check_copy(copy, n)
+    rc = lib().oracle_step_nv(_ptr(q), _ptr(scales), _ptr(copy), GFMT[gfmt], _ptr(g), SFMT[sfmt],
+                              _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx), int(index_base),
+                              *_hp_args(hp))
+    if rc != 0:
+        raise OracleError(f"oracle_step_nv returned {rc}")
+
+
+def encode_nv(x: np.ndarray):
+    """NVFP4 encoding (nearest-even): packed payload bytes and the scale array
+    (fp32 per-tensor scale in bytes 0-3, then the E4M3 block codes)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    q = np.zeros(x.size // 2, dtype=np.uint8)
+    s = np.zeros(4 + x.size // 16, dtype=np.uint8)
+    if lib().oracle_encode_nv(_ptr(x), _ptr(q), _ptr(s), x.size) != 0:
+        raise OracleError("oracle_encode_nv failed")
+    return q, s
+
+
+def nv_values(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Stored NVFP4 weights as the fp32 values the step reads."""
+    st = np.frombuffer(scales[:4].tobytes(), np.float32)[0]
+    den = (decode_array("e4m3", scales[4:]).astype(np.float32) * st).astype(np.float32)
+    el = decode_array("e2m1", unpack_e2m1(q)).astype(np.float32)
+    return (el.reshape(-1, 16) * den[:, None]).astype(np.float32).ravel()
 
 
 def unpack_e2m1(q: np.ndarray) -> np.ndarray:

@@ -82,7 +82,9 @@
  *     rounding mode.
  *   - 4-bit storage (the NVFP4/FP8 setting of Section 4.2; the paper does not
  *     define the format): the OCP MX block format MXFP4 -- 32-element blocks
- *     of E2M1 values with one E8M0 power-of-two scale; rule at oracle_step_mx.
+ *     of E2M1 values with one E8M0 power-of-two scale; rule at oracle_step_mx
+ *     -- and NVFP4 (16-element blocks, E4M3 block scales, one fp32 scale per
+ *     tensor held fixed by the step); rule at oracle_step_nv.
  *
  * Pin status (tests/test_oracle_*.py; a mutation test checks the pins catch
  * planted mistakes): the real-number update is pinned by closed forms, the
@@ -745,6 +747,110 @@ int oracle_encode_mx(const float *x, uint8_t *q, uint8_t *scales, int64_t n) {
     for (int k = 0; k < MX_BLOCK; ++k)
       mx_put(q, b * MX_BLOCK + k, mx_payload(x[b * MX_BLOCK + k], se, OR_RNE, 0u));
     scales[b] = (uint8_t)mx_scale_code(se);
+  }
+  return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* NVFP4 storage (NVIDIA's two-level 4-bit block format)                     */
+/* ------------------------------------------------------------------------ */
+
+/* NVFP4 (the format the paper's 4-bit runs name, Section 4.2): blocks of 16
+ * contiguous E2M1 values, each block with an E4M3 scale code c_b, and one
+ * fp32 scale s_t per tensor.  The weight is q * D_b with D_b = fp32(E4M3(c_b)
+ * * s_t).  The scale array holds s_t (4 bytes) followed by one c_b per block.
+ *
+ * Encoding: s_t = fp32(amax / 2688) over the finite |x| of the tensor
+ * (2688 = 6 * 448: E2M1's largest value times E4M3's), 1 when there is no
+ * finite nonzero value.  A step keeps s_t (the caller re-encodes to refresh
+ * it) and recomputes every block: c_b = RNE_E4M3(fp32(amax_b / fp32(6 s_t)))
+ * (saturating at 448), the NaN code 0x7F when the block holds a non-finite
+ * value; payloads q = round(fp32(w' / D_b)) onto E2M1 with the step's
+ * rounding, saturating at +-6, and 0 when D_b is 0 or the block is NaN. */
+#define NV_BLOCK 16
+
+static float nv_get_st(const uint8_t *scales) {
+  float st;
+  memcpy(&st, scales, 4);
+  return st;
+}
+
+/* D_b: the block's dequantization factor, fp32(E4M3 value * s_t). */
+static float nv_den(uint32_t code, float st) { return (float)decode(OF_E4M3, code) * st; }
+
+static uint32_t nv_block_code(const float *wn, float st) {
+  float amax = 0.0f;
+  for (int i = 0; i < NV_BLOCK; ++i) {
+    if (!isfinite(wn[i])) return 0x7Fu;
+    if (fabsf(wn[i]) > amax) amax = fabsf(wn[i]);
+  }
+  const float six_st = 6.0f * st;
+  return encode(OF_E4M3, amax / six_st, OR_RNE, 0u);
+}
+
+static uint32_t nv_payload(float wn, uint32_t code, float den, int mode, uint32_t r16) {
+  if (code == 0x7Fu || den == 0.0f) return 0u;
+  return encode(OF_E2M1, wn / den, mode, r16);
+}
+
+/* M+Adam step on NVFP4 storage.  n must be a multiple of 16; q holds n/2
+ * bytes, scales 4 + n/16 bytes (s_t, then the block codes). */
+int oracle_step_nv(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const void *g, int sfmt,
+                   void *m, void *v, void *ve, int64_t n, const int64_t *gidx, int64_t index_base,
+                   double lr_add, double lr_mul, double beta1, double beta2, double eps, double tau,
+                   double r_max, double eps0, double g_max, double d_mult_max, double w_max,
+                   int bias_correction, int rounding, uint64_t seed, int64_t step) {
+  init_formats();
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
+              w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (gfmt != OG_FP32 && gfmt != OG_BF16) return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
+  if (n < 0 || n % NV_BLOCK != 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  const float st = nv_get_st(scales);
+  uint8_t *codes = scales + 4;
+  float wn[NV_BLOCK];
+  for (int64_t b = 0; b < n / NV_BLOCK; ++b) {
+    const float dold = nv_den(codes[b], st);
+    for (int k = 0; k < NV_BLOCK; ++k) {
+      const int64_t i = b * NV_BLOCK + k;
+      const float wv = (float)decode(OF_E2M1, mx_get(q, i)) * dold;
+      wn[k] = step_stored(wv, load_grad(gfmt, g, i), sfmt, m, v, ve, i, &s, &h,
+                          gidx ? gidx[i] : index_base + i);
+    }
+    const uint32_t c = nv_block_code(wn, st);
+    const float dnew = nv_den(c, st);
+    for (int k = 0; k < NV_BLOCK; ++k) {
+      const int64_t i = b * NV_BLOCK + k;
+      const int64_t idx = gidx ? gidx[i] : index_base + i;
+      const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+      const uint32_t pc = nv_payload(wn[k], c, dnew, h.rounding, r16);
+      mx_put(q, i, pc);
+      if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, pc) * dnew);
+    }
+    codes[b] = (uint8_t)c;
+  }
+  return ORACLE_OK;
+}
+
+/* NVFP4 encoding of fp32 values (nearest-even), per-tensor scale included. */
+int oracle_encode_nv(const float *x, uint8_t *q, uint8_t *scales, int64_t n) {
+  init_formats();
+  if (n < 0 || n % NV_BLOCK != 0) return ORACLE_EINVAL;
+  float amax = 0.0f;
+  for (int64_t i = 0; i < n; ++i)
+    if (isfinite(x[i]) && fabsf(x[i]) > amax) amax = fabsf(x[i]);
+  const float st = amax > 0.0f ? amax / 2688.0f : 1.0f;
+  memcpy(scales, &st, 4);
+  for (int64_t b = 0; b < n / NV_BLOCK; ++b) {
+    const uint32_t c = nv_block_code(x + b * NV_BLOCK, st);
+    const float den = nv_den(c, st);
+    for (int k = 0; k < NV_BLOCK; ++k)
+      mx_put(q, b * NV_BLOCK + k, nv_payload(x[b * NV_BLOCK + k], c, den, OR_RNE, 0u));
+    scales[4 + b] = (uint8_t)c;
   }
   return ORACLE_OK;
 }

@@ -15,7 +15,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "madd_oracle.c")
 PINS = ["tests/test_oracle_step.py", "tests/test_oracle_block.py", "tests/test_oracle_sr_rng.py",
-        "tests/test_oracle_formats.py", "tests/test_oracle_mx.py"]
+        "tests/test_oracle_formats.py", "tests/test_oracle_mx.py", "tests/test_oracle_nv.py"]
 
 MUTANTS = {
     "additive sign": ("const float ua = -((s->SA * m) / den_a);",
@@ -77,6 +77,14 @@ MUTANTS = {
                                           "sr ? draw16(h->seed, h->step, 0u, idx) : 0u"),
     "v and v_e share a stream": ("sr ? draw16(h->seed, h->step, 3u, idx) : 0u",
                                  "sr ? draw16(h->seed, h->step, 2u, idx) : 0u"),
+    "NV block scale without the factor 6": ("const float six_st = 6.0f * st;",
+                                            "const float six_st = st;"),
+    "NV divisor ignores the tensor scale": (
+        "static float nv_den(uint32_t code, float st) { return (float)decode(OF_E4M3, code) * st; }",
+        "static float nv_den(uint32_t code, float st) { return (float)decode(OF_E4M3, code); }"),
+    "NV tensor scale from 448 alone": ("amax > 0.0f ? amax / 2688.0f : 1.0f", "amax > 0.0f ? amax / 448.0f : 1.0f"),
+    "NV NaN block payload": ("if (code == 0x7Fu || den == 0.0f) return 0u;",
+                             "if (code == 0x7Fu || den == 0.0f) return 7u;"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }

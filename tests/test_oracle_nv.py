@@ -1,0 +1,154 @@
+"""Pins of the oracle's NVFP4 storage (CPU).
+
+NVFP4 (NVIDIA's two-level 4-bit block format, named by the paper's 4-bit
+master-weight runs, Section 4.2): blocks of 16 E2M1 values with an E4M3
+scale code each, and one fp32 scale s_t per tensor; the weight is
+q * fp32(E4M3(c) * s_t).  Pins, independent of the oracle's code path:
+  * s_t = fp32(amax / (6 * 448)) over the finite values (numpy);
+  * block codes = torch's float8_e4m3fn conversion of fp32(amax_b / fp32(6 s_t));
+  * payloads = brute-force nearest E2M1 (ties to the even code, saturating)
+    of fp32(x / D_b);
+  * a hand-worked tensor (`tests/golden/nvfp4_block.json`);
+  * the step equals the unscaled FP32 step on the dequantized weights
+    followed by the block rule with the tensor's s_t kept, written here
+    from the pins above; stochastic rounding lands on grid neighbours.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_10611_amd.workloads import DEFAULT_HPARAMS
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "nvfp4_block.json")
+E2M1_TABLE = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]  # OCP / NVIDIA FP4 values
+
+
+def hp(**kw):
+    h = dict(DEFAULT_HPARAMS)
+    h["rounding"] = "rne"
+    h.update(kw)
+    return h
+
+
+def nearest_e2m1(y: float) -> int:
+    sign = 8 if np.signbit(y) else 0
+    a = min(abs(y), 6.0)
+    d = [abs(a - t) for t in E2M1_TABLE]
+    cands = [c for c in range(8) if d[c] == min(d)]
+    even = [c for c in cands if c % 2 == 0]
+    return sign | (even[0] if even else cands[0])
+
+
+def e4m3_code(r: np.float32) -> int:
+    r = np.float32(min(float(r), 448.0))
+    return int(torch.tensor([r]).to(torch.float8_e4m3fn).view(torch.uint8).item())
+
+
+def tensor_scale(scales):
+    return np.frombuffer(scales[:4].tobytes(), np.float32)[0]
+
+
+def reference_blocks(x: np.ndarray, st: np.float32):
+    """Block codes and payload codes by the pins (numpy, torch, brute force)."""
+    xb = x.reshape(-1, 16)
+    codes, pay = [], []
+    six_st = np.float32(np.float32(6.0) * st)
+    for blk in xb:
+        if not np.isfinite(blk).all():
+            codes.append(0x7F)
+            pay += [0] * 16
+            continue
+        amax = np.float32(np.abs(blk).max())
+        c = e4m3_code(np.float32(amax / six_st))
+        codes.append(c)
+        cv = torch.tensor([c], dtype=torch.uint8).view(torch.float8_e4m3fn).float().item()
+        den = np.float32(np.float32(cv) * st)
+        pay += [0 if den == 0 else nearest_e2m1(float(np.float32(v / den))) for v in blk]
+    return np.array(codes, np.uint8), np.array(pay, np.uint8)
+
+
+def test_encode_rule():
+    rng = np.random.default_rng(20)
+    nb = 300
+    x = (rng.normal(0, 1, (nb, 16)) * 10.0 ** rng.uniform(-4, 1, nb)[:, None]).astype(np.float32)
+    x[0] = 0.0
+    x[5, 3] = np.nan
+    x[7, 0] = np.inf
+    x = x.ravel()
+    q, s = oracle.encode_nv(x)
+    fin = x[np.isfinite(x)]
+    assert tensor_scale(s) == np.float32(np.float32(np.abs(fin).max()) / np.float32(2688.0))
+    codes, pay = reference_blocks(x, tensor_scale(s))
+    assert (s[4:] == codes).all()
+    assert (oracle.unpack_e2m1(q) == pay).all()
+    assert s[4 + 0] == 0 and s[4 + 5] == 0x7F and s[4 + 7] == 0x7F
+
+
+def test_all_zero_tensor_takes_unit_scale():
+    q, s = oracle.encode_nv(np.zeros(64, np.float32))
+    assert tensor_scale(s) == 1.0 and (s[4:] == 0).all() and (q == 0).all()
+
+
+def test_hand_computed_tensor():
+    with open(GOLDEN) as f:
+        ex = json.load(f)
+    q, s = oracle.encode_nv(np.array(ex["x"], np.float32))
+    assert s.tolist() == ex["scales"]
+    assert q.tolist() == ex["packed"]
+
+
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_step_is_unscaled_step_then_block_rule_with_the_same_tensor_scale(rounding):
+    rng = np.random.default_rng(21)
+    n = 96 * 16
+    q, s = oracle.encode_nv(rng.normal(0, 0.02, n).astype(np.float32))
+    st = tensor_scale(s)
+    z1 = [np.zeros(n, np.float32) for _ in range(3)]
+    z2 = [np.zeros(n, np.float32) for _ in range(3)]
+    for t in range(1, 5):
+        g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-5, -2, n)).astype(np.float32)
+        codes32 = oracle.nv_values(q, s).view(np.uint32).copy()
+        h = hp(step=t, lr_add=1e-2, rounding=rounding, seed=8)
+        oracle.step("fp32", codes32, g, *z2, h)
+        wn = codes32.view(np.float32)
+        oracle.step_nv(q, s, g, *z1, h)
+        assert tensor_scale(s) == st
+        codes, pay = reference_blocks(wn, st)
+        assert (s[4:] == codes).all()
+        got = oracle.unpack_e2m1(q)
+        if rounding == "rne":
+            assert (got == pay).all()
+        else:  # one of the two E2M1 neighbours of w'/D_b
+            cv = torch.from_numpy(codes.copy()).view(torch.float8_e4m3fn).float().numpy()
+            den = np.repeat((cv * st).astype(np.float32), 16)
+            y = (wn / den).astype(np.float64)
+            val = oracle.decode_array("e2m1", got)
+            grid = np.array(sorted({-t for t in E2M1_TABLE} | set(E2M1_TABLE)))
+            i = np.searchsorted(grid, y, side="right")
+            below = grid[np.clip(i - 1, 0, grid.size - 1)]
+            above = grid[np.clip(i, 0, grid.size - 1)]
+            assert ((val == below) | (val == above) | ((np.abs(y) >= 6) & (np.abs(val) == 6))).all()
+        for a, b in zip(z1, z2):
+            assert a.tobytes() == b.tobytes()
+
+
+def test_compute_copy_is_bf16_of_the_stored_value():
+    rng = np.random.default_rng(22)
+    n = 32 * 16
+    q, s = oracle.encode_nv(rng.normal(0, 0.05, n).astype(np.float32))
+    copy = np.zeros(n, np.uint16)
+    z = [np.zeros(n, np.float32) for _ in range(3)]
+    oracle.step_nv(q, s, rng.normal(0, 1e-3, n).astype(np.float32), *z, hp(rounding="sr", seed=2),
+                   copy=copy)
+    want = torch.from_numpy(oracle.nv_values(q, s)).to(torch.bfloat16).view(torch.int16).numpy()
+    assert (copy == want.view(np.uint16)).all()
+
+
+def test_validation():
+    z = [np.zeros(40, np.float32) for _ in range(4)]
+    with pytest.raises(oracle.OracleError):
+        oracle.step_nv(np.zeros(20, np.uint8), np.zeros(6, np.uint8), *z, hp())
