@@ -33,7 +33,9 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
 
-WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5}
+WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5, "nvfp4": 0.5}
+# linear-layer storage of the low-precision master settings
+LOW_MASTER = {"fp8-master": "e4m3", "fp4-master": "mxfp4", "nvfp4-master": "nvfp4"}
 SBYTES = {"fp32": 4, "bf16": 2, "bf16-sr": 2}
 
 
@@ -140,11 +142,12 @@ def main():
     ap.add_argument("--states", default="fp32", choices=["fp32", "bf16", "bf16-sr"],
                     help="storage of m, v, v_e (bf16: the paper's optimizer-state precision, "
                          "rounded to nearest; bf16-sr: rounded stochastically)")
-    ap.add_argument("--weights", default="list", choices=["list", "fp8-master", "fp4-master"],
+    ap.add_argument("--weights", default="list", choices=["list", *LOW_MASTER],
                     help="list: the configuration's weight format for every tensor; fp8-master: "
                          "linear layers block-scaled E4M3 with bf16 compute copies, embeddings, "
                          "norms and head bf16 (the paper's FP8-master setting); fp4-master: the "
-                         "same with MXFP4 linear layers (its 4-bit setting)")
+                         "same with MXFP4 linear layers (its 4-bit setting); nvfp4-master: the "
+                         "same with NVFP4 linear layers")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
     ap.add_argument("--cpu-steps", type=int, default=None,
                     help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
@@ -205,21 +208,24 @@ def main():
             off += n
         return buf, views
 
-    low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}.get(args.weights)
+    low = LOW_MASTER.get(args.weights)
     if low:
         plan = W.low_precision_master_plan(cfg, low)
     else:
         plan = [(wfmt, False, False)] * len(specs)
 
-    def flat_subset(dtype, pick, per_elem=1):
-        """One buffer for the tensors selected by pick, views (None elsewhere)."""
-        tot = sum(n // per_elem for n, p in zip(sizes, plan) if pick(p))
+    def flat_subset(dtype, pick, per_elem=1, head=0):
+        """One buffer for the tensors selected by pick, views (None elsewhere):
+        n // per_elem elements per tensor after `head` leading elements, each
+        view starting at a multiple of 4 elements."""
+        lens = [head + n // per_elem for n in sizes]
+        tot = sum(-(-k // 4) * 4 for k, p in zip(lens, plan) if pick(p))
         buf = torch.empty(max(tot, 1), dtype=dtype, device=dev)
         views, off = [], 0
-        for n, p in zip(sizes, plan):
+        for k, p in zip(lens, plan):
             if pick(p):
-                views.append(buf[off:off + n // per_elem])
-                off += n // per_elem
+                views.append(buf[off:off + k])
+                off += -(-k // 4) * 4
             else:
                 views.append(None)
         return buf, views
@@ -230,10 +236,12 @@ def main():
     else:
         wb16, w16 = flat_subset(torch.int16, lambda p: p[0] == "bf16")
         wb8, w8 = flat_subset(torch.uint8, lambda p: p[0] != "bf16",
-                              per_elem=2 if low == "mxfp4" else 1)
+                              per_elem=2 if low in ("mxfp4", "nvfp4") else 1)
         ws = [a if a is not None else b for a, b in zip(w16, w8)]
         if low == "mxfp4":
             sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=32)
+        elif low == "nvfp4":  # fp32 tensor scale, then one E4M3 code per 16
+            sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=16, head=4)
         else:
             sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
         cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
@@ -313,8 +321,10 @@ def main():
     else:
         for n, (wf, blk, cp) in zip(sizes, plan):
             alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
-            if blk:  # scale read + written: FP16 per 128 (FP8) or E8M0 per 32 (MXFP4)
-                alg_bytes += (n // 32) * 2 if wf == "mxfp4" else (n // 128) * 4
+            if blk:  # scale read + written: FP16 per 128 (FP8), E8M0 per 32 (MXFP4),
+                # E4M3 per 16 plus the fp32 tensor scale read (NVFP4)
+                alg_bytes += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4}.get(
+                    wf, (n // 128) * 4)
     bpp = alg_bytes / n_step
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
 
@@ -346,7 +356,7 @@ def main():
         kname = (f"madd_step_kernel<{wfmt} weights, fp32 grads, {args.states} moments, "
                  f"{W.CONFIGS[cfg]['rounding'].upper()}>")
     else:
-        low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}[args.weights]
+        low = LOW_MASTER[args.weights]
         kname = (f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches per "
                  "step; timed together)")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -364,7 +374,7 @@ def main():
     workload = WORKLOAD_NAMES[cfg]
     if shard:
         workload = f"rank {shard[0]} of {shard[1]} contiguous shards of the {workload}"
-    low = {"fp8-master": "e4m3", "fp4-master": "mxfp4"}.get(args.weights)
+    low = LOW_MASTER.get(args.weights)
     out = {
         "metric": METRIC,
         "value": round(n_step / (ms_per_step / 1e3) / 1e9, 3),

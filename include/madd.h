@@ -75,13 +75,21 @@ typedef enum madd_status {
  *              byte, element 2k in the low nibble of byte k (w holds n/2
  *              bytes).  Blocks of 32 contiguous elements share one E8M0
  *              scale X = 2^(code - 127) (code 255 = NaN); the weight is
- *              E2M1 value * X.  Always block-scaled (scales required). */
+ *              E2M1 value * X.  Always block-scaled (scales required).
+ *   NVFP4    : 4-bit two-level block scaling, NVIDIA's NVFP4 (the format the
+ *              paper's 4-bit runs name): E2M1 payloads packed as for MXFP4;
+ *              blocks of 16 elements, each with an OCP E4M3 scale code c
+ *              (unsigned; 0x7F = NaN); one fp32 scale st per tensor.  The
+ *              weight is E2M1 value * fp32(E4M3(c) * st).  The scale array
+ *              holds st in its first 4 bytes (fp32, 4-byte aligned), then
+ *              the n/16 block codes.  Always block-scaled. */
 typedef enum madd_wfmt {
   MADD_W_BF16 = 0,
   MADD_W_FP8_E4M3 = 1,
   MADD_W_FP8_E5M2 = 2,
   MADD_W_FP32 = 3,
-  MADD_W_MXFP4 = 4
+  MADD_W_MXFP4 = 4,
+  MADD_W_NVFP4 = 5
 } madd_wfmt;
 
 /* Gradient formats (decoded exactly to FP32). */
@@ -160,7 +168,16 @@ int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, voi
  *     - 2 (2 = exponent of E2M1's largest value 6), clamped to [-127, 127]
  *     (the OCP MX conversion rule); s = 0 for an all-zero block; the NaN
  *     scale, with zero payloads, for a block holding a non-finite value.
- *     Payloads are x / 2^s rounded onto E2M1, saturating at +-6. */
+ *     Payloads are x / 2^s rounded onto E2M1, saturating at +-6.
+ *   - NVFP4 (required): 4 + n/16 bytes, 4-byte aligned, n % 16 == 0.  The
+ *     per-tensor scale is st = fp32(amax / 2688) over the finite |x| (2688 =
+ *     6 * 448, E2M1's largest value times E4M3's; st = 1 when no value is
+ *     finite and nonzero); block b's code is RNE_E4M3(fp32(amax_b /
+ *     fp32(6 st))) saturating at 448 (NaN when the block holds a non-finite
+ *     value); payloads are fp32(x / D_b), D_b = fp32(E4M3(code) * st),
+ *     rounded onto E2M1 saturating at +-6, and 0 when D_b is 0 or the block
+ *     is NaN.  Four launches on `stream` (the amax reduction uses the first
+ *     scale word). */
 int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales, int64_t n,
                             void* stream);
 
@@ -174,13 +191,16 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
  *           (Appendix figure) rebuilds from the stored weights after every
  *           update; here the same pass writes it.  16-byte aligned for the
  *           fast path.
- * scales  : NULL, or the block scales of block-scaled FP8 or MXFP4 as in
- *           madd_encode_weights (required for MXFP4): the weight is
- *           payload * scale (fp32 product); after the update each block's
- *           scale is recomputed from the new weights by the same rule and the
- *           payloads re-encoded with hp->rounding.  Requires n % 128 == 0
- *           (FP8) or n % 32 == 0 (MXFP4) and 16-byte-aligned w, g, m, v, ve
- *           and copy (else MADD_EINVAL / MADD_EALIGN).
+ * scales  : NULL, or the block scales of block-scaled FP8, MXFP4 or NVFP4
+ *           as in madd_encode_weights (required for the 4-bit formats): the
+ *           weight is payload * scale (fp32 product); after the update each
+ *           block's scale is recomputed from the new weights by the same rule
+ *           and the payloads re-encoded with hp->rounding.  NVFP4's
+ *           per-tensor scale st is read and kept (re-encode to refresh it).
+ *           Requires n % 128 == 0 (FP8), n % 32 == 0 (MXFP4) or n % 16 == 0
+ *           (NVFP4) and 16-byte-aligned w, g, m, v, ve and copy, and a
+ *           4-byte-aligned NVFP4 scale array (else MADD_EINVAL /
+ *           MADD_EALIGN).
  * g       : device gradient of format gfmt (read only).
  * m, v, ve: device moments (first, second, multiplicative second) stored as
  *           sfmt (a madd_sfmt), updated in place.
@@ -199,10 +219,10 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
  * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
  * block-scaled) or a host array whose entry i is NULL or tensor i's scale
- * array (never NULL for an MXFP4 tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
+ * array (never NULL for an MXFP4 or NVFP4 tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
  * or tensor i's bf16 compute-copy array (as in madd_step).  Tensors of
  * different weight formats may be mixed -- e.g. block-scaled FP8 linear
- * layers (or MXFP4 ones) with BF16 embeddings, norms and head, the paper's
+ * layers (or MXFP4 / NVFP4 ones) with BF16 embeddings, norms and head, the paper's
  * FP8-master (4-bit-master) setting (Section 4.2).  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
  * The first call with a given list (same pointers and sizes) uploads a device
@@ -226,7 +246,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
  * No optimizer state.  w: device weight codes of format wfmt, in place;
  * g: device gradient of format gfmt; index_base, rounding and seed as in
  * madd_step; hp's beta1, beta2, eps, g_max and bias_correction are validated
- * but unused.  Unscaled formats only (MXFP4 is MADD_EINVAL).  Errors as in
+ * but unused.  Unscaled formats only (MXFP4, NVFP4: MADD_EINVAL).  Errors as in
  * madd_step. */
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
                         int64_t index_base, const madd_hparams* hp, void* stream);

@@ -92,9 +92,11 @@
  * OCP value tables and brute force; Philox by published known-answer vectors.
  * Parity unpinned against the paper, because the paper does not fix them:
  * the exact fp32 operation order (a contract shared with the kernel), the
- * block-scaled FP8 block length and scale rule, the 4-bit format (MXFP4,
- * pinned to the OCP specification instead), and the stochastic-rounding rule
- * and its generator (pinned to their own definitions).
+ * block-scaled FP8 block length and scale rule, the 4-bit formats (MXFP4
+ * and NVFP4, pinned to their published definitions instead; when NVFP4's
+ * tensor scale is refreshed is a choice: at encoding), and the
+ * stochastic-rounding rule and its generator (pinned to their own
+ * definitions).
  *
  * Codec implementation: values are decoded from the (sign, exponent,
  * mantissa) definition of each format; encoding searches the sorted table of

@@ -17,12 +17,13 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmadd.so")
 
 # enum values of madd.h
-W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32, W_MXFP4 = 0, 1, 2, 3, 4
+W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32, W_MXFP4, W_NVFP4 = 0, 1, 2, 3, 4, 5
 G_FP32, G_BF16 = 0, 1
 ROUND_RNE, ROUND_SR = 0, 1
 WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32,
-        "mxfp4": W_MXFP4}
+        "mxfp4": W_MXFP4, "nvfp4": W_NVFP4}
 MX_BLOCK = 32  # elements per MXFP4 block (one E8M0 scale byte)
+NV_BLOCK = 16  # elements per NVFP4 block (one E4M3 scale byte after the fp32 tensor scale)
 GFMT = {"fp32": G_FP32, "bf16": G_BF16}
 S_FP32, S_BF16, S_BF16_SR = 0, 1, 2
 SFMT = {"fp32": S_FP32, "bf16": S_BF16, "bf16_sr": S_BF16_SR}
@@ -179,8 +180,9 @@ def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, in
               n: int | None = None, sfmt: str | None = None, copy=None, stream=None):
     """One step on one tensor.  ``w`` holds the weight codes (uint16 / uint8 /
     int32 storage for bf16 / fp8 / fp32; n/2 packed bytes for mxfp4, whose
-    ``scales`` are n/32 uint8 E8M0 codes); the moments' storage follows their
-    dtype unless ``sfmt`` is given; ``copy`` (16-bit tensor) receives the
+    ``scales`` are n/32 uint8 E8M0 codes, and for nvfp4, whose ``scales`` are
+    4 + n/16 bytes, 4-byte aligned: the fp32 tensor scale, then E4M3 codes);
+    the moments' storage follows their dtype unless ``sfmt`` is given; ``copy`` (16-bit tensor) receives the
     bf16 compute copy of the new weights."""
     h = _hp(hp)
     n = m.numel() if n is None else n

@@ -48,7 +48,7 @@
 
 // The library is built from this one source compiled as several parts
 // (-DMADD_PART=k, in parallel): part 0 holds the host code, the ABI and the
-// set-up kernels; parts 1-7 each instantiate the step kernels of one weight
+// set-up kernels; parts 1-8 each instantiate the step kernels of one weight
 // format (block-scaled FP8 separately from unscaled).  Without MADD_PART
 // everything is compiled as one unit.
 #ifndef MADD_PART
@@ -66,6 +66,7 @@ constexpr int kTilesPerChunk = 1;
 constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
 constexpr int kBlock = 128;                  // block-scaled FP8 block length
 constexpr int kMxBlock = 32;                 // MXFP4 block length (OCP MX)
+constexpr int kNvBlock = 16;                 // NVFP4 block length
 
 // ---------------------------------------------------------------------------
 // Scalars and descriptors
@@ -148,7 +149,7 @@ __device__ __forceinline__ uint32_t draw_one(uint64_t idx, const Scalars& s, uin
 // Storage-format codecs (bit level)
 // ---------------------------------------------------------------------------
 
-enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3, WF_MXFP4 = 4 };
+enum : int { WF_BF16 = 0, WF_E4M3 = 1, WF_E5M2 = 2, WF_FP32 = 3, WF_MXFP4 = 4, WF_NVFP4 = 5 };
 enum : int { GF_FP32 = 0, GF_BF16 = 1 };
 // storage of the moments: fp32, bf16 rounded to nearest-even, bf16 rounded
 // stochastically (streams 1, 2, 3)
@@ -352,7 +353,7 @@ template <int WF>
 __device__ __forceinline__ float decode(uint32_t c) {
   if constexpr (WF == WF_BF16) return dec_bf16(c);
   else if constexpr (WF == WF_FP32) return __uint_as_float(c);
-  else if constexpr (WF == WF_MXFP4) return dec_e2m1(c);  // payload value, before the scale
+  else if constexpr (WF == WF_MXFP4 || WF == WF_NVFP4) return dec_e2m1(c);  // before the scale
   else return dec_fp8<WF>(c);
 }
 
@@ -455,6 +456,8 @@ struct WQuad<WF_MXFP4> {  // 4 x 4 bits: two bytes, element 2k in the low nibble
     stg<uint16_t>((uint8_t*)p + (e >> 1), (uint16_t)raw);
   }
 };
+template <>
+struct WQuad<WF_NVFP4> : WQuad<WF_MXFP4> {};  // the same packed E2M1 payloads
 template <>
 struct WQuad<WF_FP32> {  // 4 x 32 bits
   u4 raw;
@@ -783,14 +786,17 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
 
 // Block-scaled storage: the kBlk / 4 consecutive lanes that hold one block of
 // a sub-tile (32 lanes for a 128-element FP8 block, 8 for a 32-element MXFP4
-// block) combine the block's max |w'| with lane shuffles.  The launch
+// block, 4 for a 16-element NVFP4 block) combine the block's max |w'| with
+// lane shuffles.  The launch
 // requires n to be a multiple of the block length, so a block is never split
 // and whole lane groups are active or inactive together; every lane runs the
 // shuffles and the draw exchange.
 template <int WF>
-constexpr int block_len() { return WF == WF_MXFP4 ? kMxBlock : kBlock; }
+constexpr int block_len() {
+  return WF == WF_MXFP4 ? kMxBlock : (WF == WF_NVFP4 ? kNvBlock : kBlock);
+}
 
-// Max over aligned groups of LANES lanes (8, or 32): lane swaps within quads
+// Max over aligned groups of LANES lanes (4, 8 or 32): lane swaps within quads
 // (DPP quad_perm [1,0,3,2] and [2,3,0,1]), the mirrored quad of each half row
 // (row_half_mirror), the mirrored half of each row (row_mirror) and the
 // other row of each 32-lane half (ds_swizzle, xor 16).
@@ -800,11 +806,12 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
 }
 template <int LANES>
 __device__ __forceinline__ uint32_t block_amax(uint32_t a) {
-  static_assert(LANES == 8 || LANES == 32, "block lane groups are 8 or 32 lanes");
+  static_assert(LANES == 4 || LANES == 8 || LANES == 32, "block lane groups are 4, 8 or 32 lanes");
   uint32_t o = dpp_u32<0xB1>(a);
   a = o > a ? o : a;
   o = dpp_u32<0x4E>(a);
   a = o > a ? o : a;
+  if constexpr (LANES == 4) return a;
   o = dpp_u32<0x141>(a);
   a = o > a ? o : a;
   if constexpr (LANES == 32) {
@@ -816,20 +823,34 @@ __device__ __forceinline__ uint32_t block_amax(uint32_t a) {
   return a;
 }
 
+// The block's dequantization factor from its scale code; `st` is NVFP4's
+// per-tensor scale (unused by the other formats).  NVFP4's scale array holds
+// st in its first 4 bytes, then one E4M3 code per block.
 template <int WF>
-__device__ __forceinline__ float scale_value(uint32_t code) {
+__device__ __forceinline__ float scale_value(uint32_t code, float st) {
   if constexpr (WF == WF_MXFP4) return dec_e8m0(code);
+  else if constexpr (WF == WF_NVFP4) return dec_fp8<WF_E4M3>(code) * st;
   else return dec_fp16(code);
 }
 template <int WF>
 __device__ __forceinline__ uint32_t load_scale(const void* scales, int64_t b) {
   if constexpr (WF == WF_MXFP4) return ((const uint8_t*)scales)[b];
+  else if constexpr (WF == WF_NVFP4) return ((const uint8_t*)scales)[4 + b];
   else return ((const uint16_t*)scales)[b];
 }
 template <int WF>
 __device__ __forceinline__ void store_scale(void* scales, int64_t b, uint32_t code) {
   if constexpr (WF == WF_MXFP4) ((uint8_t*)scales)[b] = (uint8_t)code;
+  else if constexpr (WF == WF_NVFP4) ((uint8_t*)scales)[4 + b] = (uint8_t)code;
   else ((uint16_t*)scales)[b] = (uint16_t)code;
+}
+
+// NVFP4 block code: RNE_E4M3(amax / fp32(6 st)), saturating at 448; the E4M3
+// NaN code for a block holding a non-finite value.
+__device__ __forceinline__ uint32_t nv_block_code(uint32_t amax_bits, float st) {
+  if (amax_bits >= 0x7F800000u) return 0x7Fu;
+  const float six_st = 6.0f * st;
+  return enc_fp8<WF_E4M3>(__uint_as_float(amax_bits) / six_st, false, 0u);
 }
 
 template <int WF, bool SR, bool CLAMP>
@@ -853,8 +874,20 @@ __device__ __forceinline__ uint32_t step_quad_unrounded(Quad<WF>& q, float sold,
 // values (payload value x scale) for the compute copy.
 template <int WF, bool SR>
 __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[4], uint32_t amax,
-                                                 const uint32_t (&r)[4], float (&cv)[4]) {
-  if constexpr (WF == WF_MXFP4) {
+                                                 const uint32_t (&r)[4], float (&cv)[4], float st) {
+  if constexpr (WF == WF_NVFP4) {
+    const uint32_t sc = nv_block_code(amax, st);
+    const float den = dec_fp8<WF_E4M3>(sc) * st;
+    const bool zero = sc == 0x7Fu || den == 0.0f;  // NaN block, or a factor of 0
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float v;
+      const uint32_t c = enc_e2m1(wn[k] / den, SR, r[k], v);
+      q.w.set(k, zero ? 0u : c);
+      cv[k] = (zero ? 0.0f : v) * den;
+    }
+    return sc;
+  } else if constexpr (WF == WF_MXFP4) {
     const uint32_t sc = mx_scale(amax);
     const float inv = mx_inv_scale(sc), X = dec_e8m0(sc);
 #pragma unroll
@@ -885,6 +918,7 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
   constexpr int kLanes = kBlk / kQuad;
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
+  const float st = WF == WF_NVFP4 ? *(const float*)d.scales : 1.0f;  // NVFP4 tensor scale
   const int64_t c0 = (chunk - d.chunk0) * kChunk;
   const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
 #pragma unroll 1
@@ -912,21 +946,21 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
     }
     if (actA)
       amaxA = step_quad_unrounded<WF, SR, CLAMP>(
-          qa, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk))), wa, s);
+          qa, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk)), st), wa, s);
     if (actB)
       amaxB = step_quad_unrounded<WF, SR, CLAMP>(
-          qb, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk))), wb, s);
+          qb, scale_value<WF>(load_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk)), st), wb, s);
     amaxA = block_amax<kLanes>(amaxA);
     amaxB = block_amax<kLanes>(amaxB);
     float cv[4];
     if (actA) {
-      const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA, cv);
+      const uint32_t sc = requant_quad<WF, SR>(qa, wa, amaxA, rA, cv, st);
       store_quad<WF, SF>(qa, d, eA, mA);
       if (COPY && d.copy) store_copy_values(cv, d.copy, eA);
       if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eA / kBlk), sc);
     }
     if (actB) {
-      const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB, cv);
+      const uint32_t sc = requant_quad<WF, SR>(qb, wb, amaxB, rB, cv, st);
       store_quad<WF, SF>(qb, d, eB, mB);
       if (COPY && d.copy) store_copy_values(cv, d.copy, eB);
       if ((threadIdx.x & (kLanes - 1)) == 0u) store_scale<WF>(d.scales, (int64_t)((uint64_t)eB / kBlk), sc);
@@ -1040,6 +1074,61 @@ __global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __rest
     scales[b] = (uint8_t)sc;
   }
 }
+
+// NVFP4 encoding, three stages on the stream: the largest finite |x| of the
+// tensor into the scale array's first word (as fp32 bits; non-negative floats
+// order like their bits), that word turned into the per-tensor scale
+// st = amax / 2688 (1 when amax is 0), then one thread per 16-element block.
+__global__ __launch_bounds__(kThreads) void nv_amax_kernel(const float* __restrict__ x, int64_t n,
+                                                           uint32_t* slot) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  uint32_t m = 0u;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) {
+    const uint32_t b = __float_as_uint(x[i]) & 0x7FFFFFFFu;
+    m = (b < 0x7F800000u && b > m) ? b : m;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)m, off);
+    m = o > m ? o : m;
+  }
+  if ((threadIdx.x & 63u) == 0u && m != 0u) atomicMax(slot, m);
+}
+
+__global__ void nv_scale_kernel(uint32_t* slot) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const float amax = __uint_as_float(*slot);
+    *slot = __float_as_uint(amax > 0.0f ? amax / 2688.0f : 1.0f);
+  }
+}
+
+__global__ void nv_clear_kernel(uint32_t* slot) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *slot = 0u;
+}
+
+__global__ __launch_bounds__(kThreads) void encode_nv_kernel(const float* __restrict__ x,
+                                                             uint8_t* q, uint8_t* scales,
+                                                             int64_t nblocks) {
+  const float st = *(const float*)scales;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < nblocks; b += stride) {
+    const float* xb = x + b * kNvBlock;
+    uint32_t amax = 0u;
+    for (int k = 0; k < kNvBlock; ++k) {
+      const uint32_t ab = __float_as_uint(xb[k]) & 0x7FFFFFFFu;
+      amax = ab > amax ? ab : amax;
+    }
+    const uint32_t sc = nv_block_code(amax, st);
+    const float den = dec_fp8<WF_E4M3>(sc) * st;
+    const bool zero = sc == 0x7Fu || den == 0.0f;
+    for (int k = 0; k < kNvBlock; k += 2) {
+      const uint32_t lo = zero ? 0u : enc_e2m1(xb[k] / den, false, 0u);
+      const uint32_t hi = zero ? 0u : enc_e2m1(xb[k + 1] / den, false, 0u);
+      q[b * (kNvBlock / 2) + k / 2] = (uint8_t)(lo | (hi << 4));
+    }
+    scales[4 + b] = (uint8_t)sc;
+  }
+}
 #endif  // MADD_IN_PART(0)
 
 // ---------------------------------------------------------------------------
@@ -1093,6 +1182,7 @@ step_fn pick_part4(int gf, int sf, bool sr, bool clamp, bool copy);  // e5m2
 step_fn pick_part5(int gf, int sf, bool sr, bool clamp, bool copy);  // e5m2, block-scaled
 step_fn pick_part6(int gf, int sf, bool sr, bool clamp, bool copy);  // fp32 passthrough
 step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy);  // mxfp4 (block-scaled)
+step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy);  // nvfp4 (block-scaled)
 
 #if MADD_IN_PART(1)
 step_fn pick_part1(int gf, int sf, bool sr, bool clamp, bool copy) {
@@ -1129,12 +1219,17 @@ step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy) {
   return pick_gf<WF_MXFP4, true>(gf, sf, sr, clamp, copy);
 }
 #endif
+#if MADD_IN_PART(8)
+step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy) {
+  return pick_gf<WF_NVFP4, true>(gf, sf, sr, clamp, copy);
+}
+#endif
 
 #if MADD_IN_PART(0)
 // The step kernel for (weight, gradient and moment formats, rounding,
 // optional clamps present, compute copies present, block-scaled); nullptr for
-// combinations that do not exist (block scaling is for FP8 and MXFP4 only,
-// and MXFP4 is always block-scaled).
+// combinations that do not exist (block scaling is for FP8, MXFP4 and NVFP4
+// only, and the 4-bit formats are always block-scaled).
 step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool copy, bool blk) {
   switch (wf) {
     case WF_BF16: return blk ? nullptr : pick_part1(gf, sf, sr, clamp, copy);
@@ -1142,6 +1237,7 @@ step_fn pick_kernel(int wf, int gf, int sf, bool sr, bool clamp, bool copy, bool
     case WF_E5M2: return blk ? pick_part5(gf, sf, sr, clamp, copy) : pick_part4(gf, sf, sr, clamp, copy);
     case WF_FP32: return blk ? nullptr : pick_part6(gf, sf, sr, clamp, copy);
     case WF_MXFP4: return blk ? pick_part7(gf, sf, sr, clamp, copy) : nullptr;
+    case WF_NVFP4: return blk ? pick_part8(gf, sf, sr, clamp, copy) : nullptr;
     default: return nullptr;
   }
 }
@@ -1150,7 +1246,8 @@ bool needs_clamp(const madd_hparams& hp) {
   return !(std::isinf(hp.g_max) && hp.g_max > 0) || !(std::isinf(hp.w_max) && hp.w_max > 0);
 }
 
-bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_MXFP4; }
+bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_NVFP4; }
+bool fp4_fmt(int32_t f) { return f == MADD_W_MXFP4 || f == MADD_W_NVFP4; }
 bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
 bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16 || f == MADD_S_BF16_SR; }
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -1282,9 +1379,11 @@ TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void*
 }
 
 bool block_scaled_fmt(int32_t f) {
-  return f == MADD_W_FP8_E4M3 || f == MADD_W_FP8_E5M2 || f == MADD_W_MXFP4;
+  return f == MADD_W_FP8_E4M3 || f == MADD_W_FP8_E5M2 || fp4_fmt(f);
 }
-int64_t block_len_of(int32_t f) { return f == MADD_W_MXFP4 ? kMxBlock : kBlock; }
+int64_t block_len_of(int32_t f) {
+  return f == MADD_W_MXFP4 ? kMxBlock : (f == MADD_W_NVFP4 ? kNvBlock : kBlock);
+}
 
 int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
                      void* m, void* v, void* ve, int64_t n) {
@@ -1292,10 +1391,11 @@ int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const 
   if (n == 0) return MADD_OK;
   if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
   if (!valid_wfmt(wfmt)) return MADD_EINVAL;
-  if (wfmt == MADD_W_MXFP4 && !scales) return MADD_EINVAL;
+  if (fp4_fmt(wfmt) && !scales) return MADD_EINVAL;
   if (scales) {
     if (!block_scaled_fmt(wfmt)) return MADD_EINVAL;
     if (n % block_len_of(wfmt) != 0) return MADD_EINVAL;
+    if (wfmt == MADD_W_NVFP4 && ((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
     if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy))))
       return MADD_EALIGN;
   }
@@ -1349,8 +1449,23 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
   if (n < 0 || !valid_wfmt(wfmt)) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!x || !w) return MADD_EINVAL;
-  if (wfmt == MADD_W_MXFP4 && !scales) return MADD_EINVAL;
+  if (fp4_fmt(wfmt) && !scales) return MADD_EINVAL;
   hipStream_t st = (hipStream_t)stream;
+  if (wfmt == MADD_W_NVFP4) {
+    if (n % kNvBlock != 0) return MADD_EINVAL;
+    if (((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
+    uint32_t* slot = (uint32_t*)scales;
+    const int64_t nb = n / kNvBlock;
+    const int64_t want_x = (n + kThreads - 1) / kThreads, want_b = (nb + kThreads - 1) / kThreads;
+    const unsigned grid_x = (unsigned)(want_x < 4096 ? want_x : 4096);
+    const unsigned grid_b = (unsigned)(want_b < 65536 ? want_b : 65536);
+    hipLaunchKernelGGL(nv_clear_kernel, dim3(1), dim3(64), 0, st, slot);
+    hipLaunchKernelGGL(nv_amax_kernel, dim3(grid_x), dim3(kThreads), 0, st, x, n, slot);
+    hipLaunchKernelGGL(nv_scale_kernel, dim3(1), dim3(64), 0, st, slot);
+    hipLaunchKernelGGL(encode_nv_kernel, dim3(grid_b), dim3(kThreads), 0, st, x, (uint8_t*)w,
+                       (uint8_t*)scales, nb);
+    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  }
   if (wfmt == MADD_W_MXFP4) {
     if (n % kMxBlock != 0) return MADD_EINVAL;
     const int64_t nb = n / kMxBlock;
@@ -1409,7 +1524,7 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
   if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0 || n < 0) return MADD_EINVAL;
-  if (wfmt == MADD_W_MXFP4) return MADD_EINVAL;  // block-scaled: no scale argument here
+  if (fp4_fmt(wfmt)) return MADD_EINVAL;  // block-scaled: no scale argument here
   if (n == 0) return MADD_OK;
   if (!w || !g) return MADD_EINVAL;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
@@ -1461,7 +1576,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
     int64_t nchunks;
   };
   std::vector<Group> groups;
-  for (int wf = MADD_W_BF16; wf <= MADD_W_MXFP4; ++wf) {
+  for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4; ++wf) {
     for (int blk = 0; blk <= 1; ++blk) {
       std::vector<TensorDesc> descs;
       int64_t gbase = index_base, nch = 0;

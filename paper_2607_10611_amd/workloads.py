@@ -211,10 +211,10 @@ def grad_fp32_device_(cfg: str, i: int, step: int, out, sigma: float | None = No
 def low_precision_master_plan(cfg: str, linear_fmt: str = "e4m3"):
     """Per-tensor storage for the low-precision master settings of Section 4.2:
     attention and MLP linear weights block-scaled in ``linear_fmt`` -- "e4m3"
-    (FP16 scale per 128 elements; the FP8/FP8 setting) or "mxfp4" (E2M1 with
-    an E8M0 scale per 32 elements; standing in for the 4-bit NVFP4/FP8
-    setting) -- each with a bf16 compute copy; embeddings, norms and the LM
-    head in bf16.  Returns (weight format, block-scaled, compute copy) per
+    (FP16 scale per 128 elements; the FP8/FP8 setting), "nvfp4" (E2M1 with an
+    E4M3 scale per 16 elements and an fp32 scale per tensor; the 4-bit
+    setting) or "mxfp4" (E2M1 with an E8M0 scale per 32 elements) -- each
+    with a bf16 compute copy; embeddings, norms and the LM head in bf16.  Returns (weight format, block-scaled, compute copy) per
     tensor."""
     plan = []
     for s in specs(cfg):

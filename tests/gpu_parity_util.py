@@ -1,5 +1,7 @@
 """Helpers shared by the GPU parity tests: moving codes and states between
 numpy (oracle side) and torch device tensors (HIP side), and comparisons."""
+import gc
+
 import numpy as np
 import torch
 
@@ -7,9 +9,9 @@ import oracle
 from paper_2607_10611_amd import binding as B
 
 CODE_NP = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,
-           "mxfp4": np.uint8}  # mxfp4: packed bytes, two elements each
+           "mxfp4": np.uint8, "nvfp4": np.uint8}  # 4-bit: packed bytes, two elements each
 CODE_T = {"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8, "fp32": torch.int32,
-          "mxfp4": torch.uint8}
+          "mxfp4": torch.uint8, "nvfp4": torch.uint8}
 SIGNED_NP = {np.uint16: np.int16, np.uint32: np.int32, np.uint8: np.uint8}
 
 
@@ -95,6 +97,9 @@ def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None
     if wfmt == "mxfp4":
         oracle.step_mx(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
                        index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
+    elif wfmt == "nvfp4":
+        oracle.step_nv(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
+                       index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
     elif hs.scales is not None:
         oracle.step_block(wfmt, hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
                           index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
@@ -114,3 +119,12 @@ def assert_copy_equal(tag, ds: DevState, hs: HostState):
     got = to_host(ds.copy, np.uint16)
     bad = np.nonzero(got != hs.copy)[0]
     assert bad.size == 0, f"{tag}: {bad.size} compute-copy codes differ, first at {bad[:5]}"
+
+
+def free_device_bytes() -> int:
+    """Device memory free for a large test: blocks that earlier tests left in
+    torch's caching allocator are returned to the driver first."""
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return torch.cuda.mem_get_info()[0]

@@ -123,7 +123,23 @@ def test_mxfp4_argument_rules():
     assert lib.madd_plain_step(FAKE, B.W_MXFP4, FAKE, 0, 64, 0, ref, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, None, 64, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, FAKE, 40, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, 5, FAKE, 64, None) == -1   # no such format
+    assert lib.madd_encode_weights(FAKE, FAKE, 6, FAKE, 64, None) == -1   # no such format
+
+
+def test_nvfp4_argument_rules():
+    lib = B.lib()
+    ref, _h = _hp()
+    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_NVFP4, sc, cp, FAKE, 0, FAKE, FAKE,  # noqa: E731
+                                                   FAKE, 0, n, 0, ref, None)
+    assert call(FAKE, None, 64) == -1            # NVFP4 needs its scales
+    assert call(FAKE, FAKE, 40) == -1            # n % 16
+    assert call(FAKE, FAKE + 2, 64) == -2        # tensor scale not 4-byte aligned
+    assert call(FAKE + 2, FAKE, 64) == -2        # unaligned payload bytes
+    assert call(FAKE, FAKE, 64, FAKE + 4) == -2  # unaligned compute copy
+    assert lib.madd_plain_step(FAKE, B.W_NVFP4, FAKE, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, None, 64, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE, 40, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE + 2, 64, None) == -2
 
 
 def test_multi_tensor_rejects_bad_arguments():

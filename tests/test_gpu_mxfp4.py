@@ -11,7 +11,7 @@ import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
 from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
-                             gpu_step, oracle_step, to_dev, to_host)
+                             free_device_bytes, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -189,7 +189,7 @@ def test_fp4_master_llama7b_sampled():
     cfg = "c5"
     specs = W.specs(cfg)
     plan = W.low_precision_master_plan(cfg, "mxfp4")
-    free, _ = torch.cuda.mem_get_info()
+    free = free_device_bytes()
     need = sum(s.numel for s in specs) * 19 + (1 << 30)
     assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
     rng = np.random.default_rng(17)

@@ -1,0 +1,263 @@
+"""Parity of the HIP step on NVFP4 storage (E2M1 payloads, one E4M3 scale per
+16 elements, one fp32 scale per tensor) with the CPU oracle, through the C
+ABI.  Bar: packed payload bytes, scale bytes (tensor scale included) and
+bf16 compute copies bit-exact; fp32 moments within 2 ulp; bf16 moment codes
+bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_10611_amd import binding as B
+from paper_2607_10611_amd import workloads as W
+from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
+                             free_device_bytes, gpu_step, oracle_step, to_dev, to_host)
+from test_oracle_nv import reference_blocks
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def hp(**kw):
+    h = dict(W.DEFAULT_HPARAMS)
+    h.update(kw)
+    return h
+
+
+def nv_weights(rng, n):
+    x = rng.normal(0, 0.02, n).astype(np.float32)
+    x[rng.random(n) < 0.02] = 0.0
+    big = rng.random(n) < 0.01
+    x[big] = rng.normal(0, 3.0, big.sum())
+    if n >= 4 * 16:
+        x[:16] = 0.0                                   # zero block: code 0
+        x[16:32] = rng.normal(0, 1e-7, 16)             # block scale in E4M3's subnormals
+    return x
+
+
+def nv_grad(rng, n):
+    g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-6, -1, n)).astype(np.float32)
+    g[rng.random(n) < 0.05] = 0.0
+    return g
+
+
+def encode_nv_both(x):
+    q_ref, s_ref = oracle.encode_nv(x)
+    q = torch.empty(x.size // 2, dtype=torch.uint8, device="cuda")
+    s = torch.empty(4 + x.size // 16, dtype=torch.uint8, device="cuda")
+    B.madd_encode_weights(torch.from_numpy(x).cuda(), q, "nvfp4", scales=s)
+    torch.cuda.synchronize()
+    assert (to_host(s)[:4] == s_ref[:4]).all(), "tensor scale differs"
+    bad = np.nonzero(to_host(s)[4:] != s_ref[4:])[0]
+    assert bad.size == 0, f"block codes differ at {bad[:5]}"
+    bad = np.nonzero(to_host(q) != q_ref)[0]
+    assert bad.size == 0, f"payload bytes differ at {bad[:5]}"
+    return q_ref, s_ref
+
+
+def check(tag, ds, hs):
+    w_g, m_g, v_g, ve_g = ds.host()
+    assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+    bad = np.nonzero(to_host(ds.scales) != hs.scales)[0]
+    assert bad.size == 0, f"{tag}: scale bytes differ at {bad[:5]}"
+    assert_copy_equal(tag, ds, hs)
+
+
+def run_nv(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
+           grad=nv_grad):
+    rng = np.random.default_rng(seed)
+    q, s = encode_nv_both(nv_weights(rng, n))
+    ds = DevState("nvfp4", q, n, s, sfmt=sfmt, copy=copy)
+    hs = HostState(q, n, s, sfmt=sfmt, copy=copy)
+    for t in range(1, steps + 1):
+        g = grad(rng, n)
+        if gfmt == "bf16":
+            g = oracle.encode_array("bf16", g)
+        h = hp(step=t, **hpkw)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
+        oracle_step("nvfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
+        torch.cuda.synchronize()
+        check(f"nvfp4 n={n} t={t}", ds, hs)
+    return ds, hs
+
+
+def test_encode_matches_oracle():
+    rng = np.random.default_rng(31)
+    x = nv_weights(rng, 16 * 5000)
+    x[300] = np.nan
+    x[400] = -np.inf
+    encode_nv_both(x)
+    encode_nv_both(np.zeros(64, np.float32))        # no finite nonzero value: st = 1
+
+
+@pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
+                                                 ("sr", "bf16", True), ("sr", "bf16_sr", True)])
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+    run_nv(5 * 8192 + 7 * 16, 4, 32, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
+
+
+@pytest.mark.parametrize("n", [16, 48, 1008, 2048 + 16, 4096 + 1024 + 80])
+def test_small_and_partial_tiles(n):
+    run_nv(n, 3, 33 + n, dict(rounding="sr", seed=78, lr_add=1e-2), copy=True)
+
+
+def test_bf16_gradients_unaligned_index_base():
+    run_nv(3 * 8192 + 16, 3, 34, dict(rounding="sr", seed=6), gfmt="bf16", index_base=5,
+           copy=True)
+
+
+def test_algorithm2_clamps():
+    run_nv(2 * 8192, 3, 35, dict(rounding="sr", g_max=2.0, w_max=0.5, d_mult_max=0.25,
+                                 eps0=0.1, bias_correction=0, lr_mul=0.05))
+
+
+def test_nonfinite_gradients_poison_their_blocks():
+    def grad(rng, n):
+        g = nv_grad(rng, n)
+        g[[40, 1000, 5000]] = [np.nan, np.inf, -np.inf]
+        return g
+    ds, hs = run_nv(4 * 2048, 2, 36, dict(rounding="sr"), grad=grad, copy=True)
+    sc = to_host(ds.scales)
+    assert (sc[4 + np.array([40 // 16, 1000 // 16, 5000 // 16])] == 0x7F).all()
+
+
+def test_multi_tensor_list_with_both_4bit_formats():
+    rng = np.random.default_rng(37)
+    layout = [("nvfp4", 4096 + 48), ("bf16", 1000), ("mxfp4", 2048), ("nvfp4", 16),
+              ("e4m3", 1024), ("nvfp4", 0), ("nvfp4", 20480)]
+    devs, singles, hosts = [], [], []
+    for wfmt, n in layout:
+        if wfmt == "nvfp4":
+            q, s = encode_nv_both(nv_weights(rng, n)) if n else (np.zeros(0, np.uint8),
+                                                                  np.zeros(4, np.uint8))
+            args = (q, n, s)
+        elif wfmt == "mxfp4":
+            q, s = oracle.encode_mx(nv_weights(rng, n))
+            args = (q, n, s)
+        elif wfmt == "e4m3":
+            q, s = oracle.encode_block("e4m3", nv_weights(rng, n))
+            args = (q, n, s)
+        else:
+            args = (oracle.encode_array("bf16", nv_weights(rng, n)), n, None)
+        cp = wfmt != "bf16"
+        devs.append(DevState(wfmt, *args, copy=cp))
+        singles.append(DevState(wfmt, *args, copy=cp))
+        hosts.append(HostState(*args, copy=cp))
+    base = 4000
+    for t in range(1, 4):
+        gs = [nv_grad(rng, n) for _, n in layout]
+        gds = [to_dev(g) for g in gs]
+        h = hp(step=t, rounding="sr", seed=31415)
+        tl = B.TensorList([d.w for d in devs], [d.wfmt for d in devs], gds, [d.m for d in devs],
+                          [d.v for d in devs], [d.ve for d in devs],
+                          scales=[d.scales for d in devs], copies=[d.copy for d in devs])
+        B.madd_multi_tensor_step(tl, h, index_base=base)
+        off = base
+        for (wfmt, n), d1, hs, g, gd in zip(layout, singles, hosts, gs, gds):
+            if n:
+                gpu_step(d1, gd, h, index_base=off)
+                oracle_step(wfmt, hs, g, h, index_base=off)
+            off += n
+        torch.cuda.synchronize()
+        for (wfmt, n), d, d1, hs in zip(layout, devs, singles, hosts):
+            if not n:
+                continue
+            tag = f"multi {wfmt} n={n} t={t}"
+            w_g, m_g, v_g, ve_g = d.host()
+            assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+            assert_copy_equal(tag, d, hs)
+            for a, b in zip(d.host(), d1.host()):
+                assert a.tobytes() == b.tobytes(), tag
+            if hs.scales is not None:
+                sn = np.uint16 if wfmt == "e4m3" else np.uint8
+                assert (to_host(d.scales, sn) == hs.scales).all(), tag
+
+
+def test_nvfp4_master_llama7b_sampled():
+    """The 4-bit master setting with NVFP4 on the full 7B list (attention and
+    MLP linear weights NVFP4 with bf16 compute copies, the rest bf16), one
+    multi-tensor call per step; the oracle follows sampled whole 16-element
+    blocks, with each tensor's scale taken from the device."""
+    cfg = "c5"
+    specs = W.specs(cfg)
+    plan = W.low_precision_master_plan(cfg, "nvfp4")
+    free = free_device_bytes()
+    need = sum(s.numel for s in specs) * 19 + (1 << 30)
+    assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
+    rng = np.random.default_rng(38)
+    offsets = np.cumsum([0] + [s.numel for s in specs])
+    dev = dict(w=[], sc=[], cp=[], m=[], v=[], ve=[], g=[])
+    samples, hosts = [], []
+    for i, (s, (wfmt, blk, cp)) in enumerate(zip(specs, plan)):
+        x = W.init_fp32_device(cfg, i)
+        if blk:
+            w = torch.empty(s.numel // 2, dtype=torch.uint8, device="cuda")
+            sc = torch.empty(4 + s.numel // 16, dtype=torch.uint8, device="cuda")
+        else:
+            w = torch.empty(s.numel, dtype=torch.int16, device="cuda")
+            sc = None
+        B.madd_encode_weights(x, w, wfmt, scales=sc)
+        blen = 16 if blk else 128
+        nb = s.numel // blen
+        bidx = np.unique(np.concatenate([np.arange(4), np.arange(nb - 4, nb),
+                                         rng.choice(nb, size=min(nb, 64), replace=False)]))
+        idx = (bidx[:, None] * blen + np.arange(blen)[None, :]).ravel()
+        idx_t = torch.from_numpy(idx).cuda()
+        x_s = to_host(x[idx_t])
+        if blk:
+            byte_t = torch.from_numpy((bidx[:, None] * 8 + np.arange(8)[None, :]).ravel()).cuda()
+            st_bytes = to_host(sc[:4])
+            st = np.frombuffer(st_bytes.tobytes(), np.float32)[0]
+            assert st == np.float32(np.float32(float(x.abs().max())) / np.float32(2688.0)), s.name
+            codes_ref, pay_ref = reference_blocks(x_s, st)
+            codes_dev = to_host(sc[4 + torch.from_numpy(bidx).cuda()])
+            q_dev = to_host(w[byte_t])
+            assert (codes_dev == codes_ref).all(), s.name
+            assert (oracle.unpack_e2m1(q_dev) == pay_ref).all(), s.name
+            hs = HostState(q_dev, idx.size, np.concatenate([st_bytes, codes_dev]), copy=cp)
+        else:
+            byte_t = None
+            codes = oracle.encode_array(wfmt, x_s)
+            assert (to_host(w[idx_t], np.uint16) == codes).all(), s.name
+            hs = HostState(codes, idx.size, copy=cp)
+        del x
+        dev["w"].append(w)
+        dev["sc"].append(sc)
+        dev["cp"].append(torch.zeros(s.numel, dtype=torch.int16, device="cuda") if cp else None)
+        for k in ("m", "v", "ve"):
+            dev[k].append(torch.zeros(s.numel, device="cuda"))
+        dev["g"].append(torch.empty(s.numel, device="cuda"))
+        samples.append((idx, idx_t, bidx, byte_t))
+        hosts.append(hs)
+    tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
+                      scales=dev["sc"], copies=dev["cp"])
+    for t in (1, 2, 3):
+        for i in range(len(specs)):
+            W.grad_fp32_device_(cfg, i, t, dev["g"][i])
+        h = W.hparams(cfg, step=t)
+        B.madd_multi_tensor_step(tl, h)
+        for i, (idx, idx_t, bidx, byte_t) in enumerate(samples):
+            oracle_step(plan[i][0], hosts[i], to_host(dev["g"][i][idx_t]), h,
+                        gidx=idx + offsets[i])
+        torch.cuda.synchronize()
+        for i, (idx, idx_t, bidx, byte_t) in enumerate(samples):
+            hs, (wfmt, blk, cp) = hosts[i], plan[i]
+            tag = f"nvfp4-master {specs[i].name} t={t}"
+            w_got = to_host(dev["w"][i][byte_t]) if blk else to_host(dev["w"][i][idx_t], np.uint16)
+            assert_state_equal(tag, w_got, hs.w, to_host(dev["m"][i][idx_t]), hs.m,
+                               to_host(dev["v"][i][idx_t]), hs.v, to_host(dev["ve"][i][idx_t]),
+                               hs.ve)
+            if blk:
+                got = np.concatenate([to_host(dev["sc"][i][:4]),
+                                      to_host(dev["sc"][i][4 + torch.from_numpy(bidx).cuda()])])
+                assert (got == hs.scales).all(), tag
+            if cp:
+                assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag

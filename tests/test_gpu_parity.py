@@ -17,7 +17,7 @@ import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
 from gpu_parity_util import (CODE_NP, DevState, HostState, assert_copy_equal, assert_state_equal,
-                             gpu_step, oracle_step, to_dev, to_host)
+                             free_device_bytes, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -463,7 +463,7 @@ def test_one_tensor_past_2pow32_elements():
     past 16 GiB, chunk indices past 2^21), checked on samples at the start,
     across element 2^32 and at the ragged end."""
     n = 2 ** 32 + 4196
-    free, _ = torch.cuda.mem_get_info()
+    free = free_device_bytes()
     assert free > n * 24 + (1 << 30), "needs about 100 GiB of device memory"
     gen = torch.Generator(device="cuda")
     gen.manual_seed(5)
@@ -510,14 +510,14 @@ def test_config3_llama_1b_bf16_sr_moments_sampled():
 
 
 def test_config5_llama_7b_sampled():
-    free, _ = torch.cuda.mem_get_info()
+    free = free_device_bytes()
     need = 6_738_415_616 * 18 + (1 << 30)
     assert free > need, f"config 5 needs {need / 2**30:.0f} GiB of device memory"
     assert run_list_sampled("c5", 3, per_tensor=2048) == 6_738_415_616
 
 
 def test_config5_llama_7b_bf16_moments_sampled():
-    free, _ = torch.cuda.mem_get_info()
+    free = free_device_bytes()
     need = 6_738_415_616 * 12 + (1 << 30)
     assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
     assert run_list_sampled("c5", 2, per_tensor=1024, sfmt="bf16") == 6_738_415_616
