@@ -88,11 +88,14 @@ def cpu_threads() -> int:
     return max(1, min(n, 16))
 
 
-def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads: int = 1) -> dict:
+def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads: int = 1,
+                 seconds: float = 10.0) -> dict:
     """The CPU oracle on a bounded sample of the workload: the first `sample`
-    elements of the list, `steps` steps.  With several threads each runs the
-    unchanged oracle on a contiguous index range (the step is elementwise and
-    its draws are keyed by global index, so the split changes no result)."""
+    elements of the list, stepped until `seconds` have passed (at least two
+    steps), cycling through `steps` pre-generated gradient sets.  With several
+    threads each runs the unchanged oracle on a contiguous index range (the
+    step is elementwise and its draws are keyed by global index, so the split
+    changes no result)."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -122,15 +125,17 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
 
     with ThreadPoolExecutor(threads) as ex:
         t0 = time.perf_counter()
-        for t in range(1, steps + 1):
-            h = W.hparams(cfg, step=t)
-            list(ex.map(lambda k: part(k, t, h), range(threads)))
-        dt = time.perf_counter() - t0
-    return {"value": sample * steps / dt / 1e9, "unit": "Gparam/s", "cores": threads,
+        done, dt = 0, 0.0
+        while done < 2 or dt < seconds:
+            done += 1
+            h = W.hparams(cfg, step=done)
+            list(ex.map(lambda k: part(k, (done - 1) % steps + 1, h), range(threads)))
+            dt = time.perf_counter() - t0
+    return {"value": sample * done / dt / 1e9, "unit": "Gparam/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"first {sample:,} parameters of the list, {steps} steps "
-                      f"({dt:.1f} s on {threads} thread(s), scalar C, one contiguous index "
-                      "range per thread)"}
+            "sample": f"first {sample:,} parameters of the list, {done} steps cycling "
+                      f"{steps} gradient sets ({dt:.1f} s on {threads} thread(s), scalar C, "
+                      "one contiguous index range per thread)"}
 
 
 def main():
@@ -150,8 +155,10 @@ def main():
                          "same with NVFP4 linear layers")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
     ap.add_argument("--cpu-steps", type=int, default=None,
-                    help="oracle steps timed on the sample (default 10; 4 with bf16 moments, "
-                         "whose encoding makes the oracle slower)")
+                    help="gradient sets generated for the oracle's sample (default 10; 4 with "
+                         "bf16 moments)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="time the oracle steps the sample for (at least two steps)")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="host threads for the oracle (default: this process's CPUs, at most 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -369,7 +376,7 @@ def main():
         threads = args.cpu_threads or cpu_threads()
         log(f"timing the CPU oracle on a sample ({threads} threads)")
         steps = args.cpu_steps or (10 if args.states == "fp32" else 4)
-        cpu = cpu_baseline(cfg, args.cpu_sample, steps, sfmt, threads)
+        cpu = cpu_baseline(cfg, args.cpu_sample, steps, sfmt, threads, args.cpu_seconds)
 
     workload = WORKLOAD_NAMES[cfg]
     if shard:
