@@ -2,15 +2,16 @@
 // C ABI declared in include/madd.h.
 //
 // One fused, HBM-bound elementwise pass per step.  Per element it reads the
-// weight code, the gradient and the three fp32 moments, updates the moments,
+// weight code, the gradient and the three moments (fp32 or bf16), updates them,
 // forms the additive update u_a and the multiplicative update u_m
 // (Algorithm 1, with the optional clamps of Algorithm 2), combines
 // w + w u_m + u_a, and rounds the result back into the storage format (the
 // FP32-step / low-precision-storage round trip of Appendix B), to nearest-even
 // or stochastically with a Philox4x32-10 draw keyed by (seed, step, element).
 // Storage formats: bf16, FP8 E4M3 / E5M2 (optionally with FP16 scales per
-// 128-element block), and MXFP4 (E2M1 with an E8M0 scale per 32 elements)
-// for the 4-bit master-weight setting of Section 4.2.
+// 128-element block), and for the 4-bit master-weight setting of Section 4.2
+// NVFP4 (E2M1 with an E4M3 scale per 16 elements and an fp32 scale per
+// tensor) and MXFP4 (E2M1 with an E8M0 scale per 32 elements).
 //
 // Layout of work: a launch covers a list of tensors.  The element space of
 // each tensor is cut into chunks; one workgroup (256 threads, four wave64s)
@@ -89,7 +90,8 @@ struct TensorDesc {
   void* m;   // moments: fp32, or bf16 codes
   void* v;
   void* ve;
-  void* scales;    // FP16 codes (block FP8) or E8M0 codes (MXFP4)
+  void* scales;    // FP16 codes (block FP8), E8M0 codes (MXFP4), or fp32 tensor
+                   // scale then E4M3 codes (NVFP4)
   uint16_t* copy;  // optional bf16 compute copy of the new weights
   int64_t n;       // elements
   int64_t gbase;   // global index of element 0
@@ -101,15 +103,6 @@ struct TensorDesc {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u2 __attribute__((ext_vector_type(2)));
-
-template <typename T>
-__device__ __forceinline__ T ld_nt(const T* p) {
-  return __builtin_nontemporal_load(p);
-}
-template <typename T>
-__device__ __forceinline__ void st_nt(T* p, T x) {
-  __builtin_nontemporal_store(x, p);
-}
 
 // ---------------------------------------------------------------------------
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw; SC'11)
@@ -561,20 +554,18 @@ __device__ __forceinline__ void store_quad(const Quad<WF>& q, const TensorDesc& 
   st4s<SF>(d.ve, e, q.ve, md.ve);
 }
 
-// The bf16 compute copy of four new stored weights (value x scale for
-// block-scaled FP8), rounded to nearest-even.
-// The bf16 compute copy from the four new stored values (block-scaled: payload
-// value already multiplied by the block scale).
+// The bf16 compute copy (rounded to nearest-even) of four new stored weights,
+// given as values (block-scaled: payload value already multiplied by the
+// block's factor).
 __device__ __forceinline__ void store_copy_values(const float (&v)[4], uint16_t* copy, int64_t e) {
   stg<u2>(copy + e, u2{enc_bf16x2(v[0], v[1], false, 0u, 0u), enc_bf16x2(v[2], v[3], false, 0u, 0u)});
 }
 
 template <int WF>
-__device__ __forceinline__ void store_copy(const WQuad<WF>& w, float scale, uint16_t* copy,
-                                           int64_t e) {
+__device__ __forceinline__ void store_copy(const WQuad<WF>& w, uint16_t* copy, int64_t e) {
   float v[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) v[k] = decode<WF>(w.code(k)) * scale;
+  for (int k = 0; k < 4; ++k) v[k] = decode<WF>(w.code(k));
   store_copy_values(v, copy, e);
 }
 
@@ -756,10 +747,10 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
       mdraws_aligned<SF>(gpair, s, mA, mB);
       step_quad<WF, SR, CLAMP>(qa, rA, s);
       store_quad<WF, SF>(qa, d, eA, mA);
-      if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
+      if (COPY && d.copy) store_copy<WF>(qa.w, d.copy, eA);
       step_quad<WF, SR, CLAMP>(qb, rB, s);
       store_quad<WF, SF>(qb, d, eB, mB);
-      if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
+      if (COPY && d.copy) store_copy<WF>(qb.w, d.copy, eB);
       continue;
     }
     if (fullA) load_quad<WF, GF, SF>(qa, d, eA);
@@ -770,14 +761,14 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
     if (fullA) {
       step_quad<WF, SR, CLAMP>(qa, rA, s);
       store_quad<WF, SF>(qa, d, eA, mA);
-      if (COPY && d.copy) store_copy<WF>(qa.w, 1.0f, d.copy, eA);
+      if (COPY && d.copy) store_copy<WF>(qa.w, d.copy, eA);
     } else if (eA < cend) {
       step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eA, eA + kQuad < cend ? eA + kQuad : cend, s);
     }
     if (fullB) {
       step_quad<WF, SR, CLAMP>(qb, rB, s);
       store_quad<WF, SF>(qb, d, eB, mB);
-      if (COPY && d.copy) store_copy<WF>(qb.w, 1.0f, d.copy, eB);
+      if (COPY && d.copy) store_copy<WF>(qb.w, d.copy, eB);
     } else if (eB < cend) {
       step_scalar_range<WF, GF, SF, SR, CLAMP, COPY>(d, eB, eB + kQuad < cend ? eB + kQuad : cend, s);
     }
@@ -787,10 +778,9 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
 // Block-scaled storage: the kBlk / 4 consecutive lanes that hold one block of
 // a sub-tile (32 lanes for a 128-element FP8 block, 8 for a 32-element MXFP4
 // block, 4 for a 16-element NVFP4 block) combine the block's max |w'| with
-// lane shuffles.  The launch
-// requires n to be a multiple of the block length, so a block is never split
-// and whole lane groups are active or inactive together; every lane runs the
-// shuffles and the draw exchange.
+// lane shuffles.  The launch requires n to be a multiple of the block length,
+// so a block is never split and whole lane groups are active or inactive
+// together; every lane runs the shuffles and the draw exchange.
 template <int WF>
 constexpr int block_len() {
   return WF == WF_MXFP4 ? kMxBlock : (WF == WF_NVFP4 ? kNvBlock : kBlock);
