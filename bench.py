@@ -43,6 +43,20 @@ def bytes_per_param(wfmt: str, sfmt: str) -> float:
     """Algorithmic bytes: read w, g (fp32), m, v, v_e; write w, m, v, v_e."""
     return 2 * WBYTES[wfmt] + 4 + 6 * SBYTES[sfmt]
 
+
+def algorithmic_bytes(sizes, plan, sfmt: str) -> float:
+    """Bytes one step over a tensor list must move: every array read and
+    written once, plus per tensor its bf16 compute copy (written) and its
+    block scales (read and written: FP16 per 128 elements for FP8, E8M0 per
+    32 for MXFP4, E4M3 per 16 for NVFP4, whose fp32 tensor scale is read).
+    `plan` holds (weight format, block-scaled, compute copy) per tensor."""
+    total = 0.0
+    for n, (wf, blk, cp) in zip(sizes, plan):
+        total += n * bytes_per_param(wf, sfmt) + (n * 2 if cp else 0)
+        if blk:
+            total += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4}.get(wf, (n // 128) * 4)
+    return total
+
 WORKLOAD_NAMES = {
     "c5": "llama-7b-shaped list (32 layers, d=4096, SwiGLU 11008, vocab 32000)",
     "c3": "llama-1.1b-shaped list (22 layers, d=2048, GQA 32/4, SwiGLU 5632, vocab 32000)",
@@ -322,16 +336,10 @@ def main():
         f"max {max(per_launch_ms):.3f} ms")
 
     n_step = hi - lo
-    alg_bytes = 0.0
     if shard:
         alg_bytes = n_step * bytes_per_param(wfmt, args.states)
     else:
-        for n, (wf, blk, cp) in zip(sizes, plan):
-            alg_bytes += n * bytes_per_param(wf, args.states) + (n * 2 if cp else 0)
-            if blk:  # scale read + written: FP16 per 128 (FP8), E8M0 per 32 (MXFP4),
-                # E4M3 per 16 plus the fp32 tensor scale read (NVFP4)
-                alg_bytes += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4}.get(
-                    wf, (n // 128) * 4)
+        alg_bytes = algorithmic_bytes(sizes, plan, args.states)
     bpp = alg_bytes / n_step
     achieved = alg_bytes / (avg_launch_ms / 1e3) / 1e9
 

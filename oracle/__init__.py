@@ -16,11 +16,11 @@ What each function follows in the paper:
                        FP32-step / BF16-storage round trip of Appendix B.
   * ``step_block``  -- the same step on FP8 payloads with FP16 block scales
                        (Section 4.2, FP8 master-weight setting).
-  * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
-                       E8M0 scale per 32 elements; the format stands in for
-                       the 4-bit master weights of Section 4.2).
   * ``step_nv``     -- the same step on NVFP4 storage (E2M1 payloads, one E4M3
-                       scale per 16 elements, one fp32 scale per tensor).
+                       scale per 16 elements, one fp32 scale per tensor; the
+                       format of the 4-bit master weights of Section 4.2).
+  * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
+                       E8M0 scale per 32 elements; OCP's 4-bit block format).
   * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
                        storage formats' value grids.
   * ``philox`` / ``draw16`` -- the counter-based generator that keys
@@ -32,8 +32,10 @@ implementation; everything else is pinned by closed forms, limits,
 invariants, library conversions and brute force (see the tests).  Parity
 unpinned against the paper (the paper does not fix them): the exact fp32
 operation order, the block-scaled FP8 block length and scale rule, the 4-bit
-format (``step_mx``: pinned to the OCP MX specification instead) and the
-stochastic-rounding rule with its generator.
+formats (``step_mx`` and ``step_nv``: pinned to the OCP MX specification and
+to NVFP4's published definition instead; when NVFP4's tensor scale is
+refreshed is a choice, at encoding) and the stochastic-rounding rule with its
+generator.
 """
 from __future__ import annotations
 
