@@ -349,7 +349,9 @@ def main():
                                  vebuf[lo:hi], 4 if args.states == "fp32" else 2, args.steps,
                                  stream, alg_bytes, achieved)
         log(f"streaming ceiling: {ceiling['achieved']:.1f} GB/s; the step reaches "
-            f"{ceiling['step_frac_of_ceiling'] * 100:.1f}% of it")
+            f"{ceiling['step_frac_of_ceiling'] * 100:.1f}% of it; plain streams: read "
+            f"{ceiling['read_only_gbs']:.0f}, write {ceiling['write_only_gbs']:.0f}, copy "
+            f"{ceiling['copy_gbs']:.0f} GB/s")
 
     if args.copy_probe_gib > 0:
         nbytes = int(args.copy_probe_gib * 2**30) // 4 * 4
@@ -446,10 +448,43 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
     torch.cuda.synchronize()
     ms = ev[0].elapsed_time(ev[-1]) / steps
     gbs = alg_bytes / (ms / 1e3) / 1e9
-    return {"kernel": "madd_ceiling_stream (same buffers and bytes, no arithmetic)",
-            "avg_launch_ms": round(ms, 4), "achieved": round(gbs, 1), "unit": "GB/s",
-            "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
-            "step_frac_of_ceiling": round(step_gbs / gbs, 4)}
+    out = {"kernel": "madd_ceiling_stream (same buffers and bytes, no arithmetic)",
+           "avg_launch_ms": round(ms, 4), "achieved": round(gbs, 1), "unit": "GB/s",
+           "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+           "step_frac_of_ceiling": round(step_gbs / gbs, 4)}
+    out.update(stream_modes(lib, steps, stream))
+    return out
+
+
+def stream_modes(lib, steps, stream, gib: int = 8) -> dict:
+    """HBM bandwidth of plain read-only, write-only and copy streams in the
+    step's access shape (madd_stream_modes) over two fresh `gib` GiB buffers."""
+    import ctypes
+
+    import torch
+
+    lib.madd_stream_modes.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_int64, ctypes.c_void_p]
+    lib.madd_stream_modes.restype = ctypes.c_int32
+    nbytes = gib << 30
+    a = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    res = {}
+    for mode, name, moved in ((0, "read_only_gbs", nbytes), (1, "write_only_gbs", nbytes),
+                              (2, "copy_gbs", 2 * nbytes)):
+        args = (mode, a.data_ptr(), b.data_ptr(), nbytes, stream.cuda_stream)
+        for _ in range(2):
+            assert lib.madd_stream_modes(*args) == 0
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(steps):
+            assert lib.madd_stream_modes(*args) == 0
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        res[name] = round(moved / (ev[0].elapsed_time(ev[1]) / steps / 1e3) / 1e9, 1)
+    del a, b
+    return res
 
 
 if __name__ == "__main__":

@@ -14,6 +14,12 @@
  * written back unchanged (each value is XORed with the gradient's bits
  * masked by a runtime zero), so the probe can run on live optimizer state.
  *
+ * madd_stream_modes: plain streams in the same access shape (a 256-thread
+ * workgroup per 8 KiB tile, 16 bytes per thread in each 4 KiB half,
+ * non-temporal): read only, write only, or copy.  Together with the
+ * ceiling probe they place the step between what HBM delivers for reads
+ * alone, for writes alone and for the step's own read:write mix.
+ *
  * madd_probe_bf16_rounding: the step kernel rounds fp32 to bf16 with the
  * v_cvt_pk_bf16_f32 (round to nearest-even) and v_cvt_sr_bf16_f32
  * (stochastic) instructions.  The probe runs both on all 2^32 fp32 bit
@@ -41,6 +47,16 @@ extern "C" {
  * fails; nothing is launched on an error. */
 int32_t madd_ceiling_stream(void* w, const float* g, void* m, void* v, void* ve,
                             int32_t state_bytes, int64_t n, void* stream);
+
+/* One pass of a plain stream over `bytes` bytes (a positive multiple of
+ * 8192): mode 0 reads a (and writes at most the first 4 KiB of b, and only
+ * when an XOR of what it read equals a fixed key, which keeps the loads
+ * alive), mode 1 writes b, mode 2 copies a to b.  DEVICE pointers, 16-byte
+ * aligned, owned by the caller; a may be NULL in mode 1.  Enqueued on
+ * `stream`.  Returns 0, -1 for an invalid argument (unknown mode, bad size,
+ * NULL pointer), -2 for an unaligned pointer, -4 when the launch fails;
+ * nothing is launched on an error. */
+int32_t madd_stream_modes(int32_t mode, const void* a, void* b, int64_t bytes, void* stream);
 
 /* Exhaustive check of the two bf16 conversion instructions.
  * counters: DEVICE array of 4 uint64 values owned by the caller, which the

@@ -1,5 +1,8 @@
 // Device probes declared in include/madd_probes.h.
 //
+// Plain read-only, write-only and copy streams (madd_stream_modes) measure
+// what HBM delivers for each direction alone in the same access shape.
+//
 // Streaming-ceiling probe for the M+Adam step: the step kernel's bytes and
 // work mapping without its arithmetic.  A workgroup of 256 threads owns 2048 elements; thread t
 // moves elements [4t, 4t+4) of both 1024-element sub-tiles, all loads of a
@@ -139,7 +142,52 @@ __global__ __launch_bounds__(256) void bf16_rounding_kernel(unsigned long long* 
   if (threadIdx.x == 0) atomicAdd(&c[3], 256ull * 256ull);  // this workgroup's inputs
 }
 
+// Plain streams in the step's access shape: a 256-thread workgroup owns one
+// 8 KiB tile and thread t moves 16 bytes at offset 16 t of each 4 KiB half,
+// non-temporal.  Read: the loads feed an XOR that is stored (to the sink's
+// first 4 KiB) only if it equals `key`, so the compiler keeps every load.
+constexpr int64_t kStreamTile = 8192;
+constexpr int kHalf16 = 256;  // 16-byte words per half tile
+
+__global__ __launch_bounds__(kThreads) void stream_read_kernel(const u4* a, u4* sink, uint32_t key) {
+  const int64_t i = (int64_t)blockIdx.x * (2 * kHalf16) + threadIdx.x;
+  const u4 x = ldg<u4>(a + i), y = ldg<u4>(a + i + kHalf16);
+  const u4 z = x ^ y;
+  if ((z.x ^ z.y ^ z.z ^ z.w) == key) sink[threadIdx.x] = z;
+}
+__global__ __launch_bounds__(kThreads) void stream_write_kernel(u4* b) {
+  const int64_t i = (int64_t)blockIdx.x * (2 * kHalf16) + threadIdx.x;
+  const uint32_t v = (uint32_t)i, u = v + (uint32_t)kHalf16;  // word k holds k
+  stg<u4>(b + i, u4{v, v, v, v});
+  stg<u4>(b + i + kHalf16, u4{u, u, u, u});
+}
+__global__ __launch_bounds__(kThreads) void stream_copy_kernel(const u4* a, u4* b) {
+  const int64_t i = (int64_t)blockIdx.x * (2 * kHalf16) + threadIdx.x;
+  const u4 x = ldg<u4>(a + i), y = ldg<u4>(a + i + kHalf16);
+  stg<u4>(b + i, x);
+  stg<u4>(b + i + kHalf16, y);
+}
+
 }  // namespace
+
+extern "C" int32_t madd_stream_modes(int32_t mode, const void* a, void* b, int64_t bytes,
+                                     void* stream) {
+  if (mode < 0 || mode > 2 || bytes <= 0 || bytes % kStreamTile != 0) return -1;
+  if (!b || (mode != 1 && !a)) return -1;
+  if (!al16(b) || (mode != 1 && !al16(a))) return -2;
+  const int64_t tiles = bytes / kStreamTile;
+  if (tiles > 0x7FFFFFFFll) return -1;
+  hipStream_t st = (hipStream_t)stream;
+  const dim3 grid((unsigned)tiles);
+  if (mode == 0)
+    hipLaunchKernelGGL(stream_read_kernel, grid, dim3(kThreads), 0, st, (const u4*)a, (u4*)b,
+                       0x9E3779B9u);
+  else if (mode == 1)
+    hipLaunchKernelGGL(stream_write_kernel, grid, dim3(kThreads), 0, st, (u4*)b);
+  else
+    hipLaunchKernelGGL(stream_copy_kernel, grid, dim3(kThreads), 0, st, (const u4*)a, (u4*)b);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
 
 extern "C" int32_t madd_probe_bf16_rounding(uint64_t* counters, void* stream) {
   if (!counters) return -1;

@@ -48,6 +48,16 @@ def test_ceiling_probe_rejects_bad_arguments():
     assert f(None, FAKE, FAKE, FAKE, FAKE, 4, 64, None) == -1
     assert f(FAKE, FAKE + 4, FAKE, FAKE, FAKE, 4, 64, None) == -2
     assert f(None, None, None, None, None, 2, 0, None) == 0
+    sm = L.madd_stream_modes
+    sm.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.c_void_p]
+    sm.restype = ctypes.c_int32
+    assert sm(3, FAKE, FAKE, 8192, None) == -1           # no such mode
+    assert sm(2, FAKE, FAKE, 4096, None) == -1           # not a multiple of 8192
+    assert sm(2, FAKE, FAKE, 0, None) == -1
+    assert sm(0, None, FAKE, 8192, None) == -1           # read needs a
+    assert sm(1, FAKE, None, 8192, None) == -1           # every mode needs b
+    assert sm(2, FAKE + 8, FAKE, 8192, None) == -2       # unaligned
     L.madd_probe_bf16_rounding.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     L.madd_probe_bf16_rounding.restype = ctypes.c_int32
     assert L.madd_probe_bf16_rounding(None, None) == -1

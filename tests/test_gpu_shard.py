@@ -114,3 +114,30 @@ def test_ceiling_probe_writes_back_what_it_read(state_bytes, n):
     torch.cuda.synchronize()
     for a, b in zip(before, (w, *st)):
         assert torch.equal(a, b)
+
+
+def test_stream_modes_move_exactly_their_bytes():
+    L = ctypes.CDLL(_build.PROBE_LIB)
+    f = L.madd_stream_modes
+    f.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                  ctypes.c_void_p]
+    f.restype = ctypes.c_int32
+    nbytes = 8192 * 37
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    a = torch.randint(-2**31, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, device="cuda",
+                      generator=gen)
+    b = torch.zeros_like(a)
+    st = torch.cuda.current_stream().cuda_stream
+    assert f(2, a.data_ptr(), b.data_ptr(), nbytes, st) == 0          # copy
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert f(1, None, b.data_ptr(), nbytes, st) == 0                  # write: word k of 16 B
+    torch.cuda.synchronize()
+    want = torch.arange(nbytes // 16, device="cuda", dtype=torch.int64).to(torch.int32)
+    assert torch.equal(b.view(-1, 4), want[:, None].expand(-1, 4))
+    z = torch.zeros_like(a)                                           # XOR 0 never meets the key
+    before = b.clone()
+    assert f(0, z.data_ptr(), b.data_ptr(), nbytes, st) == 0          # read
+    torch.cuda.synchronize()
+    assert torch.equal(b, before)
