@@ -188,9 +188,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures the optimizer step on one GPU only; multi-GPU runs are not "
-              "part of this build (the step shards by index range without communication).",
-              file=sys.stderr)
+        print("bench.py measures the optimizer step on one GPU only; runs on several GPUs "
+              "are not implemented (the step shards by index range without communication: "
+              "use --shard K/P to time one GPU's share).", file=sys.stderr)
         sys.exit(2)
 
     import torch
