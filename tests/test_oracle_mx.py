@@ -224,3 +224,24 @@ def test_mx_step_validation():
     z = [np.zeros(48, np.float32) for _ in range(4)]
     with pytest.raises(oracle.OracleError):
         oracle.step_mx(np.zeros(24, np.uint8), np.zeros(1, np.uint8), *z, hp())
+
+
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_mx_zero_learning_rates_keep_every_stored_value(rounding):
+    # eta_a = eta_m = 0 gives w' = the stored value q X.  A block whose largest
+    # |q| is below 4 gets a smaller power-of-two scale X' = X 2^-k, and q 2^k
+    # is again an E2M1 value (the grid doubles onto itself below 6), so the
+    # scale code may change but no stored value does.
+    rng = np.random.default_rng(15)
+    nb = 200
+    x = (rng.normal(0, 1, (nb, 32)) * 10.0 ** rng.uniform(-6, 2, nb)[:, None]).astype(np.float32)
+    x[0] = 0.0
+    x[1] = 0.0
+    x[1, 5] = 3e-3
+    x = x.ravel()
+    q, s = oracle.encode_mx(x)
+    before = oracle.mx_values(q, s).copy()
+    z = [np.zeros(x.size, np.float32) for _ in range(3)]
+    g = rng.normal(0, 1e-2, x.size).astype(np.float32)
+    oracle.step_mx(q, s, g, *z, hp(lr_add=0.0, lr_mul=0.0, rounding=rounding, seed=4))
+    assert (oracle.mx_values(q, s) == before).all()

@@ -152,3 +152,49 @@ def test_validation():
     z = [np.zeros(40, np.float32) for _ in range(4)]
     with pytest.raises(oracle.OracleError):
         oracle.step_nv(np.zeros(20, np.uint8), np.zeros(6, np.uint8), *z, hp())
+
+
+def test_nv_sr_keys_by_global_index():
+    rng = np.random.default_rng(23)
+    n = 16 * 16
+    x = rng.normal(0, 0.05, n).astype(np.float32)
+    g = rng.normal(0, 1e-2, n).astype(np.float32)
+    outs = []
+    for kw in (dict(index_base=4000), dict(gidx=4000 + np.arange(n))):
+        q, s = oracle.encode_nv(x)
+        z = [np.zeros(n, np.float32) for _ in range(3)]
+        oracle.step_nv(q, s, g, *z, hp(rounding="sr", seed=10, lr_add=1e-2), **kw)
+        outs.append((q.copy(), s.copy()))
+    assert (outs[0][0] == outs[1][0]).all() and (outs[0][1] == outs[1][1]).all()
+    q, s = oracle.encode_nv(x)
+    z = [np.zeros(n, np.float32) for _ in range(3)]
+    oracle.step_nv(q, s, g, *z, hp(rounding="sr", seed=10, lr_add=1e-2), index_base=0)
+    assert (q != outs[0][0]).any()
+
+
+def test_nv_zero_learning_rates_keep_blocks_whose_largest_payload_is_six():
+    # eta_a = eta_m = 0 gives w' = q D.  A block whose largest |q| is 6 has
+    # amax' = 6 D, which the block rule maps back to the same code whenever
+    # 6 D / fp32(6 s_t) rounds to E4M3(c) (checked here with numpy); those
+    # blocks keep every payload.  Other blocks may be re-scaled: the NVFP4
+    # block rule is not idempotent on its own output.
+    rng = np.random.default_rng(24)
+    n = 64 * 16
+    q, s = oracle.encode_nv(rng.normal(0, 0.05, n).astype(np.float32))
+    st = tensor_scale(s)
+    vals = oracle.nv_values(q, s).reshape(-1, 16)
+    codes0 = s[4:].copy()
+    six = np.array([np.abs(oracle.decode_array("e2m1", oracle.unpack_e2m1(q)[16 * b:16 * b + 16])).max()
+                    == 6.0 for b in range(n // 16)])
+    amax = np.abs(vals).max(axis=1).astype(np.float32)
+    same = np.array([e4m3_code(np.float32(a / np.float32(np.float32(6.0) * st))) == c
+                     for a, c in zip(amax, codes0)])
+    keep = six & same
+    assert keep.sum() > 10
+    z = [np.zeros(n, np.float32) for _ in range(3)]
+    g = rng.normal(0, 1e-2, n).astype(np.float32)
+    oracle.step_nv(q, s, g, *z, hp(lr_add=0.0, lr_mul=0.0, seed=5))
+    after = oracle.nv_values(q, s).reshape(-1, 16)
+    assert (s[4:][keep] == codes0[keep]).all()
+    assert (after[keep] == vals[keep]).all()
+    assert (np.abs(after - vals) <= np.abs(vals) * 0.5 + 1e-30).all()
