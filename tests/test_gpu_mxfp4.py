@@ -255,3 +255,10 @@ def test_fp4_master_llama7b_sampled():
                 assert (got == hs.scales).all(), tag
             if cp:
                 assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag
+
+
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_zero_learning_rates(rounding):
+    """Both rates zero: every stored value is kept (the scale may be
+    renormalized by a power of two); GPU and oracle agree."""
+    run_mx(3 * 2048 + 96, 3, 17, dict(rounding=rounding, lr_add=0.0, lr_mul=0.0), copy=True)

@@ -261,3 +261,10 @@ def test_nvfp4_master_llama7b_sampled():
                 assert (got == hs.scales).all(), tag
             if cp:
                 assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag
+
+
+@pytest.mark.parametrize("rounding", ["rne", "sr"])
+def test_zero_learning_rates(rounding):
+    """Both rates zero: the step re-derives every block code from the stored
+    values (not idempotent for NVFP4 in general); GPU and oracle agree."""
+    run_nv(3 * 2048 + 48, 3, 39, dict(rounding=rounding, lr_add=0.0, lr_mul=0.0), copy=True)
