@@ -24,6 +24,7 @@ WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32,
         "mxfp4": W_MXFP4, "nvfp4": W_NVFP4}
 MX_BLOCK = 32  # elements per MXFP4 block (one E8M0 scale byte)
 NV_BLOCK = 16  # elements per NVFP4 block (one E4M3 scale byte after the fp32 tensor scale)
+_WFMT_NAME = {v: k for k, v in WFMT.items()}
 GFMT = {"fp32": G_FP32, "bf16": G_BF16}
 S_FP32, S_BF16, S_BF16_SR = 0, 1, 2
 SFMT = {"fp32": S_FP32, "bf16": S_BF16, "bf16_sr": S_BF16_SR}
@@ -137,6 +138,47 @@ def _stream(stream) -> int | None:
     return stream.cuda_stream
 
 
+# Bytes per element of each storage, for the size checks below (the C ABI
+# receives bare pointers and cannot check them).
+CODE_BYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "fp32": 4, "mxfp4": 0.5, "nvfp4": 0.5}
+GRAD_BYTES = {"fp32": 4, "bf16": 2}
+STATE_BYTES = {"fp32": 4, "bf16": 2, "bf16_sr": 2}
+
+
+def scale_bytes(wfmt: str, n: int) -> int:
+    """Bytes of the block-scale array of n elements: FP16 per 128 (block FP8),
+    E8M0 per 32 (MXFP4), the fp32 tensor scale then E4M3 per 16 (NVFP4)."""
+    if wfmt == "mxfp4":
+        return n // MX_BLOCK
+    if wfmt == "nvfp4":
+        return 4 + n // NV_BLOCK
+    return (n // 128) * 2
+
+
+def _need(what: str, t, nbytes: int):
+    """A tensor argument must be a contiguous GPU tensor of at least `nbytes`
+    bytes (a raw int pointer is the caller's responsibility)."""
+    if t is None or isinstance(t, int):
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a GPU tensor (got one on {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what} holds {have} bytes; the call reads or writes {nbytes}")
+
+
+def _need_tensor(fn: str, wfmt: str, n: int, w, m, v, ve, sfmt: str, scales=None, copy=None):
+    _need(f"{fn}: w", w, math.ceil(n * CODE_BYTES[wfmt]))
+    for name, t in (("m", m), ("v", v), ("ve", ve)):
+        _need(f"{fn}: {name}", t, n * STATE_BYTES[sfmt])
+    if scales is not None:
+        _need(f"{fn}: scales", scales, scale_bytes(wfmt, n))
+    if copy is not None:
+        _need(f"{fn}: copy", copy, 2 * n)
+
+
 def _check(fn: str, rc: int):
     if rc != 0:
         raise MaddError(fn, rc)
@@ -165,12 +207,19 @@ def state_format(t) -> str:
 def madd_init_state(m, v, ve, sfmt: str | None = None, stream=None):
     n = m.numel()
     sfmt = sfmt or state_format(m)
+    for name, t in (("m", m), ("v", v), ("ve", ve)):
+        _need(f"madd_init_state: {name}", t, n * STATE_BYTES[sfmt])
     _check("madd_init_state", lib().madd_init_state(_ptr(m), _ptr(v), _ptr(ve), SFMT[sfmt], n,
                                                     _stream(stream)))
 
 
 def madd_encode_weights(x, w, wfmt: str, scales=None, stream=None):
     """Round fp32 ``x`` into the storage ``w`` (and its block ``scales``)."""
+    n = x.numel()
+    _need("madd_encode_weights: x", x, 4 * n)
+    _need("madd_encode_weights: w", w, math.ceil(n * CODE_BYTES[wfmt]))
+    if scales is not None:
+        _need("madd_encode_weights: scales", scales, scale_bytes(wfmt, n))
     _check("madd_encode_weights",
            lib().madd_encode_weights(_ptr(x), _ptr(w), WFMT[wfmt], _ptr(scales), x.numel(),
                                      _stream(stream)))
@@ -187,6 +236,8 @@ def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, in
     h = _hp(hp)
     n = m.numel() if n is None else n
     sfmt = sfmt or state_format(m)
+    _need_tensor("madd_step", wfmt, n, w, m, v, ve, sfmt, scales, copy)
+    _need("madd_step: g", g, n * GRAD_BYTES[gfmt])
     _check("madd_step",
            lib().madd_step(_ptr(w), WFMT[wfmt], _ptr(scales), _ptr(copy), _ptr(g), GFMT[gfmt],
                            _ptr(m), _ptr(v), _ptr(ve), SFMT[sfmt], int(n), int(index_base),
@@ -197,17 +248,23 @@ def madd_plain_step(w, wfmt: str, g, hp, gfmt: str = "fp32", index_base: int = 0
     """One step of Appendix B's moment-free rules (additive: lr_mul = 0,
     multiplicative: lr_add = 0, combined: both) on one tensor."""
     h = _hp(hp)
+    _need("madd_plain_step: g", g, w.numel() * GRAD_BYTES[gfmt])
     _check("madd_plain_step",
            lib().madd_plain_step(_ptr(w), WFMT[wfmt], _ptr(g), GFMT[gfmt], w.numel(),
                                  int(index_base), ctypes.byref(h), _stream(stream)))
 
 
 class TensorList:
-    """Marshalled pointer arrays of a tensor list, built once and reused."""
+    """Marshalled pointer arrays of a tensor list, built once and reused.  It
+    holds references to every tensor it points into, so the memory stays
+    allocated for as long as the list can be stepped."""
 
     def __init__(self, ws, wfmts, gs, ms, vs, ves, scales=None, sfmt: str | None = None,
                  copies=None):
         k = len(ws)
+        self._tensors = [list(ws), list(gs), list(ms), list(vs), list(ves),
+                         list(scales) if scales is not None else [],
+                         list(copies) if copies is not None else []]
         self.sfmt = sfmt or (state_format(ms[0]) if k else "fp32")
         assert all(len(x) == k for x in (wfmts, gs, ms, vs, ves))
         self.n = k
@@ -223,16 +280,34 @@ class TensorList:
                                            for f in wfmts])
         self.numel = (ctypes.c_int64 * k)(*[t.numel() for t in ms])
         self.total = sum(t.numel() for t in ms)
+        for i in range(k):
+            f = wfmts[i] if isinstance(wfmts[i], str) else _WFMT_NAME[int(wfmts[i])]
+            _need_tensor(f"TensorList[{i}]", f, ms[i].numel(), ws[i], ms[i], vs[i], ves[i],
+                         self.sfmt, scales[i] if scales is not None else None,
+                         copies[i] if copies is not None else None)
+        self._grads_ok = set()  # gradient formats the current gradients were checked for
 
     def set_grads(self, gs):
+        gs = list(gs)
+        assert len(gs) == self.n
         for i, t in enumerate(gs):
             self.g[i] = _ptr(t)
+        self._tensors[1] = gs
+        self._grads_ok = set()
+
+    def check_grads(self, gfmt: str):
+        if gfmt in self._grads_ok:
+            return
+        for i, t in enumerate(self._tensors[1]):
+            _need(f"TensorList[{i}]: g", t, self.numel[i] * GRAD_BYTES[gfmt])
+        self._grads_ok.add(gfmt)
 
 
 def madd_multi_tensor_step(tl: TensorList, hp, gfmt: str = "fp32", index_base: int = 0,
                            stream=None):
     """One step over a TensorList (one launch per weight format)."""
     h = _hp(hp)
+    tl.check_grads(gfmt)
     PP = ctypes.POINTER(ctypes.c_void_p)
     cast = lambda a: ctypes.cast(a, PP) if a is not None else None  # noqa: E731
     _check("madd_multi_tensor_step",

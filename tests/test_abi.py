@@ -209,3 +209,21 @@ def test_binding_has_no_cpu_fallback(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "_lib", None)
     with pytest.raises(ImportError):
         B.lib()
+
+
+def test_binding_rejects_host_tensors_before_any_call():
+    import torch
+    t16 = torch.zeros(64, dtype=torch.int16)
+    t32 = torch.zeros(64)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.madd_step(t16, "bf16", t32, t32, t32, t32, _hp()[1])
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.madd_init_state(t32, t32, t32)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.madd_encode_weights(t32, t16, "bf16")
+
+
+def test_scale_bytes():
+    assert B.scale_bytes("e4m3", 1024) == 16
+    assert B.scale_bytes("mxfp4", 1024) == 32
+    assert B.scale_bytes("nvfp4", 1024) == 68

@@ -589,3 +589,30 @@ def test_fp8_master_llama7b_sampled():
                 assert (got == hs.scales).all(), tag
             if cp:
                 assert (to_host(dev["cp"][i][idx_t], np.uint16) == hs.copy).all(), tag
+
+
+def test_binding_checks_buffer_sizes_before_launch():
+    """The binding refuses tensors too small for the call, non-contiguous
+    ones and short scale arrays, so no kernel touches memory past a buffer."""
+    n = 4096
+    w = torch.zeros(n, dtype=torch.int16, device="cuda")
+    g, m, v, ve = (torch.zeros(n, device="cuda") for _ in range(4))
+    with pytest.raises(ValueError, match="bytes"):
+        B.madd_step(w[:n - 8], "bf16", g, m, v, ve, hp())
+    with pytest.raises(ValueError, match="bytes"):
+        B.madd_step(w, "bf16", g[:n - 4], m, v, ve, hp())
+    with pytest.raises(ValueError, match="contiguous"):
+        B.madd_step(w, "bf16", torch.zeros(2 * n, device="cuda")[::2], m, v, ve, hp())
+    q = torch.zeros(n // 2, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError, match="scales"):
+        B.madd_step(q, "nvfp4", g, m, v, ve, hp(),
+                    scales=torch.zeros(n // 16, dtype=torch.uint8, device="cuda"))
+    with pytest.raises(ValueError, match="copy"):
+        B.madd_step(w, "bf16", g, m, v, ve, hp(), copy=w[:10])
+    with pytest.raises(ValueError, match="bytes"):
+        B.TensorList([w], ["bf16"], [g], [m], [v[:100]], [ve])
+    tl = B.TensorList([w], ["bf16"], [g[:n // 2]], [m], [v], [ve])
+    with pytest.raises(ValueError, match="bytes"):
+        B.madd_multi_tensor_step(tl, hp())
+    torch.cuda.synchronize()
+    assert (m == 0).all() and (w == 0).all()
