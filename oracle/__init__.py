@@ -19,6 +19,9 @@ What each function follows in the paper:
   * ``step_nv``     -- the same step on NVFP4 storage (E2M1 payloads, one E4M3
                        scale per 16 elements, one fp32 scale per tensor; the
                        format of the 4-bit master weights of Section 4.2).
+  * ``step_nv_current`` -- the NVFP4 step with its per-tensor scale derived
+                       anew from the updated tensor, as a dequantize / FP32
+                       step / quantize round trip does.
   * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
                        E8M0 scale per 32 elements; OCP's 4-bit block format).
   * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
@@ -103,6 +106,8 @@ def lib():
         L.oracle_encode_mx.restype = I
         L.oracle_step_nv.argtypes = [P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step_nv.restype = I
+        L.oracle_step_nv_current.argtypes = [P, P, P, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_nv_current.restype = I
         L.oracle_encode_nv.argtypes = [P, P, P, I64]
         L.oracle_encode_nv.restype = I
         L.oracle_decode.argtypes = [I, U32]
@@ -246,6 +251,44 @@ def step_nv(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray, v: 
                               *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_nv returned {rc}")
+
+
+def step_nv_current(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray,
+                    v: np.ndarray, ve: np.ndarray, hp: dict, index_base: int = 0,
+                    gidx: np.ndarray | None = None, sfmt: str = "fp32",
+                    copy: np.ndarray | None = None):
+    """NVFP4 step with current scaling: ``scales`` holds 8 + n/16 bytes (the
+    fp32 per-tensor scale, a word receiving the bits of the largest finite
+    |w'|, then the E4M3 block codes); the per-tensor scale is derived anew
+    from the updated tensor.  ``g`` (fp32) receives the updated weights w'."""
+    n = 2 * q.size
+    if q.dtype != np.uint8 or scales.dtype != np.uint8 or scales.size != 8 + n // 16:
+        raise OracleError("q must be n/2 packed bytes and scales 8 + n/16 bytes")
+    if g.dtype != np.float32:
+        raise OracleError("current scaling needs fp32 gradients (they receive w')")
+    _check_state(n, g, m, v, ve, "fp32", sfmt)
+    if gidx is not None:
+        gidx = np.ascontiguousarray(gidx, dtype=np.int64)
+        assert gidx.size == n
+    _check_copy(copy, n)
+    rc = lib().oracle_step_nv_current(_ptr(q), _ptr(scales), _ptr(copy), _ptr(g), SFMT[sfmt],
+                                      _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
+                                      int(index_base), *_hp_args(hp))
+    if rc != 0:
+        raise OracleError(f"oracle_step_nv_current returned {rc}")
+
+
+def encode_nv_current(x: np.ndarray):
+    """NVFP4 encoding for the current-scaling layout: the encode_nv payloads,
+    and the scale array with a zero word between the tensor scale and the
+    block codes."""
+    q, s = encode_nv(x)
+    return q, np.concatenate([s[:4], np.zeros(4, np.uint8), s[4:]])
+
+
+def nv_current_values(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Stored weights of the current-scaling layout."""
+    return nv_values(q, np.concatenate([scales[:4], scales[8:]]))
 
 
 def encode_nv(x: np.ndarray):

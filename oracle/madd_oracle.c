@@ -84,7 +84,8 @@
  *     define the format): the OCP MX block format MXFP4 -- 32-element blocks
  *     of E2M1 values with one E8M0 power-of-two scale; rule at oracle_step_mx
  *     -- and NVFP4 (16-element blocks, E4M3 block scales, one fp32 scale per
- *     tensor held fixed by the step); rule at oracle_step_nv.
+ *     tensor), either held fixed by the step (oracle_step_nv) or derived
+ *     anew from the updated tensor every step (oracle_step_nv_current).
  *
  * Pin status (tests/test_oracle_*.py; a mutation test checks the pins catch
  * planted mistakes): the real-number update is pinned by closed forms, the
@@ -832,6 +833,65 @@ int oracle_step_nv(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const 
       const uint32_t pc = nv_payload(wn[k], c, dnew, h.rounding, r16);
       mx_put(q, i, pc);
       if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, pc) * dnew);
+    }
+    codes[b] = (uint8_t)c;
+  }
+  return ORACLE_OK;
+}
+
+/* NVFP4 with current scaling: the per-tensor scale is derived anew from the
+ * updated tensor at every step.  Section 4.2's prototype keeps its master
+ * weights in NVFP4 by dequantizing, taking the FP32 step and quantizing the
+ * result again (the quantize/dequantize simulation its overhead discussion
+ * and Appendix G describe); a quantizer that sees the whole updated tensor
+ * derives its per-tensor scale from that tensor's amax.  This step does the
+ * same: every w' of the tensor first (moments updated as in every step),
+ * then s_t' = fp32(amax / 2688) over the finite |w'| (1 when none is
+ * nonzero), then every block by the NVFP4 rule above with s_t'.
+ * Layout: q n/2 bytes; scales 8 + n/16 bytes: s_t (fp32), then a word that
+ * receives the bits of the tensor's largest finite |w'|, then the block
+ * codes.  The gradient array (fp32 only) receives w'. */
+int oracle_step_nv_current(uint8_t *q, uint8_t *scales, uint16_t *copy, float *g, int sfmt,
+                           void *m, void *v, void *ve, int64_t n, const int64_t *gidx,
+                           int64_t index_base, double lr_add, double lr_mul, double beta1,
+                           double beta2, double eps, double tau, double r_max, double eps0,
+                           double g_max, double d_mult_max, double w_max, int bias_correction,
+                           int rounding, uint64_t seed, int64_t step) {
+  init_formats();
+  ohp h;
+  if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
+              w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
+    return ORACLE_EINVAL;
+  if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
+  if (n < 0 || n % NV_BLOCK != 0) return ORACLE_EINVAL;
+  oscal s;
+  make_scalars(&h, &s);
+  const float st = nv_get_st(scales);
+  uint8_t *codes = scales + 8;
+  /* the FP32 step on every dequantized weight; w' replaces the gradient */
+  float amax = 0.0f;
+  for (int64_t i = 0; i < n; ++i) {
+    const float wv = (float)decode(OF_E2M1, mx_get(q, i)) * nv_den(codes[i / NV_BLOCK], st);
+    const float wn = step_stored(wv, g[i], sfmt, m, v, ve, i, &s, &h,
+                                 gidx ? gidx[i] : index_base + i);
+    g[i] = wn;
+    if (isfinite(wn) && fabsf(wn) > amax) amax = fabsf(wn);
+  }
+  /* the new per-tensor scale, then every block with it */
+  const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;
+  memcpy(scales, &stn, 4);
+  memcpy(scales + 4, &amax, 4);
+  for (int64_t b = 0; b < n / NV_BLOCK; ++b) {
+    const float *wn = g + b * NV_BLOCK;
+    const uint32_t c = nv_block_code(wn, stn);
+    const float den = nv_den(c, stn);
+    for (int k = 0; k < NV_BLOCK; ++k) {
+      const int64_t i = b * NV_BLOCK + k;
+      const int64_t idx = gidx ? gidx[i] : index_base + i;
+      const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
+      const uint32_t pc = nv_payload(wn[k], c, den, h.rounding, r16);
+      mx_put(q, i, pc);
+      if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, pc) * den);
     }
     codes[b] = (uint8_t)c;
   }

@@ -85,6 +85,12 @@ MUTANTS = {
     "NV tensor scale from 448 alone": ("amax > 0.0f ? amax / 2688.0f : 1.0f", "amax > 0.0f ? amax / 448.0f : 1.0f"),
     "NV NaN block payload": ("if (code == 0x7Fu || den == 0.0f) return 0u;",
                              "if (code == 0x7Fu || den == 0.0f) return 7u;"),
+    "NV current scale over non-finite values too": (
+        "    if (isfinite(wn) && fabsf(wn) > amax) amax = fabsf(wn);",
+        "    if (fabsf(wn) > amax) amax = fabsf(wn);"),
+    "NV current scaling keeps the old scale": (
+        "  const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;\n  memcpy(scales, &stn, 4);",
+        "  const float stn = st;\n  memcpy(scales, &stn, 4);"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }
