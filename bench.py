@@ -33,9 +33,10 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2607_10611_amd", "csrc", "madd.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "madd_step_kernel_llama7b_bf16_sr_pmc.md")
 
-WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5, "nvfp4": 0.5}
+WBYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "mxfp4": 0.5, "nvfp4": 0.5, "nvfp4_current": 0.5}
 # linear-layer storage of the low-precision master settings
-LOW_MASTER = {"fp8-master": "e4m3", "fp4-master": "mxfp4", "nvfp4-master": "nvfp4"}
+LOW_MASTER = {"fp8-master": "e4m3", "fp4-master": "mxfp4", "nvfp4-master": "nvfp4",
+              "nvfp4cs-master": "nvfp4_current"}
 SBYTES = {"fp32": 4, "bf16": 2, "bf16-sr": 2}
 
 
@@ -49,12 +50,16 @@ def algorithmic_bytes(sizes, plan, sfmt: str) -> float:
     written once, plus per tensor its bf16 compute copy (written) and its
     block scales (read and written: FP16 per 128 elements for FP8, E8M0 per
     32 for MXFP4, E4M3 per 16 for NVFP4, whose fp32 tensor scale is read).
+    NVFP4 with current scaling also writes w' over the fp32 gradient in its
+    first pass and reads it back in its second (8 B per element), and per
+    tensor reads and writes its scale and amax words (16 B).
     `plan` holds (weight format, block-scaled, compute copy) per tensor."""
     total = 0.0
     for n, (wf, blk, cp) in zip(sizes, plan):
         total += n * bytes_per_param(wf, sfmt) + (n * 2 if cp else 0)
         if blk:
-            total += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4}.get(wf, (n // 128) * 4)
+            total += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4,
+                      "nvfp4_current": (n // 16) * 2 + 16 + 8 * n}.get(wf, (n // 128) * 4)
     return total
 
 WORKLOAD_NAMES = {
@@ -165,8 +170,10 @@ def main():
                     help="list: the configuration's weight format for every tensor; fp8-master: "
                          "linear layers block-scaled E4M3 with bf16 compute copies, embeddings, "
                          "norms and head bf16 (the paper's FP8-master setting); fp4-master: the "
-                         "same with MXFP4 linear layers (its 4-bit setting); nvfp4-master: the "
-                         "same with NVFP4 linear layers")
+                         "same with MXFP4 linear layers; nvfp4-master: the same with NVFP4 "
+                         "linear layers (the paper's 4-bit setting) whose tensor scale the step "
+                         "keeps; nvfp4cs-master: NVFP4 with the tensor scale derived anew every "
+                         "step (current scaling)")
     ap.add_argument("--cpu-sample", type=int, default=1 << 24)
     ap.add_argument("--cpu-steps", type=int, default=None,
                     help="gradient sets generated for the oracle's sample (default 10; 4 with "
@@ -257,12 +264,14 @@ def main():
     else:
         wb16, w16 = flat_subset(torch.int16, lambda p: p[0] == "bf16")
         wb8, w8 = flat_subset(torch.uint8, lambda p: p[0] != "bf16",
-                              per_elem=2 if low in ("mxfp4", "nvfp4") else 1)
+                              per_elem=2 if low in ("mxfp4", "nvfp4", "nvfp4_current") else 1)
         ws = [a if a is not None else b for a, b in zip(w16, w8)]
         if low == "mxfp4":
             sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=32)
         elif low == "nvfp4":  # fp32 tensor scale, then one E4M3 code per 16
             sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=16, head=4)
+        elif low == "nvfp4_current":  # tensor scale, amax word, E4M3 codes
+            sbuf, scales = flat_subset(torch.uint8, lambda p: p[1], per_elem=16, head=8)
         else:
             sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
         cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
@@ -374,8 +383,13 @@ def main():
                  f"{W.CONFIGS[cfg]['rounding'].upper()}>")
     else:
         low = LOW_MASTER[args.weights]
-        kname = (f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches per "
-                 "step; timed together)")
+        if low == "nvfp4_current":
+            kname = ("nvcs_clear_kernel + nvcs_pass1_kernel + nvcs_pass2_kernel (NVFP4 with "
+                     "current scaling) + madd_step_kernel<bf16> (four launches per step; timed "
+                     "together)")
+        else:
+            kname = (f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches per "
+                     "step; timed together)")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": int(round(alg_bytes)),

@@ -82,14 +82,26 @@ typedef enum madd_status {
  *              (unsigned; 0x7F = NaN); one fp32 scale st per tensor.  The
  *              weight is E2M1 value * fp32(E4M3(c) * st).  The scale array
  *              holds st in its first 4 bytes (fp32, 4-byte aligned), then
- *              the n/16 block codes.  Always block-scaled. */
+ *              the n/16 block codes.  Always block-scaled.  A step keeps st.
+ *   NVFP4_CURRENT : NVFP4 whose per-tensor scale is derived anew from the
+ *              updated tensor at every step (current scaling), as the
+ *              dequantize / FP32 step / quantize round trip of the paper's
+ *              NVFP4 prototype (Section 4.2, Appendix G) does.  Payloads and
+ *              block codes as NVFP4; the scale array holds st (4 bytes), one
+ *              4-byte word that a step sets to the bits of the tensor's
+ *              largest finite |w'|, then the n/16 block codes (8 + n/16
+ *              bytes, 4-byte aligned).  The step needs fp32 gradients and
+ *              overwrites them with the updated weights w' (fp32): the
+ *              second of its two passes re-encodes them once the new st is
+ *              known. */
 typedef enum madd_wfmt {
   MADD_W_BF16 = 0,
   MADD_W_FP8_E4M3 = 1,
   MADD_W_FP8_E5M2 = 2,
   MADD_W_FP32 = 3,
   MADD_W_MXFP4 = 4,
-  MADD_W_NVFP4 = 5
+  MADD_W_NVFP4 = 5,
+  MADD_W_NVFP4_CURRENT = 6
 } madd_wfmt;
 
 /* Gradient formats (decoded exactly to FP32). */
@@ -177,7 +189,9 @@ int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, voi
  *     value); payloads are fp32(x / D_b), D_b = fp32(E4M3(code) * st),
  *     rounded onto E2M1 saturating at +-6, and 0 when D_b is 0 or the block
  *     is NaN.  Four launches on `stream` (the amax reduction uses the first
- *     scale word). */
+ *     scale word).
+ *   - NVFP4_CURRENT (required): 8 + n/16 bytes, 4-byte aligned: st and the
+ *     block codes as for NVFP4, with the second word set to 0. */
 int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales, int64_t n,
                             void* stream);
 
@@ -196,12 +210,20 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
  *           weight is payload * scale (fp32 product); after the update each
  *           block's scale is recomputed from the new weights by the same rule
  *           and the payloads re-encoded with hp->rounding.  NVFP4's
- *           per-tensor scale st is read and kept (re-encode to refresh it).
+ *           per-tensor scale st is read and kept (re-encode to refresh it);
+ *           NVFP4_CURRENT derives st' = fp32(amax / 2688) over the finite
+ *           |w'| of the whole tensor (1 when none is nonzero), stores it and
+ *           the amax bits, and re-encodes every block with st'.  It takes
+ *           three launches: clear the amax word, pass 1 (the FP32 step:
+ *           moments stored, w' written over g, amax folded in with atomics),
+ *           pass 2 (block codes and payloads from w' and st').  gfmt must be
+ *           FP32 (else MADD_EINVAL) and g is overwritten.
  *           Requires n % 128 == 0 (FP8), n % 32 == 0 (MXFP4) or n % 16 == 0
- *           (NVFP4) and 16-byte-aligned w, g, m, v, ve and copy, and a
- *           4-byte-aligned NVFP4 scale array (else MADD_EINVAL /
+ *           (NVFP4, NVFP4_CURRENT) and 16-byte-aligned w, g, m, v, ve and
+ *           copy, and a 4-byte-aligned NVFP4 scale array (else MADD_EINVAL /
  *           MADD_EALIGN).
- * g       : device gradient of format gfmt (read only).
+ * g       : device gradient of format gfmt (read only, except for
+ *           NVFP4_CURRENT, which overwrites it with w').
  * m, v, ve: device moments (first, second, multiplicative second) stored as
  *           sfmt (a madd_sfmt), updated in place.
  * index_base: global index of element 0 (keys the stochastic-rounding draw);
@@ -219,14 +241,14 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
  * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
  * block-scaled) or a host array whose entry i is NULL or tensor i's scale
- * array (never NULL for an MXFP4 or NVFP4 tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
+ * array (never NULL for an MXFP4, NVFP4 or NVFP4_CURRENT tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
  * or tensor i's bf16 compute-copy array (as in madd_step).  Tensors of
  * different weight formats may be mixed -- e.g. block-scaled FP8 linear
  * layers (or MXFP4 / NVFP4 ones) with BF16 embeddings, norms and head, the paper's
  * FP8-master (4-bit-master) setting (Section 4.2).  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
  * The first call with a given list (same pointers and sizes) uploads a device
- * descriptor table (80 bytes per tensor) with a synchronous copy and caches it
+ * descriptor table (88 bytes per tensor) with a synchronous copy and caches it
  * (up to 32 lists per process; evicting one drains the device first).  Later
  * calls with the same list enqueue only the kernels. */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
@@ -246,7 +268,8 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
  * No optimizer state.  w: device weight codes of format wfmt, in place;
  * g: device gradient of format gfmt; index_base, rounding and seed as in
  * madd_step; hp's beta1, beta2, eps, g_max and bias_correction are validated
- * but unused.  Unscaled formats only (MXFP4, NVFP4: MADD_EINVAL).  Errors as in
+ * but unused.  Unscaled formats only (MXFP4, NVFP4, NVFP4_CURRENT:
+ * MADD_EINVAL).  Errors as in
  * madd_step. */
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
                         int64_t index_base, const madd_hparams* hp, void* stream);

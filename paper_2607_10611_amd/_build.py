@@ -43,7 +43,7 @@ def hipcc() -> str:
     return "hipcc"
 
 
-NPARTS = 9  # csrc/madd.hip is compiled as parts 0..8 (-DMADD_PART=k), in parallel
+NPARTS = 10  # csrc/madd.hip is compiled as parts 0..9 (-DMADD_PART=k), in parallel
 
 
 def _run(cmd, verbose):

@@ -17,11 +17,11 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmadd.so")
 
 # enum values of madd.h
-W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32, W_MXFP4, W_NVFP4 = 0, 1, 2, 3, 4, 5
+W_BF16, W_FP8_E4M3, W_FP8_E5M2, W_FP32, W_MXFP4, W_NVFP4, W_NVFP4_CURRENT = 0, 1, 2, 3, 4, 5, 6
 G_FP32, G_BF16 = 0, 1
 ROUND_RNE, ROUND_SR = 0, 1
 WFMT = {"bf16": W_BF16, "e4m3": W_FP8_E4M3, "e5m2": W_FP8_E5M2, "fp32": W_FP32,
-        "mxfp4": W_MXFP4, "nvfp4": W_NVFP4}
+        "mxfp4": W_MXFP4, "nvfp4": W_NVFP4, "nvfp4_current": W_NVFP4_CURRENT}
 MX_BLOCK = 32  # elements per MXFP4 block (one E8M0 scale byte)
 NV_BLOCK = 16  # elements per NVFP4 block (one E4M3 scale byte after the fp32 tensor scale)
 _WFMT_NAME = {v: k for k, v in WFMT.items()}
@@ -140,18 +140,22 @@ def _stream(stream) -> int | None:
 
 # Bytes per element of each storage, for the size checks below (the C ABI
 # receives bare pointers and cannot check them).
-CODE_BYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "fp32": 4, "mxfp4": 0.5, "nvfp4": 0.5}
+CODE_BYTES = {"bf16": 2, "e4m3": 1, "e5m2": 1, "fp32": 4, "mxfp4": 0.5, "nvfp4": 0.5,
+              "nvfp4_current": 0.5}
 GRAD_BYTES = {"fp32": 4, "bf16": 2}
 STATE_BYTES = {"fp32": 4, "bf16": 2, "bf16_sr": 2}
 
 
 def scale_bytes(wfmt: str, n: int) -> int:
     """Bytes of the block-scale array of n elements: FP16 per 128 (block FP8),
-    E8M0 per 32 (MXFP4), the fp32 tensor scale then E4M3 per 16 (NVFP4)."""
+    E8M0 per 32 (MXFP4), the fp32 tensor scale then E4M3 per 16 (NVFP4), and
+    for NVFP4 with current scaling the amax word between them."""
     if wfmt == "mxfp4":
         return n // MX_BLOCK
     if wfmt == "nvfp4":
         return 4 + n // NV_BLOCK
+    if wfmt == "nvfp4_current":
+        return 8 + n // NV_BLOCK
     return (n // 128) * 2
 
 
@@ -230,7 +234,9 @@ def madd_step(w, wfmt: str, g, m, v, ve, hp, gfmt: str = "fp32", scales=None, in
     """One step on one tensor.  ``w`` holds the weight codes (uint16 / uint8 /
     int32 storage for bf16 / fp8 / fp32; n/2 packed bytes for mxfp4, whose
     ``scales`` are n/32 uint8 E8M0 codes, and for nvfp4, whose ``scales`` are
-    4 + n/16 bytes, 4-byte aligned: the fp32 tensor scale, then E4M3 codes);
+    4 + n/16 bytes, 4-byte aligned: the fp32 tensor scale, then E4M3 codes;
+    for nvfp4_current 8 + n/16 bytes, the tensor scale derived anew each step
+    and ``g`` (fp32) overwritten with the updated weights);
     the moments' storage follows their dtype unless ``sfmt`` is given; ``copy`` (16-bit tensor) receives the
     bf16 compute copy of the new weights."""
     h = _hp(hp)

@@ -50,8 +50,9 @@
 // The library is built from this one source compiled as several parts
 // (-DMADD_PART=k, in parallel): part 0 holds the host code, the ABI and the
 // set-up kernels; parts 1-8 each instantiate the step kernels of one weight
-// format (block-scaled FP8 separately from unscaled).  Without MADD_PART
-// everything is compiled as one unit.
+// format (block-scaled FP8 separately from unscaled), part 9 those of NVFP4
+// with current scaling.  Without MADD_PART everything is compiled as one
+// unit.
 #ifndef MADD_PART
 #define MADD_PART -1
 #endif
@@ -958,6 +959,145 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// NVFP4 with current scaling: the per-tensor scale derived anew from the
+// updated tensor at every step.  Three launches: clear each tensor's amax
+// word; pass 1 takes the FP32 step (moments stored, w' written over the fp32
+// gradient, the largest finite |w'| folded into the amax word); pass 2
+// derives s_t' = fp32(amax / 2688) and re-encodes every block of w' with it.
+// Scale array: s_t (fp32), the amax word, then one E4M3 code per 16 elements.
+// ---------------------------------------------------------------------------
+
+#if MADD_IN_PART(9)
+__global__ __launch_bounds__(kThreads) void nvcs_clear_kernel(const TensorDesc* __restrict__ table,
+                                                              int ntab, TensorDesc single,
+                                                              Scalars) {
+  const int i = (int)(blockIdx.x * kThreads + threadIdx.x);
+  if (i >= (ntab == 0 ? 1 : ntab)) return;
+  void* scales = ntab == 0 ? single.scales : table[i].scales;
+  ((uint32_t*)scales)[1] = 0u;
+}
+
+// |x| as raw bits when x is finite, else 0.
+__device__ __forceinline__ uint32_t finite_abs_bits(float x) {
+  const uint32_t b = __float_as_uint(x) & 0x7FFFFFFFu;
+  return b < 0x7F800000u ? b : 0u;
+}
+
+template <int SF, bool CLAMP>
+__device__ __forceinline__ uint32_t nvcs_step_quad(const TensorDesc& d, int64_t e, float st,
+                                                   const MDraws& md, const Scalars& s) {
+  Quad<WF_NVFP4> q;
+  load_quad<WF_NVFP4, GF_FP32, SF>(q, d, e);
+  const float den = scale_value<WF_NVFP4>(
+      load_scale<WF_NVFP4>((const uint8_t*)d.scales + 4, (int64_t)((uint64_t)e / kNvBlock)), st);
+  f4 wn;
+  uint32_t amax = 0u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    float m = q.m[k], v = q.v[k], ve = q.ve[k];
+    wn[k] = step_elem<CLAMP>(decode<WF_NVFP4>(q.w.code(k)) * den, q.g[k], m, v, ve, s);
+    q.m[k] = m;
+    q.v[k] = v;
+    q.ve[k] = ve;
+    const uint32_t ab = finite_abs_bits(wn[k]);
+    amax = ab > amax ? ab : amax;
+  }
+  st4s<SF>(d.m, e, q.m, md.m);
+  st4s<SF>(d.v, e, q.v, md.v);
+  st4s<SF>(d.ve, e, q.ve, md.ve);
+  stg<f4>((float*)d.g + e, wn);  // w' replaces the gradient
+  return amax;
+}
+
+template <int SF, bool CLAMP>
+__global__ __launch_bounds__(kThreads) void nvcs_pass1_kernel(const TensorDesc* __restrict__ table,
+                                                              int ntab, TensorDesc single,
+                                                              Scalars s) {
+  const int64_t chunk = blockIdx.x;
+  const TensorDesc d = find_tensor(table, ntab, single, chunk);
+  const float st = *(const float*)d.scales;
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
+  MDraws mA, mB;
+  if (d.vec_ok) {  // uniform: index base a multiple of 8
+    mdraws_aligned<SF>((uint64_t)(d.gbase + c0) + 8u * (threadIdx.x >> 1), s, mA, mB);
+  } else {
+    mdraws_any<SF>((uint64_t)(d.gbase + eA), s, mA);
+    mdraws_any<SF>((uint64_t)(d.gbase + eB), s, mB);
+  }
+  uint32_t amax = 0u;
+  if (eA < cend) amax = nvcs_step_quad<SF, CLAMP>(d, eA, st, mA, s);  // n % 16 == 0: whole quads
+  if (eB < cend) {
+    const uint32_t b = nvcs_step_quad<SF, CLAMP>(d, eB, st, mB, s);
+    amax = b > amax ? b : amax;
+  }
+  // the wave's largest finite |w'|, folded into the tensor's amax word; a
+  // wave whose value is not above the word's current one skips the atomic
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)amax, off);
+    amax = o > amax ? o : amax;
+  }
+  if ((threadIdx.x & 63u) == 0u && amax != 0u) {
+    uint32_t* word = (uint32_t*)d.scales + 1;
+    if (amax > __atomic_load_n(word, __ATOMIC_RELAXED)) atomicMax(word, amax);
+  }
+}
+
+template <bool SR, bool COPY>
+__device__ __forceinline__ void nvcs_requant(const TensorDesc& d, int64_t e, f4 w,
+                                             uint32_t amax, const uint32_t (&r)[4], float st) {
+  Quad<WF_NVFP4> q;
+  q.w.raw = 0u;
+  const float wn[4] = {w.x, w.y, w.z, w.w};
+  float cv[4];
+  const uint32_t sc = requant_quad<WF_NVFP4, SR>(q, wn, amax, r, cv, st);
+  q.w.store(d.w, e);
+  if (COPY && d.copy) store_copy_values(cv, d.copy, e);
+  if ((threadIdx.x & 3u) == 0u)
+    store_scale<WF_NVFP4>((uint8_t*)d.scales + 4, (int64_t)((uint64_t)e / kNvBlock), sc);
+}
+
+template <bool SR, bool COPY>
+__global__ __launch_bounds__(kThreads) void nvcs_pass2_kernel(const TensorDesc* __restrict__ table,
+                                                              int ntab, TensorDesc single,
+                                                              Scalars s) {
+  const int64_t chunk = blockIdx.x;
+  const TensorDesc d = find_tensor(table, ntab, single, chunk);
+  const float amax_t = __uint_as_float(((const uint32_t*)d.scales)[1]);
+  const float st = amax_t > 0.0f ? amax_t / 2688.0f : 1.0f;
+  if (chunk == d.chunk0 && threadIdx.x == 0) *(float*)d.scales = st;  // pass 2 reads only the amax word
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
+  const bool actA = eA < cend, actB = eB < cend;  // whole lane groups of a block agree
+  f4 wa = f4{0.0f, 0.0f, 0.0f, 0.0f}, wb = wa;
+  if (actA) wa = ldg<f4>((const float*)d.g + eA);
+  if (actB) wb = ldg<f4>((const float*)d.g + eB);
+  uint32_t rA[4], rB[4];
+  if (d.vec_ok) {
+    draws_aligned<SR>((uint64_t)(d.gbase + c0) + 8u * (threadIdx.x >> 1), s, rA, rB);
+  } else {
+    draws_any<SR>((uint64_t)(d.gbase + eA), s, rA);
+    draws_any<SR>((uint64_t)(d.gbase + eB), s, rB);
+  }
+  uint32_t amaxA = 0u, amaxB = 0u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t a = __float_as_uint(wa[k]) & 0x7FFFFFFFu, b = __float_as_uint(wb[k]) & 0x7FFFFFFFu;
+    amaxA = a > amaxA ? a : amaxA;
+    amaxB = b > amaxB ? b : amaxB;
+  }
+  amaxA = block_amax<4>(amaxA);
+  amaxB = block_amax<4>(amaxB);
+  if (actA) nvcs_requant<SR, COPY>(d, eA, wa, amaxA, rA, st);
+  if (actB) nvcs_requant<SR, COPY>(d, eB, wb, amaxB, rB, st);
+}
+#endif  // MADD_IN_PART(9)
+
 // ---------------------------------------------------------------------------
 // The moment-free rules of Appendix B's diagnostic
 // ---------------------------------------------------------------------------
@@ -1092,13 +1232,16 @@ __global__ void nv_scale_kernel(uint32_t* slot) {
   }
 }
 
-__global__ void nv_clear_kernel(uint32_t* slot) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) *slot = 0u;
+// Zero the first `words` 32-bit words of a scale array.
+__global__ void nv_clear_kernel(uint32_t* slot, int words) {
+  if (blockIdx.x == 0 && (int)threadIdx.x < words) slot[threadIdx.x] = 0u;
 }
 
+// `scales` holds st in its first word; the block codes start `head` bytes in
+// (4 for NVFP4, 8 for NVFP4 with current scaling).
 __global__ __launch_bounds__(kThreads) void encode_nv_kernel(const float* __restrict__ x,
                                                              uint8_t* q, uint8_t* scales,
-                                                             int64_t nblocks) {
+                                                             int64_t nblocks, int head) {
   const float st = *(const float*)scales;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x; b < nblocks; b += stride) {
@@ -1116,7 +1259,7 @@ __global__ __launch_bounds__(kThreads) void encode_nv_kernel(const float* __rest
       const uint32_t hi = zero ? 0u : enc_e2m1(xb[k + 1] / den, false, 0u);
       q[b * (kNvBlock / 2) + k / 2] = (uint8_t)(lo | (hi << 4));
     }
-    scales[4 + b] = (uint8_t)sc;
+    scales[head + b] = (uint8_t)sc;
   }
 }
 #endif  // MADD_IN_PART(0)
@@ -1174,6 +1317,12 @@ step_fn pick_part6(int gf, int sf, bool sr, bool clamp, bool copy);  // fp32 pas
 step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy);  // mxfp4 (block-scaled)
 step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy);  // nvfp4 (block-scaled)
 
+// NVFP4 with current scaling: its three kernels.
+struct NvcsKernels {
+  step_fn clear, pass1, pass2;
+};
+NvcsKernels pick_part9(int sf, bool sr, bool clamp, bool copy);
+
 #if MADD_IN_PART(1)
 step_fn pick_part1(int gf, int sf, bool sr, bool clamp, bool copy) {
   return pick_gf<WF_BF16, false>(gf, sf, sr, clamp, copy);
@@ -1215,6 +1364,25 @@ step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy) {
 }
 #endif
 
+#if MADD_IN_PART(9)
+template <int SF>
+NvcsKernels pick_nvcs(bool sr, bool clamp, bool copy) {
+  NvcsKernels k;
+  k.clear = nvcs_clear_kernel;
+  k.pass1 = clamp ? nvcs_pass1_kernel<SF, true> : nvcs_pass1_kernel<SF, false>;
+  k.pass2 = sr ? (copy ? nvcs_pass2_kernel<true, true> : nvcs_pass2_kernel<true, false>)
+               : (copy ? nvcs_pass2_kernel<false, true> : nvcs_pass2_kernel<false, false>);
+  return k;
+}
+NvcsKernels pick_part9(int sf, bool sr, bool clamp, bool copy) {
+  switch (sf) {
+    case SF_FP32: return pick_nvcs<SF_FP32>(sr, clamp, copy);
+    case SF_BF16: return pick_nvcs<SF_BF16>(sr, clamp, copy);
+    default: return pick_nvcs<SF_BF16_SR>(sr, clamp, copy);
+  }
+}
+#endif
+
 #if MADD_IN_PART(0)
 // The step kernel for (weight, gradient and moment formats, rounding,
 // optional clamps present, compute copies present, block-scaled); nullptr for
@@ -1236,8 +1404,9 @@ bool needs_clamp(const madd_hparams& hp) {
   return !(std::isinf(hp.g_max) && hp.g_max > 0) || !(std::isinf(hp.w_max) && hp.w_max > 0);
 }
 
-bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_NVFP4; }
-bool fp4_fmt(int32_t f) { return f == MADD_W_MXFP4 || f == MADD_W_NVFP4; }
+bool valid_wfmt(int32_t f) { return f >= MADD_W_BF16 && f <= MADD_W_NVFP4_CURRENT; }
+bool nv_fmt(int32_t f) { return f == MADD_W_NVFP4 || f == MADD_W_NVFP4_CURRENT; }
+bool fp4_fmt(int32_t f) { return f == MADD_W_MXFP4 || nv_fmt(f); }
 bool valid_gfmt(int32_t f) { return f == MADD_G_FP32 || f == MADD_G_BF16; }
 bool valid_sfmt(int32_t f) { return f == MADD_S_FP32 || f == MADD_S_BF16 || f == MADD_S_BF16_SR; }
 bool al16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -1349,6 +1518,22 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
+// NVFP4 with current scaling: clear the amax words (one thread per tensor),
+// then the two passes over the same chunks.
+int32_t launch_nvcs(const NvcsKernels& k, const TensorDesc* table, int ntab,
+                    const TensorDesc& single, int64_t nchunks, const Scalars& s,
+                    hipStream_t stream) {
+  if (nchunks <= 0) return MADD_OK;
+  if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+  const unsigned clear_grid = (unsigned)(((ntab == 0 ? 1 : ntab) + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(k.clear, dim3(clear_grid), dim3(kThreads), 0, stream, table, ntab, single, s);
+  hipLaunchKernelGGL(k.pass1, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
+                     single, s);
+  hipLaunchKernelGGL(k.pass2, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
+                     single, s);
+  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+}
+
 TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void* m, void* v,
                      void* ve, int64_t n, int64_t gbase) {
   TensorDesc d;
@@ -1372,7 +1557,7 @@ bool block_scaled_fmt(int32_t f) {
   return f == MADD_W_FP8_E4M3 || f == MADD_W_FP8_E5M2 || fp4_fmt(f);
 }
 int64_t block_len_of(int32_t f) {
-  return f == MADD_W_MXFP4 ? kMxBlock : (f == MADD_W_NVFP4 ? kNvBlock : kBlock);
+  return f == MADD_W_MXFP4 ? kMxBlock : (nv_fmt(f) ? kNvBlock : kBlock);
 }
 
 int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
@@ -1385,7 +1570,7 @@ int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const 
   if (scales) {
     if (!block_scaled_fmt(wfmt)) return MADD_EINVAL;
     if (n % block_len_of(wfmt) != 0) return MADD_EINVAL;
-    if (wfmt == MADD_W_NVFP4 && ((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
+    if (nv_fmt(wfmt) && ((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
     if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy))))
       return MADD_EALIGN;
   }
@@ -1441,19 +1626,20 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
   if (!x || !w) return MADD_EINVAL;
   if (fp4_fmt(wfmt) && !scales) return MADD_EINVAL;
   hipStream_t st = (hipStream_t)stream;
-  if (wfmt == MADD_W_NVFP4) {
+  if (nv_fmt(wfmt)) {
     if (n % kNvBlock != 0) return MADD_EINVAL;
     if (((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
     uint32_t* slot = (uint32_t*)scales;
+    const int head = wfmt == MADD_W_NVFP4 ? 4 : 8;  // current scaling: st, amax word
     const int64_t nb = n / kNvBlock;
     const int64_t want_x = (n + kThreads - 1) / kThreads, want_b = (nb + kThreads - 1) / kThreads;
     const unsigned grid_x = (unsigned)(want_x < 4096 ? want_x : 4096);
     const unsigned grid_b = (unsigned)(want_b < 65536 ? want_b : 65536);
-    hipLaunchKernelGGL(nv_clear_kernel, dim3(1), dim3(64), 0, st, slot);
+    hipLaunchKernelGGL(nv_clear_kernel, dim3(1), dim3(64), 0, st, slot, head / 4);
     hipLaunchKernelGGL(nv_amax_kernel, dim3(grid_x), dim3(kThreads), 0, st, x, n, slot);
     hipLaunchKernelGGL(nv_scale_kernel, dim3(1), dim3(64), 0, st, slot);
     hipLaunchKernelGGL(encode_nv_kernel, dim3(grid_b), dim3(kThreads), 0, st, x, (uint8_t*)w,
-                       (uint8_t*)scales, nb);
+                       (uint8_t*)scales, nb, head);
     return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
   }
   if (wfmt == MADD_W_MXFP4) {
@@ -1502,6 +1688,13 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
   if (n == 0) return MADD_OK;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
   const Scalars s = make_scalars(*hp);
+  if (wfmt == MADD_W_NVFP4_CURRENT) {
+    if (gfmt != MADD_G_FP32) return MADD_EINVAL;  // w' is written over the fp32 gradient
+    const NvcsKernels k = pick_part9(sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
+                                     copy != nullptr);
+    const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
+    return launch_nvcs(k, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
+  }
   step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                            copy != nullptr, scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
@@ -1549,6 +1742,8 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
   int64_t total = 0;
   for (int32_t i = 0; i < ntensors; ++i) {
     if (!valid_wfmt(wfmt[i])) return MADD_EINVAL;
+    if (wfmt[i] == MADD_W_NVFP4_CURRENT && gfmt != MADD_G_FP32 && numel[i] > 0)
+      return MADD_EINVAL;  // w' is written over the fp32 gradient
     rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, copy ? copy[i] : nullptr, g[i],
                       m[i], v[i], ve[i], numel[i]);
     if (rc != MADD_OK) return rc;
@@ -1560,13 +1755,14 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
   // One launch per (format, scaled) group; global indices follow list order.
   // All tables are prepared before the first launch.
   struct Group {
-    step_fn fn;
+    step_fn fn;  // null for NVFP4 with current scaling, which launches `nvcs`
+    NvcsKernels nvcs;
     TensorDesc* table;
     int ntab;
     int64_t nchunks;
   };
   std::vector<Group> groups;
-  for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4; ++wf) {
+  for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4_CURRENT; ++wf) {
     for (int blk = 0; blk <= 1; ++blk) {
       std::vector<TensorDesc> descs;
       int64_t gbase = index_base, nch = 0;
@@ -1585,18 +1781,26 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
       if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
       bool any_copy = false;
       for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
-      step_fn fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
-      if (!fn) return MADD_EUNSUPPORTED;
+      step_fn fn = nullptr;
+      NvcsKernels nvcs = {nullptr, nullptr, nullptr};
+      if (wf == MADD_W_NVFP4_CURRENT) {
+        nvcs = pick_part9(sfmt, sr, needs_clamp(*hp), any_copy);
+      } else {
+        fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
+        if (!fn) return MADD_EUNSUPPORTED;
+      }
       TensorDesc* table = nullptr;
       rc = get_table(descs, &table);
       if (rc != MADD_OK) return rc;
-      groups.push_back(Group{fn, table, (int)descs.size(), nch});
+      groups.push_back(Group{fn, nvcs, table, (int)descs.size(), nch});
     }
   }
   TensorDesc none;
   memset(&none, 0, sizeof(none));
   for (const Group& gr : groups) {
-    rc = launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, (hipStream_t)stream);
+    rc = gr.fn ? launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, (hipStream_t)stream)
+               : launch_nvcs(gr.nvcs, gr.table, gr.ntab, none, gr.nchunks, s,
+                             (hipStream_t)stream);
     if (rc != MADD_OK) return rc;
   }
   return MADD_OK;

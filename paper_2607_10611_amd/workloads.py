@@ -213,7 +213,8 @@ def low_precision_master_plan(cfg: str, linear_fmt: str = "e4m3"):
     attention and MLP linear weights block-scaled in ``linear_fmt`` -- "e4m3"
     (FP16 scale per 128 elements; the FP8/FP8 setting), "nvfp4" (E2M1 with an
     E4M3 scale per 16 elements and an fp32 scale per tensor; the 4-bit
-    setting) or "mxfp4" (E2M1 with an E8M0 scale per 32 elements) -- each
+    setting; "nvfp4_current" derives that scale anew every step) or "mxfp4"
+    (E2M1 with an E8M0 scale per 32 elements) -- each
     with a bf16 compute copy; embeddings, norms and the LM head in bf16.  Returns (weight format, block-scaled, compute copy) per
     tensor."""
     plan = []

@@ -9,9 +9,10 @@ import oracle
 from paper_2607_10611_amd import binding as B
 
 CODE_NP = {"bf16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "fp32": np.uint32,
-           "mxfp4": np.uint8, "nvfp4": np.uint8}  # 4-bit: packed bytes, two elements each
+           "mxfp4": np.uint8, "nvfp4": np.uint8,  # 4-bit: packed bytes, two elements each
+           "nvfp4_current": np.uint8}
 CODE_T = {"bf16": torch.int16, "e4m3": torch.uint8, "e5m2": torch.uint8, "fp32": torch.int32,
-          "mxfp4": torch.uint8, "nvfp4": torch.uint8}
+          "mxfp4": torch.uint8, "nvfp4": torch.uint8, "nvfp4_current": torch.uint8}
 SIGNED_NP = {np.uint16: np.int16, np.uint32: np.int32, np.uint8: np.uint8}
 
 
@@ -94,7 +95,13 @@ class HostState:
 
 
 def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
-    if wfmt == "mxfp4":
+    """One oracle step on hs.  For nvfp4_current, g (fp32) receives w' as the
+    device's gradient buffer does."""
+    if wfmt == "nvfp4_current":
+        assert gfmt == "fp32"
+        oracle.step_nv_current(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, index_base=index_base,
+                               gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
+    elif wfmt == "mxfp4":
         oracle.step_mx(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
                        index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
     elif wfmt == "nvfp4":

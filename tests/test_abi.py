@@ -133,7 +133,7 @@ def test_mxfp4_argument_rules():
     assert lib.madd_plain_step(FAKE, B.W_MXFP4, FAKE, 0, 64, 0, ref, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, None, 64, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, FAKE, 40, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, 6, FAKE, 64, None) == -1   # no such format
+    assert lib.madd_encode_weights(FAKE, FAKE, 7, FAKE, 64, None) == -1   # no such format
 
 
 def test_nvfp4_argument_rules():
@@ -150,6 +150,27 @@ def test_nvfp4_argument_rules():
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, None, 64, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE, 40, None) == -1
     assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE + 2, 64, None) == -2
+
+
+def test_nvfp4_current_argument_rules():
+    lib = B.lib()
+    ref, _h = _hp()
+    W = B.W_NVFP4_CURRENT
+    call = lambda w, sc, n, gfmt=0, cp=None: lib.madd_step(w, W, sc, cp, FAKE, gfmt, FAKE, FAKE,  # noqa: E731
+                                                           FAKE, 0, n, 0, ref, None)
+    assert call(FAKE, None, 64) == -1            # scales required
+    assert call(FAKE, FAKE, 40) == -1            # n % 16
+    assert call(FAKE, FAKE + 2, 64) == -2        # scale array not 4-byte aligned
+    assert call(FAKE, FAKE, 64, gfmt=1) == -1    # w' is written over the gradient: fp32 only
+    assert lib.madd_plain_step(FAKE, W, FAKE, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, W, None, 64, None) == -1
+    assert lib.madd_encode_weights(FAKE, FAKE, W, FAKE, 40, None) == -1
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
+    n = (ctypes.c_int64 * 1)(64)
+    wf = (ctypes.c_int32 * 1)(W)
+    assert lib.madd_multi_tensor_step(1, arr(FAKE), wf, arr(FAKE), None, arr(FAKE), 1, arr(FAKE),
+                                      arr(FAKE), arr(FAKE), 0, n, 0, ref, None) == -1
 
 
 def test_multi_tensor_rejects_bad_arguments():
@@ -227,3 +248,4 @@ def test_scale_bytes():
     assert B.scale_bytes("e4m3", 1024) == 16
     assert B.scale_bytes("mxfp4", 1024) == 32
     assert B.scale_bytes("nvfp4", 1024) == 68
+    assert B.scale_bytes("nvfp4_current", 1024) == 72

@@ -1,0 +1,296 @@
+"""Parity of the HIP step on NVFP4 storage with current scaling (the
+per-tensor scale derived anew from the updated tensor every step: clear,
+pass 1, pass 2) with the CPU oracle, through the C ABI.  Bar: payload bytes,
+the whole scale array (tensor scale, amax word, block codes), the gradient
+buffer (which receives w') and bf16 compute copies bit-exact; fp32 moments
+within 2 ulp; bf16 moment codes bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_10611_amd import binding as B
+from paper_2607_10611_amd import workloads as W
+from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
+                             free_device_bytes, gpu_step, oracle_step, to_dev, to_host, ulp_dist)
+from test_oracle_nv import e4m3_code
+
+pytestmark = pytest.mark.gpu
+FMT = "nvfp4_current"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def hp(**kw):
+    h = dict(W.DEFAULT_HPARAMS)
+    h.update(kw)
+    return h
+
+
+def weights(rng, n):
+    x = rng.normal(0, 0.02, n).astype(np.float32)
+    x[rng.random(n) < 0.02] = 0.0
+    big = rng.random(n) < 0.01
+    x[big] = rng.normal(0, 3.0, big.sum())
+    if n >= 4 * 16:
+        x[:16] = 0.0
+        x[16:32] = rng.normal(0, 1e-7, 16)
+    return x
+
+
+def grad(rng, n):
+    g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-6, -1, n)).astype(np.float32)
+    g[rng.random(n) < 0.05] = 0.0
+    return g
+
+
+def encode_both(x):
+    q_ref, s_ref = oracle.encode_nv_current(x)
+    q = torch.empty(x.size // 2, dtype=torch.uint8, device="cuda")
+    s = torch.full((8 + x.size // 16,), 0xAB, dtype=torch.uint8, device="cuda")
+    B.madd_encode_weights(torch.from_numpy(x).cuda(), q, FMT, scales=s)
+    torch.cuda.synchronize()
+    assert (to_host(s) == s_ref).all(), "scale array differs"
+    assert (to_host(q) == q_ref).all(), "payload bytes differ"
+    return q_ref, s_ref
+
+
+def same_bits(a, b):
+    """fp32 arrays equal bit for bit, a NaN matching any NaN (the host's and
+    the device's default NaNs differ in sign)."""
+    nan = np.isnan(a) & np.isnan(b)
+    return bool(((a.view(np.uint32) == b.view(np.uint32)) | nan).all())
+
+
+def check(tag, ds, hs, g_dev, g_host):
+    w_g, m_g, v_g, ve_g = ds.host()
+    assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+    bad = np.nonzero(to_host(ds.scales) != hs.scales)[0]
+    assert bad.size == 0, f"{tag}: scale bytes differ at {bad[:5]}"
+    assert same_bits(to_host(g_dev), g_host), f"{tag}: w' in the gradient buffer differs"
+    assert_copy_equal(tag, ds, hs)
+
+
+def run_cs(n, steps, seed, hpkw, index_base=0, sfmt="fp32", copy=False, gradf=grad):
+    rng = np.random.default_rng(seed)
+    q, s = encode_both(weights(rng, n))
+    ds = DevState(FMT, q, n, s, sfmt=sfmt, copy=copy)
+    hs = HostState(q, n, s, sfmt=sfmt, copy=copy)
+    for t in range(1, steps + 1):
+        g = gradf(rng, n)
+        g_dev = to_dev(g)
+        h = hp(step=t, **hpkw)
+        gpu_step(ds, g_dev, h, index_base=index_base)
+        oracle_step(FMT, hs, g, h, index_base=index_base)
+        torch.cuda.synchronize()
+        check(f"{FMT} n={n} t={t}", ds, hs, g_dev, g)
+    return ds, hs
+
+
+def test_encode_matches_oracle():
+    rng = np.random.default_rng(41)
+    x = weights(rng, 16 * 3000)
+    x[100] = np.nan
+    encode_both(x)
+
+
+@pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
+                                                 ("sr", "bf16", True), ("sr", "bf16_sr", True)])
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+    run_cs(5 * 8192 + 7 * 16, 4, 42, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
+
+
+@pytest.mark.parametrize("n", [16, 48, 1008, 2048 + 16, 4096 + 1024 + 80])
+def test_small_and_partial_tiles(n):
+    run_cs(n, 3, 43 + n, dict(rounding="sr", seed=71, lr_add=1e-2), copy=True)
+
+
+def test_unaligned_index_base_and_clamps():
+    run_cs(3 * 8192 + 16, 3, 44, dict(rounding="sr", seed=5), index_base=3, copy=True)
+    run_cs(2 * 8192, 3, 45, dict(rounding="sr", g_max=2.0, w_max=0.5, d_mult_max=0.25,
+                                 eps0=0.1, bias_correction=0, lr_mul=0.05))
+
+
+def test_scale_follows_growing_weights():
+    """Weights pushed outward for many steps: the tensor scale follows them
+    and the block codes stay below saturation (GPU and oracle alike)."""
+    def push(rng, n):
+        return np.full(n, -1e-2, np.float32)
+    ds, hs = run_cs(4 * 2048, 12, 46, dict(rounding="rne", lr_add=0.0, lr_mul=0.5),
+                    gradf=push)
+    st = np.frombuffer(to_host(ds.scales)[:4].tobytes(), np.float32)[0]
+    assert st > 1e-3 and (to_host(ds.scales)[8:] == 0x7E).mean() < 0.2
+
+
+def test_nonfinite_gradients():
+    def g_bad(rng, n):
+        g = grad(rng, n)
+        g[[40, 1000, 5000]] = [np.nan, np.inf, -np.inf]
+        return g
+    ds, hs = run_cs(4 * 2048, 2, 47, dict(rounding="sr"), gradf=g_bad, copy=True)
+    sc = to_host(ds.scales)
+    assert (sc[8 + np.array([40 // 16, 1000 // 16, 5000 // 16])] == 0x7F).all()
+
+
+def test_multi_tensor_list_mixed_with_other_formats():
+    rng = np.random.default_rng(48)
+    layout = [(FMT, 4096 + 48), ("bf16", 1000), ("nvfp4", 2048), (FMT, 16), ("mxfp4", 1024),
+              (FMT, 0), (FMT, 20480)]
+    devs, singles, hosts = [], [], []
+    for wfmt, n in layout:
+        if wfmt == FMT:
+            q, s = encode_both(weights(rng, n)) if n else (np.zeros(0, np.uint8),
+                                                          np.zeros(8, np.uint8))
+            args = (q, n, s)
+        elif wfmt == "nvfp4":
+            args = (*oracle.encode_nv(weights(rng, n)),)
+            args = (args[0], n, args[1])
+        elif wfmt == "mxfp4":
+            q, s = oracle.encode_mx(weights(rng, n))
+            args = (q, n, s)
+        else:
+            args = (oracle.encode_array("bf16", weights(rng, n)), n, None)
+        cp = wfmt != "bf16"
+        devs.append(DevState(wfmt, *args, copy=cp))
+        singles.append(DevState(wfmt, *args, copy=cp))
+        hosts.append(HostState(*args, copy=cp))
+    base = 777
+    for t in range(1, 4):
+        gs = [grad(rng, n) for _, n in layout]
+        gl = [to_dev(g) for g in gs]
+        g1 = [to_dev(g) for g in gs]
+        h = hp(step=t, rounding="sr", seed=99)
+        tl = B.TensorList([d.w for d in devs], [d.wfmt for d in devs], gl, [d.m for d in devs],
+                          [d.v for d in devs], [d.ve for d in devs],
+                          scales=[d.scales for d in devs], copies=[d.copy for d in devs])
+        B.madd_multi_tensor_step(tl, h, index_base=base)
+        off = base
+        for (wfmt, n), d1, hs, g, gd in zip(layout, singles, hosts, gs, g1):
+            if n:
+                gpu_step(d1, gd, h, index_base=off)
+                oracle_step(wfmt, hs, g, h, index_base=off)
+            off += n
+        torch.cuda.synchronize()
+        for (wfmt, n), d, d1, hs, g, gd, gd1 in zip(layout, devs, singles, hosts, gs, gl, g1):
+            if not n:
+                continue
+            tag = f"multi {wfmt} n={n} t={t}"
+            w_g, m_g, v_g, ve_g = d.host()
+            assert_state_equal(tag, w_g, hs.w, m_g, hs.m, v_g, hs.v, ve_g, hs.ve)
+            assert_copy_equal(tag, d, hs)
+            for a, b in zip(d.host(), d1.host()):
+                assert a.tobytes() == b.tobytes(), tag
+            if hs.scales is not None:
+                assert (to_host(d.scales) == hs.scales).all(), tag
+            if wfmt == FMT:
+                assert same_bits(to_host(gd), g) and same_bits(to_host(gd1), g), tag
+
+
+def test_nvfp4_current_master_llama7b_sampled():
+    """The 4-bit master setting with current scaling on the full 7B list, one
+    multi-tensor call per step.  Sampled 16-element blocks follow the oracle's
+    FP32 step exactly (moments and w' in the gradient buffer); each tensor's
+    new scale is checked against the largest finite |w'| of the whole
+    gradient buffer, and the sampled blocks' codes and payloads against the
+    NVFP4 rule applied to w' with that scale (block codes by torch's E4M3
+    conversion, payloads by the oracle's E2M1 encoder with the step's keyed
+    draws)."""
+    cfg = "c5"
+    specs = W.specs(cfg)
+    plan = W.low_precision_master_plan(cfg, FMT)
+    free = free_device_bytes()
+    need = sum(s.numel for s in specs) * 19 + (1 << 30)
+    assert free > need, f"needs {need / 2**30:.0f} GiB of device memory"
+    rng = np.random.default_rng(49)
+    offsets = np.cumsum([0] + [s.numel for s in specs])
+    dev = dict(w=[], sc=[], cp=[], m=[], v=[], ve=[], g=[])
+    samples = []
+    for i, (s, (wfmt, blk, cp)) in enumerate(zip(specs, plan)):
+        x = W.init_fp32_device(cfg, i)
+        if blk:
+            w = torch.empty(s.numel // 2, dtype=torch.uint8, device="cuda")
+            sc = torch.empty(8 + s.numel // 16, dtype=torch.uint8, device="cuda")
+        else:
+            w = torch.empty(s.numel, dtype=torch.int16, device="cuda")
+            sc = None
+        B.madd_encode_weights(x, w, wfmt, scales=sc)
+        del x
+        nb = s.numel // 16
+        bidx = np.unique(np.concatenate([np.arange(2), np.arange(nb - 2, nb),
+                                         rng.choice(nb, size=min(nb, 32), replace=False)]))
+        idx = (bidx[:, None] * 16 + np.arange(16)[None, :]).ravel()
+        dev["w"].append(w)
+        dev["sc"].append(sc)
+        dev["cp"].append(torch.zeros(s.numel, dtype=torch.int16, device="cuda") if cp else None)
+        for k in ("m", "v", "ve"):
+            dev[k].append(torch.zeros(s.numel, device="cuda"))
+        dev["g"].append(torch.empty(s.numel, device="cuda"))
+        samples.append((idx, torch.from_numpy(idx).cuda(), bidx))
+    tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
+                      scales=dev["sc"], copies=dev["cp"])
+    hm = [None] * len(specs)
+    for t in (1, 2):
+        # the sampled old weights and gradients, before the step
+        before = []
+        for i, (idx, idx_t, bidx) in enumerate(samples):
+            W.grad_fp32_device_(cfg, i, t, dev["g"][i])
+            if plan[i][1]:
+                sc = to_host(dev["sc"][i])
+                st_old = np.frombuffer(sc[:4].tobytes(), np.float32)[0]
+                q = to_host(dev["w"][i][torch.from_numpy(
+                    (bidx[:, None] * 8 + np.arange(8)[None, :]).ravel()).cuda()])
+                codes = sc[8 + bidx]
+                den = (torch.from_numpy(codes.copy()).view(torch.float8_e4m3fn).float().numpy()
+                       * st_old).astype(np.float32)
+                w_old = (oracle.decode_array("e2m1", oracle.unpack_e2m1(q)).astype(np.float32)
+                         .reshape(-1, 16) * den[:, None]).astype(np.float32).ravel()
+            else:
+                w_old = oracle.decode_array("bf16", to_host(dev["w"][i][idx_t], np.uint16)
+                                            ).astype(np.float32)
+            before.append((w_old, to_host(dev["g"][i][idx_t])))
+        h = W.hparams(cfg, step=t)
+        B.madd_multi_tensor_step(tl, h)
+        torch.cuda.synchronize()
+        for i, (idx, idx_t, bidx) in enumerate(samples):
+            wfmt, blk, cp = plan[i]
+            w_old, g = before[i]
+            tag = f"{FMT}-master {specs[i].name} t={t}"
+            if hm[i] is None:
+                hm[i] = [np.zeros(idx.size, np.float32) for _ in range(3)]
+            codes32 = w_old.view(np.uint32).copy()
+            oracle.step("fp32", codes32, g.copy(), *hm[i], h, gidx=idx + offsets[i])
+            wn = codes32.view(np.float32)
+            for k, name in enumerate(("m", "v", "ve")):
+                assert ulp_dist(to_host(dev[name][i][idx_t]), hm[i][k]).max() <= 2, (tag, name)
+            if not blk:
+                continue
+            g_dev = dev["g"][i]
+            assert same_bits(to_host(g_dev[idx_t]), wn), tag                  # w'
+            a = g_dev.abs()
+            amax = float(torch.where(torch.isfinite(a), a, torch.zeros_like(a)).max())
+            sc = to_host(dev["sc"][i])
+            assert np.frombuffer(sc[4:8].tobytes(), np.float32)[0] == np.float32(amax), tag
+            st = np.float32(np.float32(amax) / np.float32(2688.0))
+            assert np.frombuffer(sc[:4].tobytes(), np.float32)[0] == st, tag
+            six_st = np.float32(np.float32(6.0) * st)
+            wb = wn.reshape(-1, 16)
+            want_codes = np.array([e4m3_code(np.float32(np.float32(np.abs(b).max()) / six_st))
+                                   for b in wb], np.uint8)
+            assert (sc[8 + bidx] == want_codes).all(), tag
+            den = (torch.from_numpy(want_codes.copy()).view(torch.float8_e4m3fn).float().numpy()
+                   * st).astype(np.float32)
+            y = (wb / den[:, None]).astype(np.float32).ravel()
+            r16 = np.array([oracle.draw16(h["seed"], t, 0, int(j)) for j in idx + offsets[i]])
+            dead = np.repeat((want_codes == 0x7F) | (den == 0), 16)  # payloads 0
+            want = np.array([0 if z else oracle.encode("e2m1", float(v), h["rounding"], int(r))
+                             for v, r, z in zip(y, r16, dead)], np.uint8)
+            q = to_host(dev["w"][i][torch.from_numpy(
+                (bidx[:, None] * 8 + np.arange(8)[None, :]).ravel()).cuda()])
+            assert (oracle.unpack_e2m1(q) == want).all(), tag
