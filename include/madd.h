@@ -239,7 +239,9 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
 /* One M+Adam step on a list of tensors in as few launches as the formats
  * allow (one per distinct (format, scaled) pair).
  * ntensors >= 0; w, wfmt, g, m, v, ve, numel: host arrays of ntensors
- * entries; gfmt and sfmt apply to every tensor; scales: NULL (no tensor
+ * entries; gfmt and sfmt apply to every tensor (gfmt must be FP32 when the
+ * list holds a nonempty NVFP4_CURRENT tensor, whose gradient the step
+ * overwrites with w'); scales: NULL (no tensor
  * block-scaled) or a host array whose entry i is NULL or tensor i's scale
  * array (never NULL for an MXFP4, NVFP4 or NVFP4_CURRENT tensor); copy: NULL (no compute copies) or a host array whose entry i is NULL
  * or tensor i's bf16 compute-copy array (as in madd_step).  Tensors of
