@@ -19,7 +19,9 @@
  *   combine
  *       w <- clamp_{w_max}(w + w u_m + u_a), rounded into the storage format
  *       (the FP32-step / low-precision-storage round trip of Appendix B),
- *       to nearest-even or stochastically.
+ *       to nearest-even or stochastically.  Storage: bf16, FP8 (unscaled or
+ *       with FP16 scales per 128 elements), MXFP4 and NVFP4 (Section 4.2's
+ *       4-bit master weights), FP32 for testing.
  *
  * The step is computed in FP32 in one fixed operation order; results are
  * bit-reproducible across launches, shardings and tensor groupings.
@@ -32,7 +34,8 @@
  *     Work is enqueued asynchronously on it; no call synchronizes the host
  *     except madd_multi_tensor_step the first time it sees a given tensor
  *     list (it uploads a descriptor table; see that function).
- *   - Updates are in place on w, m, v, ve and scales; g is read-only.
+ *   - Updates are in place on w, m, v, ve and scales; g is read-only
+ *     (except for NVFP4_CURRENT tensors, whose step writes w' over g).
  *     Buffers must not alias each other.  Concurrent calls that touch the
  *     same buffers race.
  *   - Arguments are validated before any device work; on any status other
