@@ -37,7 +37,8 @@ unpinned against the paper (the paper does not fix them): the exact fp32
 operation order, the block-scaled FP8 block length and scale rule, the 4-bit
 formats (``step_mx`` and ``step_nv``: pinned to the OCP MX specification and
 to NVFP4's published definition instead; when NVFP4's tensor scale is
-refreshed is a choice, at encoding) and the stochastic-rounding rule with its
+refreshed is a choice, and both are built: at encoding only (``step_nv``) or
+at every step (``step_nv_current``)) and the stochastic-rounding rule with its
 generator.
 """
 from __future__ import annotations

@@ -95,7 +95,8 @@
  * the exact fp32 operation order (a contract shared with the kernel), the
  * block-scaled FP8 block length and scale rule, the 4-bit formats (MXFP4
  * and NVFP4, pinned to their published definitions instead; when NVFP4's
- * tensor scale is refreshed is a choice: at encoding), and the
+ * tensor scale is refreshed is a choice, and both are built: at encoding
+ * only, or at every step), and the
  * stochastic-rounding rule and its generator (pinned to their own
  * definitions).
  *
