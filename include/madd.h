@@ -256,7 +256,8 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
  * descriptor table (88 bytes per tensor) with a synchronous copy and caches it
  * (up to 32 lists per process; evicting one drains the device first).  Later
  * calls with the same list enqueue only the kernels, so such a call can be
- * captured into a HIP graph (no call records a memset). */
+ * captured into a HIP graph (no call records a memset); the hyper-parameters,
+ * step counter included, are kernel arguments fixed at capture. */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
                                void* const* scales, uint16_t* const* copy,
                                const void* const* g, int32_t gfmt,
