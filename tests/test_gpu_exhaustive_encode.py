@@ -53,3 +53,56 @@ def test_rne_encode_on_every_fp32_input(fmt):
         bad += nb
         del x, nan, xr, ref
     assert bad == 0, f"{fmt}: {bad} of 2^32 inputs encode differently, e.g. {examples}"
+
+
+MIDS = (0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0)   # between E2M1 magnitudes 0 .5 1 1.5 2 3 4 6
+
+
+def e2m1_rne_reference(x):
+    """E2M1 code of |x| <= 6 rounded to nearest, ties to the even code."""
+    a = x.abs()
+    s = torch.zeros_like(a, dtype=torch.int64)
+    tie = torch.zeros_like(a, dtype=torch.bool)
+    for m in MIDS:
+        s += (a > m).to(torch.int64)
+        tie |= a == m
+    k = s + (tie & (s % 2 == 1)).to(torch.int64)
+    return k | ((x.view(torch.int32) < 0).to(torch.int64) << 3)
+
+
+def test_e2m1_rne_encode_on_every_fp32_value_up_to_six():
+    """NVFP4 encoding with the tensor scale forced to 1 (one block holding
+    2688 = 6 x 448) and every other block led by 6.0 (block code E4M3(1.0),
+    factor 1): the other 15 elements of each block take the E2M1 code of
+    their own value, for every fp32 bit pattern with |x| <= 6."""
+    per = 15 << 23                                      # test values per call
+    ranges = [(0, 0x40C00000 + 1), (0x80000000, 0xC0C00000 + 1)]
+    bad, examples = 0, []
+    for lo, hi in ranges:
+        for start in range(lo, hi, per):
+            cnt = min(per, hi - start)
+            nb = -(-cnt // 15)
+            vals = torch.arange(start, start + nb * 15, dtype=torch.int64, device="cuda")
+            vals = torch.where(vals < hi, vals, torch.full_like(vals, start))  # pad with a tested value
+            x = torch.empty(nb + 1, 16, device="cuda")
+            x[:nb, 0] = 6.0
+            x[:nb, 1:] = vals.to(torch.int32).view(torch.float32).view(nb, 15)
+            x[nb] = 0.0
+            x[nb, 0] = 2688.0
+            x = x.view(-1)
+            q = torch.empty(x.numel() // 2, dtype=torch.uint8, device="cuda")
+            s = torch.empty(4 + x.numel() // 16, dtype=torch.uint8, device="cuda")
+            B.madd_encode_weights(x, q, "nvfp4", scales=s)
+            assert float(s[:4].view(torch.float32)[0]) == 1.0
+            codes = torch.stack([q & 0xF, q >> 4], dim=1).view(-1).to(torch.int64).view(nb + 1, 16)
+            got = codes[:nb, 1:].reshape(-1)
+            ref = e2m1_rne_reference(x.view(nb + 1, 16)[:nb, 1:].reshape(-1))
+            mism = got != ref
+            n_bad = int(mism.sum())
+            if n_bad and not examples:
+                i = torch.nonzero(mism)[:5, 0]
+                xs = x.view(nb + 1, 16)[:nb, 1:].reshape(-1)
+                examples = [(float(xs[j]), int(got[j]), int(ref[j])) for j in i]
+            bad += n_bad
+            del vals, x, q, s, codes, got, ref, mism
+    assert bad == 0, f"{bad} values encode differently, e.g. {examples}"
