@@ -36,10 +36,15 @@
  *     list (it uploads a descriptor table; see that function).
  *   - Updates are in place on w, m, v, ve and scales; g is read-only
  *     (except for NVFP4_CURRENT tensors, whose step writes w' over g).
- *     Buffers must not alias each other.  Concurrent calls that touch the
- *     same buffers race.
+ *     Buffers must not alias each other: each call checks that the byte
+ *     ranges of the arrays it takes for one tensor (weights, scales, compute
+ *     copy, gradient, moments; input and output of an encoding) are
+ *     pairwise disjoint, from their formats and sizes, and returns
+ *     MADD_EINVAL otherwise.  Overlap between different tensors of a list is
+ *     not checked.  Concurrent calls that touch the same buffers race.
  *   - Arguments are validated before any device work; on any status other
- *     than MADD_OK no buffer has been touched.
+ *     than MADD_OK no buffer has been touched.  A tensor holds at most 2^60
+ *     elements (larger sizes are MADD_EINVAL).
  *   - Every status is a madd_status value; madd_status_string() names it.
  */
 #ifndef MADD_H

@@ -1560,9 +1560,46 @@ int64_t block_len_of(int32_t f) {
   return f == MADD_W_MXFP4 ? kMxBlock : (nv_fmt(f) ? kNvBlock : kBlock);
 }
 
+constexpr int64_t kMaxN = (int64_t)1 << 60;  // elements per tensor (byte sizes fit 64 bits)
+
+// Bytes one tensor of n elements occupies in each of its buffers.
+uint64_t code_bytes(int32_t wfmt, int64_t n) {
+  switch (wfmt) {
+    case MADD_W_BF16: return 2ull * (uint64_t)n;
+    case MADD_W_FP32: return 4ull * (uint64_t)n;
+    case MADD_W_FP8_E4M3:
+    case MADD_W_FP8_E5M2: return (uint64_t)n;
+    default: return ((uint64_t)n + 1u) / 2u;  // two E2M1 codes per byte
+  }
+}
+uint64_t scale_bytes(int32_t wfmt, int64_t n) {
+  const uint64_t u = (uint64_t)n;
+  switch (wfmt) {
+    case MADD_W_MXFP4: return u / kMxBlock;
+    case MADD_W_NVFP4: return 4u + u / kNvBlock;
+    case MADD_W_NVFP4_CURRENT: return 8u + u / kNvBlock;
+    default: return 2u * (u / kBlock);
+  }
+}
+
+// The buffers of one tensor must be pairwise disjoint byte ranges (the
+// kernels read and write them in place, in no fixed order between arrays).
+bool disjoint(const void* const* p, const uint64_t* bytes, int k) {
+  for (int i = 0; i < k; ++i) {
+    if (!p[i] || bytes[i] == 0) continue;
+    const uintptr_t a0 = (uintptr_t)p[i], a1 = a0 + bytes[i];
+    for (int j = i + 1; j < k; ++j) {
+      if (!p[j] || bytes[j] == 0) continue;
+      const uintptr_t b0 = (uintptr_t)p[j], b1 = b0 + bytes[j];
+      if (a0 < b1 && b0 < a1) return false;
+    }
+  }
+  return true;
+}
+
 int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
-                     void* m, void* v, void* ve, int64_t n) {
-  if (n < 0) return MADD_EINVAL;
+                     int32_t gfmt, void* m, void* v, void* ve, int32_t sfmt, int64_t n) {
+  if (n < 0 || n > kMaxN) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!w || !g || !m || !v || !ve) return MADD_EINVAL;
   if (!valid_wfmt(wfmt)) return MADD_EINVAL;
@@ -1574,6 +1611,12 @@ int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const 
     if (!(al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy))))
       return MADD_EALIGN;
   }
+  const uint64_t u = (uint64_t)n;
+  const uint64_t sb = (sfmt == MADD_S_FP32 ? 4u : 2u) * u;
+  const void* const p[7] = {w, scales, copy, g, m, v, ve};
+  const uint64_t b[7] = {code_bytes(wfmt, n), scales ? scale_bytes(wfmt, n) : 0u, 2u * u,
+                         (gfmt == MADD_G_FP32 ? 4u : 2u) * u, sb, sb, sb};
+  if (!disjoint(p, b, 7)) return MADD_EINVAL;
   return MADD_OK;
 }
 
@@ -1602,9 +1645,15 @@ const char* madd_status_string(int32_t status) {
 }
 
 int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, void* stream) {
-  if (n < 0 || !valid_sfmt(sfmt)) return MADD_EINVAL;
+  if (n < 0 || n > kMaxN || !valid_sfmt(sfmt)) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!m || !v || !ve) return MADD_EINVAL;
+  {
+    const uint64_t sb = (sfmt == MADD_S_FP32 ? 4u : 2u) * (uint64_t)n;
+    const void* const p[3] = {m, v, ve};
+    const uint64_t b[3] = {sb, sb, sb};
+    if (!disjoint(p, b, 3)) return MADD_EINVAL;
+  }
   const int64_t want = (n + kThreads - 1) / kThreads;
   const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
   hipStream_t st = (hipStream_t)stream;
@@ -1621,14 +1670,27 @@ int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, voi
 
 int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales, int64_t n,
                             void* stream) {
-  if (n < 0 || !valid_wfmt(wfmt)) return MADD_EINVAL;
+  if (n < 0 || n > kMaxN || !valid_wfmt(wfmt)) return MADD_EINVAL;
   if (n == 0) return MADD_OK;
   if (!x || !w) return MADD_EINVAL;
   if (fp4_fmt(wfmt) && !scales) return MADD_EINVAL;
-  hipStream_t st = (hipStream_t)stream;
   if (nv_fmt(wfmt)) {
     if (n % kNvBlock != 0) return MADD_EINVAL;
     if (((uintptr_t)scales & 3u) != 0) return MADD_EALIGN;
+  } else if (wfmt == MADD_W_MXFP4) {
+    if (n % kMxBlock != 0) return MADD_EINVAL;
+  } else if (scales) {
+    if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
+    if (n % kBlock != 0) return MADD_EINVAL;
+  }
+  {
+    const void* const p[3] = {x, w, scales};
+    const uint64_t b[3] = {4u * (uint64_t)n, code_bytes(wfmt, n),
+                           scales ? scale_bytes(wfmt, n) : 0u};
+    if (!disjoint(p, b, 3)) return MADD_EINVAL;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  if (nv_fmt(wfmt)) {
     uint32_t* slot = (uint32_t*)scales;
     const int head = wfmt == MADD_W_NVFP4 ? 4 : 8;  // current scaling: st, amax word
     const int64_t nb = n / kNvBlock;
@@ -1643,7 +1705,6 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
     return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
   }
   if (wfmt == MADD_W_MXFP4) {
-    if (n % kMxBlock != 0) return MADD_EINVAL;
     const int64_t nb = n / kMxBlock;
     const int64_t want = (nb + kThreads - 1) / kThreads;
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
@@ -1652,8 +1713,6 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
     return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
   }
   if (scales) {
-    if (wfmt != MADD_W_FP8_E4M3 && wfmt != MADD_W_FP8_E5M2) return MADD_EINVAL;
-    if (n % kBlock != 0) return MADD_EINVAL;
     const int64_t nb = n / kBlock;
     const int64_t want = (nb + kThreads - 1) / kThreads;
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
@@ -1683,7 +1742,7 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
   if (rc != MADD_OK) return rc;
   if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
     return MADD_EINVAL;
-  rc = check_tensor(w, wfmt, scales, copy, g, m, v, ve, n);
+  rc = check_tensor(w, wfmt, scales, copy, g, gfmt, m, v, ve, sfmt, n);
   if (rc != MADD_OK) return rc;
   if (n == 0) return MADD_OK;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
@@ -1706,11 +1765,17 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
                         int64_t index_base, const madd_hparams* hp, void* stream) {
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
-  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0 || n < 0) return MADD_EINVAL;
+  if (!valid_wfmt(wfmt) || !valid_gfmt(gfmt) || index_base < 0 || n < 0 || n > kMaxN)
+    return MADD_EINVAL;
   if (fp4_fmt(wfmt)) return MADD_EINVAL;  // block-scaled: no scale argument here
   if (n == 0) return MADD_OK;
   if (!w || !g) return MADD_EINVAL;
   if (n > INT64_MAX - index_base) return MADD_EINVAL;
+  {
+    const void* const p[2] = {w, g};
+    const uint64_t b[2] = {code_bytes(wfmt, n), (gfmt == MADD_G_FP32 ? 4u : 2u) * (uint64_t)n};
+    if (!disjoint(p, b, 2)) return MADD_EINVAL;
+  }
   const Scalars s = make_scalars(*hp);
   const bool sr = hp->rounding == MADD_ROUND_SR;
   plain_fn fn = nullptr;
@@ -1745,7 +1810,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
     if (wfmt[i] == MADD_W_NVFP4_CURRENT && gfmt != MADD_G_FP32 && numel[i] > 0)
       return MADD_EINVAL;  // w' is written over the fp32 gradient
     rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, copy ? copy[i] : nullptr, g[i],
-                      m[i], v[i], ve[i], numel[i]);
+                      gfmt, m[i], v[i], ve[i], sfmt, numel[i]);
     if (rc != MADD_OK) return rc;
     if (numel[i] > INT64_MAX - index_base - total) return MADD_EINVAL;
     total += numel[i];

@@ -9,6 +9,20 @@ import pytest
 
 from paper_2607_10611_amd import binding as B
 
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:  # noqa: BLE001
+        return False
+
+
+# Tests that pass made-up device addresses: each call must fail validation
+# before any launch; where a GPU is visible they are skipped, so that a
+# broken check could never launch a kernel on those addresses.
+fake_addresses = pytest.mark.skipif(_gpu_visible(), reason="made-up device addresses; CPU only")
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "madd.h")
 
@@ -37,6 +51,7 @@ def test_every_header_symbol_is_exported_by_its_library():
             assert re.search(rf"\bT {name}\b", nm), (h, name)
 
 
+@fake_addresses
 def test_ceiling_probe_rejects_bad_arguments():
     from paper_2607_10611_amd import _build
     L = ctypes.CDLL(_build.PROBE_LIB)
@@ -85,8 +100,12 @@ def _hp(**kw):
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
+# distinct fake device addresses (1 MiB apart) for the buffers of one call,
+# so that a rejection comes from the rule under test, not from overlap
+W_, S_, C_, G_, M_, V_, E_ = (0x100000 * (k + 1) for k in range(7))
 
 
+@fake_addresses
 @pytest.mark.parametrize("kw", [dict(beta1=1.0), dict(beta2=-0.5), dict(eps=-1.0), dict(tau=0.0),
                                 dict(r_max=0.0), dict(r_max=1.0), dict(eps0=0.75),
                                 dict(g_max=0.0), dict(d_mult_max=-1.0), dict(w_max=0.0),
@@ -95,84 +114,121 @@ FAKE = 0x10000  # never dereferenced: every call below fails validation first
 def test_step_rejects_bad_hparams(kw):
     lib = B.lib()
     ref, _h = _hp(**kw)
-    rc = lib.madd_step(FAKE, B.W_BF16, None, None, FAKE, B.G_FP32, FAKE, FAKE, FAKE, 0, 1024, 0,
-                       ref, None)
+    rc = lib.madd_step(W_, B.W_BF16, None, None, G_, B.G_FP32, M_, V_, E_, 0, 1024, 0, ref, None)
     assert rc == -1
 
 
+@fake_addresses
 def test_step_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
     call = lambda w, wf, sc, *a: lib.madd_step(w, wf, sc, None, *a, ref, None)  # noqa: E731
-    assert lib.madd_step(FAKE, 0, None, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0, None,
-                         None) == -1
-    assert lib.madd_step(FAKE, 1, FAKE, FAKE + 8, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0, ref,
+    assert lib.madd_step(W_, 0, None, None, G_, 0, M_, V_, E_, 0, 8, 0, None, None) == -1
+    assert lib.madd_step(W_, 1, S_, C_ + 8, G_, 0, M_, V_, E_, 0, 128, 0, ref,
                          None) == -2  # block-scaled with an unaligned copy
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, -1, 0) == -1          # n < 0
-    assert call(None, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # null w
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, None, FAKE, 0, 8, 0) == -1           # null v
-    assert call(FAKE, 9, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad wfmt
-    assert call(FAKE, 0, None, FAKE, 5, FAKE, FAKE, FAKE, 0, 8, 0) == -1           # bad gfmt
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 3, 8, 0) == -1           # bad sfmt
-    assert call(FAKE, 0, None, FAKE, 0, FAKE, FAKE, FAKE, 0, 8, -3) == -1          # base < 0
-    assert call(FAKE, 0, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0) == -1         # scales + bf16
-    assert call(FAKE, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 100, 0) == -1         # n % 128
-    assert call(FAKE + 4, 1, FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 128, 0) == -2     # unaligned
-    assert call(None, 0, None, None, 0, None, None, None, 0, 0, 0) == 0            # empty: no-op
+    assert call(W_, 0, None, G_, 0, M_, V_, E_, 0, -1, 0) == -1          # n < 0
+    assert call(None, 0, None, G_, 0, M_, V_, E_, 0, 8, 0) == -1         # null w
+    assert call(W_, 0, None, G_, 0, M_, None, E_, 0, 8, 0) == -1         # null v
+    assert call(W_, 9, None, G_, 0, M_, V_, E_, 0, 8, 0) == -1           # bad wfmt
+    assert call(W_, 0, None, G_, 5, M_, V_, E_, 0, 8, 0) == -1           # bad gfmt
+    assert call(W_, 0, None, G_, 0, M_, V_, E_, 3, 8, 0) == -1           # bad sfmt
+    assert call(W_, 0, None, G_, 0, M_, V_, E_, 0, 8, -3) == -1          # base < 0
+    assert call(W_, 0, S_, G_, 0, M_, V_, E_, 0, 128, 0) == -1           # scales + bf16
+    assert call(W_, 1, S_, G_, 0, M_, V_, E_, 0, 100, 0) == -1           # n % 128
+    assert call(W_ + 4, 1, S_, G_, 0, M_, V_, E_, 0, 128, 0) == -2       # unaligned
+    assert call(None, 0, None, None, 0, None, None, None, 0, 0, 0) == 0  # empty: no-op
+    assert call(W_, 0, None, G_, 0, M_, V_, E_, 0, 2 ** 62, 2 ** 62) == -1  # index overflow
 
 
+@fake_addresses
+def test_step_rejects_overlapping_buffers():
+    """The byte ranges of one tensor's buffers, sized from the formats, must
+    be pairwise disjoint: identical, partly overlapping or nested ranges are
+    rejected before any device work."""
+    lib = B.lib()
+    ref, _h = _hp()
+    n = 256
+    step = lambda w, wf, sc, cp, g, gf, m, v, ve, sf=0: lib.madd_step(  # noqa: E731
+        w, wf, sc, cp, g, gf, m, v, ve, sf, n, 0, ref, None)
+    assert step(W_, 0, None, None, G_, 0, M_, M_, E_) == -1               # v is m
+    assert step(W_, 0, None, None, G_, 0, M_, M_ + 4 * n - 16, E_) == -1  # v starts inside m
+    assert step(W_, 0, None, None, G_, 0, M_, V_, V_ + 2 * n - 2, 1) == -1  # bf16 v, ve share 2 bytes
+    assert step(W_, 0, None, None, M_ + 64, 0, M_, V_, E_) == -1          # g inside m
+    assert step(G_ + 4 * n - 2, 0, None, None, G_, 0, M_, V_, E_) == -1   # w's first code in g
+    assert step(W_, 1, W_ + 128, None, G_, 0, M_, V_, E_) == -1           # FP8 scales in the codes
+    assert step(W_, B.W_NVFP4, W_ + 112, None, G_, 0, M_, V_, E_) == -1   # NVFP4 scales in the codes
+    assert step(W_, 0, None, G_ + 16, G_, 0, M_, V_, E_) == -1            # compute copy in g
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
+    fm = (ctypes.c_int32 * 2)(0, 0)
+    ne = (ctypes.c_int64 * 2)(n, n)
+    w, g, m, v = (arr(p, p + 0x80000) for p in (W_, G_, M_, V_))
+    ve = arr(E_, V_ + 0x80000 + 4 * n - 4)  # second tensor's ve overlaps its v
+    assert lib.madd_multi_tensor_step(2, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref,
+                                      None) == -1
+    assert lib.madd_plain_step(W_, 0, W_ + 2 * n - 2, 0, n, 0, ref, None) == -1  # g in w
+    assert lib.madd_init_state(M_, V_, M_ + 4 * n - 4, 0, n, None) == -1          # ve in m
+    assert lib.madd_init_state(M_, V_, M_ + 2 * n - 2, 1, n, None) == -1          # bf16 ve in m
+    assert lib.madd_encode_weights(G_, G_ + 4 * n - 2, 0, None, n, None) == -1    # w in x
+    assert lib.madd_encode_weights(G_, W_, B.W_MXFP4, W_ + n // 2 - 1, n, None) == -1  # scales
+
+
+@fake_addresses
 def test_mxfp4_argument_rules():
     lib = B.lib()
     ref, _h = _hp()
-    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_MXFP4, sc, cp, FAKE, 0, FAKE, FAKE,  # noqa: E731
-                                                   FAKE, 0, n, 0, ref, None)
-    assert call(FAKE, None, 64) == -1            # MXFP4 needs its scales
-    assert call(FAKE, FAKE, 48) == -1            # n % 32
-    assert call(FAKE + 2, FAKE, 64) == -2        # unaligned payload bytes
-    assert call(FAKE, FAKE, 64, FAKE + 4) == -2  # unaligned compute copy
-    assert lib.madd_plain_step(FAKE, B.W_MXFP4, FAKE, 0, 64, 0, ref, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, None, 64, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, B.W_MXFP4, FAKE, 40, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, 7, FAKE, 64, None) == -1   # no such format
+    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_MXFP4, sc, cp, G_, 0, M_, V_,  # noqa: E731
+                                                   E_, 0, n, 0, ref, None)
+    assert call(W_, None, 64) == -1            # MXFP4 needs its scales
+    assert call(W_, S_, 48) == -1            # n % 32
+    assert call(W_ + 2, S_, 64) == -2        # unaligned payload bytes
+    assert call(W_, S_, 64, C_ + 4) == -2  # unaligned compute copy
+    assert lib.madd_plain_step(W_, B.W_MXFP4, G_, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(G_, W_, B.W_MXFP4, None, 64, None) == -1
+    assert lib.madd_encode_weights(G_, W_, B.W_MXFP4, S_, 40, None) == -1
+    assert lib.madd_encode_weights(G_, W_, 7, S_, 64, None) == -1   # no such format
 
 
+@fake_addresses
 def test_nvfp4_argument_rules():
     lib = B.lib()
     ref, _h = _hp()
-    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_NVFP4, sc, cp, FAKE, 0, FAKE, FAKE,  # noqa: E731
-                                                   FAKE, 0, n, 0, ref, None)
-    assert call(FAKE, None, 64) == -1            # NVFP4 needs its scales
-    assert call(FAKE, FAKE, 40) == -1            # n % 16
-    assert call(FAKE, FAKE + 2, 64) == -2        # tensor scale not 4-byte aligned
-    assert call(FAKE + 2, FAKE, 64) == -2        # unaligned payload bytes
-    assert call(FAKE, FAKE, 64, FAKE + 4) == -2  # unaligned compute copy
-    assert lib.madd_plain_step(FAKE, B.W_NVFP4, FAKE, 0, 64, 0, ref, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, None, 64, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE, 40, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, B.W_NVFP4, FAKE + 2, 64, None) == -2
+    call = lambda w, sc, n, cp=None: lib.madd_step(w, B.W_NVFP4, sc, cp, G_, 0, M_, V_,  # noqa: E731
+                                                   E_, 0, n, 0, ref, None)
+    assert call(W_, None, 64) == -1            # NVFP4 needs its scales
+    assert call(W_, S_, 40) == -1            # n % 16
+    assert call(W_, S_ + 2, 64) == -2        # tensor scale not 4-byte aligned
+    assert call(W_ + 2, S_, 64) == -2        # unaligned payload bytes
+    assert call(W_, S_, 64, C_ + 4) == -2  # unaligned compute copy
+    assert lib.madd_plain_step(W_, B.W_NVFP4, G_, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(G_, W_, B.W_NVFP4, None, 64, None) == -1
+    assert lib.madd_encode_weights(G_, W_, B.W_NVFP4, S_, 40, None) == -1
+    assert lib.madd_encode_weights(G_, W_, B.W_NVFP4, S_ + 2, 64, None) == -2
 
 
+@fake_addresses
 def test_nvfp4_current_argument_rules():
     lib = B.lib()
     ref, _h = _hp()
     W = B.W_NVFP4_CURRENT
-    call = lambda w, sc, n, gfmt=0, cp=None: lib.madd_step(w, W, sc, cp, FAKE, gfmt, FAKE, FAKE,  # noqa: E731
-                                                           FAKE, 0, n, 0, ref, None)
-    assert call(FAKE, None, 64) == -1            # scales required
-    assert call(FAKE, FAKE, 40) == -1            # n % 16
-    assert call(FAKE, FAKE + 2, 64) == -2        # scale array not 4-byte aligned
-    assert call(FAKE, FAKE, 64, gfmt=1) == -1    # w' is written over the gradient: fp32 only
-    assert lib.madd_plain_step(FAKE, W, FAKE, 0, 64, 0, ref, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, W, None, 64, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, W, FAKE, 40, None) == -1
+    call = lambda w, sc, n, gfmt=0, cp=None: lib.madd_step(w, W, sc, cp, G_, gfmt, M_, V_,  # noqa: E731
+                                                           E_, 0, n, 0, ref, None)
+    assert call(W_, None, 64) == -1            # scales required
+    assert call(W_, S_, 40) == -1            # n % 16
+    assert call(W_, S_ + 2, 64) == -2        # scale array not 4-byte aligned
+    assert call(W_, S_, 64, gfmt=1) == -1    # w' is written over the gradient: fp32 only
+    assert lib.madd_plain_step(W_, W, G_, 0, 64, 0, ref, None) == -1
+    assert lib.madd_encode_weights(G_, W_, W, None, 64, None) == -1
+    assert lib.madd_encode_weights(G_, W_, W, S_, 40, None) == -1
     PP = ctypes.POINTER(ctypes.c_void_p)
     arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
     n = (ctypes.c_int64 * 1)(64)
     wf = (ctypes.c_int32 * 1)(W)
-    assert lib.madd_multi_tensor_step(1, arr(FAKE), wf, arr(FAKE), None, arr(FAKE), 1, arr(FAKE),
-                                      arr(FAKE), arr(FAKE), 0, n, 0, ref, None) == -1
+    assert lib.madd_multi_tensor_step(1, arr(W_), wf, arr(S_), None, arr(G_), 1, arr(M_),
+                                      arr(V_), arr(E_), 0, n, 0, ref, None) == -1
 
 
+@fake_addresses
 def test_multi_tensor_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
@@ -180,49 +236,50 @@ def test_multi_tensor_rejects_bad_arguments():
     arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
     fm = (ctypes.c_int32 * 2)(0, 0)
     ne = (ctypes.c_int64 * 2)(128, 256)
-    ok_ptrs = [arr(FAKE, FAKE) for _ in range(5)]
-    w, g, m, v, ve = ok_ptrs
+    w, g, m, v, ve = (arr(p, p + 0x80000) for p in (W_, G_, M_, V_, E_))
     mt = lib.madd_multi_tensor_step
     assert mt(0, None, None, None, None, None, 0, None, None, None, 0, None, 0, ref, None) == 0
     assert mt(-1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
     assert mt(2, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, None, None) == -1
     assert mt(2, w, fm, None, None, g, 0, m, v, ve, 3, ne, 0, ref, None) == -1      # bad sfmt
-    bad = arr(FAKE, None)
+    bad = arr(V_, None)
     assert mt(2, w, fm, None, None, g, 0, m, bad, ve, 0, ne, 0, ref, None) == -1
     fm_bad = (ctypes.c_int32 * 2)(0, 11)
     assert mt(2, w, fm_bad, None, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
     ne_bad = (ctypes.c_int64 * 2)(128, -5)
     assert mt(2, w, fm, None, None, g, 0, m, v, ve, 0, ne_bad, 0, ref, None) == -1
-    sc = arr(None, FAKE)  # second tensor block-scaled but bf16
+    sc = arr(None, S_)  # second tensor block-scaled but bf16
     assert mt(2, w, fm, sc, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
     fm_mx = (ctypes.c_int32 * 2)(4, 4)
-    sc_one = arr(FAKE, None)  # second MXFP4 tensor without scales
+    sc_one = arr(S_, None)  # second MXFP4 tensor without scales
     assert mt(2, w, fm_mx, sc_one, None, g, 0, m, v, ve, 0, ne, 0, ref, None) == -1
 
 
+@fake_addresses
 def test_plain_step_rejects_bad_arguments():
     lib = B.lib()
     ref, _h = _hp()
-    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, 8, 0, None, None) == -1        # no hparams
-    assert lib.madd_plain_step(FAKE, 6, FAKE, 0, 8, 0, ref, None) == -1         # bad wfmt
-    assert lib.madd_plain_step(FAKE, 0, FAKE, 3, 8, 0, ref, None) == -1         # bad gfmt
-    assert lib.madd_plain_step(FAKE, 0, None, 0, 8, 0, ref, None) == -1         # null g
-    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, -2, 0, ref, None) == -1        # n < 0
+    assert lib.madd_plain_step(W_, 0, G_, 0, 8, 0, None, None) == -1        # no hparams
+    assert lib.madd_plain_step(W_, 6, G_, 0, 8, 0, ref, None) == -1         # bad wfmt
+    assert lib.madd_plain_step(W_, 0, G_, 3, 8, 0, ref, None) == -1         # bad gfmt
+    assert lib.madd_plain_step(W_, 0, None, 0, 8, 0, ref, None) == -1         # null g
+    assert lib.madd_plain_step(W_, 0, G_, 0, -2, 0, ref, None) == -1        # n < 0
     assert lib.madd_plain_step(None, 0, None, 0, 0, 0, ref, None) == 0          # empty
     bad, _h2 = _hp(r_max=1.5)
-    assert lib.madd_plain_step(FAKE, 0, FAKE, 0, 8, 0, bad, None) == -1
+    assert lib.madd_plain_step(W_, 0, G_, 0, 8, 0, bad, None) == -1
 
 
+@fake_addresses
 def test_init_and_encode_reject_bad_arguments():
     lib = B.lib()
-    assert lib.madd_init_state(FAKE, FAKE, FAKE, 0, -1, None) == -1
-    assert lib.madd_init_state(None, FAKE, FAKE, 0, 5, None) == -1
-    assert lib.madd_init_state(FAKE, FAKE, FAKE, 4, 5, None) == -1   # bad sfmt
+    assert lib.madd_init_state(M_, V_, E_, 0, -1, None) == -1
+    assert lib.madd_init_state(None, V_, E_, 0, 5, None) == -1
+    assert lib.madd_init_state(M_, V_, E_, 4, 5, None) == -1   # bad sfmt
     assert lib.madd_init_state(None, None, None, 1, 0, None) == 0
-    assert lib.madd_encode_weights(FAKE, FAKE, 7, None, 8, None) == -1
-    assert lib.madd_encode_weights(FAKE, FAKE, 0, FAKE, 128, None) == -1   # scales + bf16
-    assert lib.madd_encode_weights(FAKE, FAKE, 1, FAKE, 130, None) == -1   # n % 128
-    assert lib.madd_encode_weights(None, FAKE, 1, None, 8, None) == -1
+    assert lib.madd_encode_weights(G_, W_, 7, None, 8, None) == -1
+    assert lib.madd_encode_weights(G_, W_, 0, S_, 128, None) == -1   # scales + bf16
+    assert lib.madd_encode_weights(G_, W_, 1, S_, 130, None) == -1   # n % 128
+    assert lib.madd_encode_weights(None, W_, 1, None, 8, None) == -1
 
 
 def test_binding_has_no_cpu_fallback(monkeypatch, tmp_path):

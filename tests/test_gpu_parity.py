@@ -616,3 +616,44 @@ def test_binding_checks_buffer_sizes_before_launch():
         B.madd_multi_tensor_step(tl, hp())
     torch.cuda.synchronize()
     assert (m == 0).all() and (w == 0).all()
+
+
+def test_adjacent_slices_of_one_buffer_step_like_separate_buffers():
+    """Disjoint buffers may sit back to back in one allocation (m, v, v_e as
+    consecutive slices, the gradient right after the weights): the step takes
+    them and gives the same bits as separate allocations; slices that overlap
+    by one element are rejected (MADD_EINVAL) before any device work."""
+    n = 3 * 2048 + 520
+    rng = np.random.default_rng(91)
+    x = random_weights(rng, n, "bf16")
+    codes = oracle.encode_array("bf16", x)
+    h = hp(step=1, rounding="sr", seed=5)
+    results = []
+    for packed in (False, True):
+        grads = [random_grad(np.random.default_rng(7 + t), n) for t in (1, 2)]
+        if packed:
+            state = torch.zeros(3 * n, device="cuda")
+            m, v, ve = state[:n], state[n:2 * n], state[2 * n:]
+            wg = torch.zeros(n + 2 * n, dtype=torch.int16, device="cuda")  # w, then g (fp32)
+            w, g = wg[:n], wg[n:].view(torch.float32)
+        else:
+            m, v, ve = (torch.zeros(n, device="cuda") for _ in range(3))
+            w = torch.zeros(n, dtype=torch.int16, device="cuda")
+            g = torch.zeros(n, device="cuda")
+        w.copy_(torch.from_numpy(codes.view(np.int16)).cuda())
+        for t, gh in enumerate(grads, start=1):
+            g.copy_(torch.from_numpy(gh).cuda())
+            B.madd_step(w, "bf16", g, m, v, ve, dict(h, step=t))
+        torch.cuda.synchronize()
+        results.append([to_host(a) for a in (w, m, v, ve)])
+    for a, b in zip(*results):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+    state = torch.zeros(3 * n, device="cuda")
+    w = torch.zeros(n, dtype=torch.int16, device="cuda")
+    g = torch.zeros(n, device="cuda")
+    with pytest.raises(B.MaddError, match="EINVAL"):
+        B.madd_step(w, "bf16", g, state[:n], state[n - 1:2 * n - 1], state[2 * n:], h)
+    with pytest.raises(B.MaddError, match="EINVAL"):
+        B.madd_init_state(state[:n], state[:n], state[2 * n:])
+    torch.cuda.synchronize()
+    assert (state == 0).all()
