@@ -1,0 +1,178 @@
+"""``torch.optim`` front end of the M+Adam step (Section 3, Algorithm 2).
+
+A parameter's own storage is its weight storage: a bfloat16 parameter holds
+bf16 codes, a float32 one fp32 codes, float8_e4m3fn / float8_e5m2 ones E4M3 /
+E5M2 codes.  Each step rounds w' back into that format (to nearest, or
+stochastically with draws keyed by seed, step and each element's global
+index) and keeps m, v and v_e in the optimizer state, as fp32 or bf16.  Every
+update runs in the HIP kernels of libmadd.so: one madd_multi_tensor_step call
+per run of consecutive parameters that share a gradient dtype and a step
+count, on the current stream; nothing falls back to the CPU.
+
+Global indices: the optimizer's k-th parameter (counting over all groups in
+order) starts at the total size of the parameters before it, fixed when it
+is added, so its draws do not depend on which other parameters have
+gradients in a step, and a rebuilt optimizer over the same parameters draws
+the same bits.
+"""
+from __future__ import annotations
+
+import math
+from collections import OrderedDict
+
+import torch
+
+from . import binding as B
+
+# weight dtype -> (storage format, integer view of the codes)
+_WEIGHTS = {torch.bfloat16: ("bf16", torch.int16), torch.float32: ("fp32", torch.int32)}
+for _name, _fmt in (("float8_e4m3fn", "e4m3"), ("float8_e5m2", "e5m2")):
+    if hasattr(torch, _name):
+        _WEIGHTS[getattr(torch, _name)] = (_fmt, torch.uint8)
+_GRADS = {torch.float32: "fp32", torch.bfloat16: "bf16"}
+_STATES = {"fp32": torch.float32, "bf16": torch.int16, "bf16_sr": torch.int16}
+_HP_KEYS = ("lr_add", "lr_mul", "eps", "tau", "r_max", "eps0", "g_max", "d_mult_max", "w_max",
+            "rounding", "seed")
+
+
+class MAdam(torch.optim.Optimizer):
+    """M+Adam with its weights kept in the parameters' low-precision storage.
+
+    lr_add, lr_mul: the additive and multiplicative learning rates (eta_a,
+    eta_m); betas: (beta1, beta2); eps; tau: the floor of |w| in the relative
+    multiplicative update; r_max, eps0: its clip (-(r_max - eps0), r_max);
+    g_max: clip of the normalized exponent gradient; d_mult_max: cap on the
+    exponent change (2^+-d); w_max: final clamp of w'; bias_correction;
+    rounding: "sr" or "rne"; seed: the stochastic-rounding key; state_format:
+    "fp32", "bf16" or "bf16_sr" (bf16 moments rounded to nearest or
+    stochastically)."""
+
+    def __init__(self, params, lr_add: float = 1e-3, lr_mul: float = 1e-3,
+                 betas=(0.9, 0.999), eps: float = 1e-8, tau: float = 1e-8, r_max: float = 0.75,
+                 eps0: float = 0.0, g_max: float = math.inf, d_mult_max: float = math.inf,
+                 w_max: float = math.inf, bias_correction: bool = True, rounding: str = "sr",
+                 seed: int = 0, state_format: str = "fp32"):
+        if rounding not in B.ROUND:
+            raise ValueError(f"rounding must be one of {sorted(B.ROUND)}, not {rounding!r}")
+        if state_format not in _STATES:
+            raise ValueError(f"state_format must be one of {sorted(_STATES)}, "
+                             f"not {state_format!r}")
+        if len(tuple(betas)) != 2:
+            raise ValueError("betas must be (beta1, beta2)")
+        defaults = dict(lr_add=lr_add, lr_mul=lr_mul, betas=tuple(betas), eps=eps, tau=tau,
+                        r_max=r_max, eps0=eps0, g_max=g_max, d_mult_max=d_mult_max,
+                        w_max=w_max, bias_correction=bool(bias_correction), rounding=rounding,
+                        seed=int(seed), state_format=state_format)
+        self._base = {}          # parameter -> global index of its first element
+        self._next_base = 0
+        self._lists = OrderedDict()  # marshalled lists of recent runs (LRU)
+        super().__init__(params, defaults)
+
+    def add_param_group(self, param_group):
+        super().add_param_group(param_group)
+        for p in self.param_groups[-1]["params"]:
+            if p not in self._base:
+                self._base[p] = self._next_base
+                self._next_base += p.numel()
+
+    def load_state_dict(self, state_dict):
+        """As torch.optim.Optimizer's, except that the moments keep the dtype
+        and bits they were saved with (the base class casts every state
+        tensor to its parameter's dtype)."""
+        from itertools import chain
+        saved = state_dict["state"]
+        super().load_state_dict(state_dict)
+        ids = chain.from_iterable(g["params"] for g in state_dict["param_groups"])
+        params = chain.from_iterable(g["params"] for g in self.param_groups)
+        for pid, p in zip(ids, params):
+            for k in ("m", "v", "ve"):
+                if pid in saved and k in saved[pid]:
+                    self.state[p][k] = saved[pid][k].to(device=p.device, copy=True)
+        self._lists.clear()
+
+    @staticmethod
+    def _check_param(p):
+        if p.dtype not in _WEIGHTS:
+            raise TypeError(f"MAdam: parameters of dtype {p.dtype} have no storage format "
+                            f"(supported: {sorted(str(d) for d in _WEIGHTS)})")
+        g = p.grad
+        if g.is_sparse:
+            raise TypeError("MAdam: sparse gradients are not supported")
+        if g.dtype not in _GRADS:
+            raise TypeError(f"MAdam: gradients of dtype {g.dtype} are not supported "
+                            "(float32 or bfloat16)")
+        for what, t in (("parameter", p), ("gradient", g)):
+            if not t.is_cuda:
+                raise ValueError(f"MAdam: every {what} must be a GPU tensor (got {t.device})")
+            if not t.is_contiguous():
+                raise ValueError(f"MAdam: every {what} must be contiguous")
+        if g.shape != p.shape:
+            raise ValueError("MAdam: gradient and parameter shapes differ")
+
+    def _state_of(self, p, sfmt: str):
+        st = self.state[p]
+        if not st:
+            dt = _STATES[sfmt]
+            st["step"] = 0
+            st["m"], st["v"], st["ve"] = (torch.empty(p.numel(), dtype=dt, device=p.device)
+                                          for _ in range(3))
+            B.madd_init_state(st["m"], st["v"], st["ve"], sfmt=sfmt)
+        if st["m"].dtype != _STATES[sfmt] or st["m"].numel() != p.numel():
+            raise ValueError(f"MAdam: the state of a parameter does not hold {sfmt} moments of "
+                             f"{p.numel()} elements")
+        return st
+
+    def _marshal(self, run, sfmt: str):
+        key = (sfmt,) + tuple((p.data_ptr(), p.numel(), p.dtype, self.state[p]["m"].data_ptr(),
+                               self.state[p]["v"].data_ptr(), self.state[p]["ve"].data_ptr())
+                              for p in run)
+        tl = self._lists.get(key)
+        gs = [p.grad for p in run]
+        if tl is None:
+            ws = [p.detach().view(_WEIGHTS[p.dtype][1]).view(-1) for p in run]
+            st = [self.state[p] for p in run]
+            tl = B.TensorList(ws, [_WEIGHTS[p.dtype][0] for p in run], gs,
+                              [s["m"] for s in st], [s["v"] for s in st], [s["ve"] for s in st],
+                              sfmt=sfmt)
+            self._lists[key] = tl
+            while len(self._lists) > 16:
+                self._lists.popitem(last=False)
+        else:
+            self._lists.move_to_end(key)
+            tl.set_grads(gs)
+        return tl
+
+    @torch.no_grad()
+    def step(self, closure=None):
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for group in self.param_groups:
+            sfmt = group["state_format"]
+            runs, cur, cur_key, end = [], None, None, None
+            for p in group["params"]:
+                if p.grad is None:
+                    cur = None
+                    continue
+                self._check_param(p)
+                st = self._state_of(p, sfmt)
+                key = (_GRADS[p.grad.dtype], st["step"])
+                if cur is None or key != cur_key or self._base[p] != end:
+                    cur, cur_key = [], key
+                    runs.append((key, cur))
+                cur.append(p)
+                end = self._base[p] + p.numel()
+            b1, b2 = group["betas"]
+            for (gfmt, t), run in runs:
+                hp = {k: group[k] for k in _HP_KEYS}
+                hp.update(beta1=b1, beta2=b2, bias_correction=int(group["bias_correction"]),
+                          step=t + 1)
+                tl = self._marshal(run, sfmt)
+                B.madd_multi_tensor_step(tl, hp, gfmt=gfmt, index_base=self._base[run[0]])
+                # the launch is ordered on the current stream: the gradients
+                # need no reference past it
+                tl.set_grads([None] * tl.n)
+                for p in run:
+                    self.state[p]["step"] = t + 1
+        return loss

@@ -1,0 +1,209 @@
+"""The torch.optim front end (paper_2607_10611_amd.optim.MAdam) against the
+CPU oracle (GPU): every parameter's stored codes bit-exact and fp32 moments
+within 2 ulp after each step, each parameter keyed by its own global index
+base, with fp32 or bf16 gradients, fp32 / bf16 / stochastic bf16 moments,
+bf16, fp32 and FP8 parameters, gaps (parameters without gradients), a
+state_dict round trip and a bf16 layer trained through autograd."""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_10611_amd import binding as B
+from paper_2607_10611_amd.optim import MAdam
+from gpu_parity_util import HostState, assert_state_equal, oracle_step, to_host
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(4096 + 40,), (1000,), (3, 2048 + 8), (33,), (64, 64)]
+CODE = {torch.bfloat16: ("bf16", torch.int16, np.uint16), torch.float32: ("fp32", torch.int32, np.uint32),
+        torch.float8_e4m3fn: ("e4m3", torch.uint8, np.uint8)}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def make_params(seed, dtype=torch.bfloat16, grad_dtype=None):
+    gen = torch.Generator().manual_seed(seed)
+    ps = []
+    for s in SHAPES:
+        x = (torch.randn(s, generator=gen) * 0.02)
+        if dtype == torch.float8_e4m3fn:
+            x = x.clamp(-448, 448)
+        p = torch.nn.Parameter(x.to(dtype).cuda())
+        if grad_dtype is not None and grad_dtype != dtype:
+            p.grad_dtype = None
+        ps.append(p)
+    return ps
+
+
+def grads(seed, ps, dtype):
+    gen = torch.Generator().manual_seed(seed)
+    out = []
+    for p in ps:
+        g = torch.randn(p.shape, generator=gen) * 10.0 ** torch.empty(p.shape).uniform_(
+            -6, -2, generator=gen)
+        g[torch.rand(p.shape, generator=gen) < 0.05] = 0.0
+        out.append(g.to(dtype))
+    return out
+
+
+def host_states(ps, sfmt):
+    out = []
+    for p in ps:
+        fmt, it, nt = CODE[p.dtype]
+        codes = to_host(p.detach().view(it).reshape(-1), nt)
+        out.append(HostState(codes, p.numel(), sfmt=sfmt))
+    return out
+
+
+def group_hp(opt, p, step):
+    g = next(gr for gr in opt.param_groups if any(q is p for q in gr["params"]))
+    hp = {k: g[k] for k in ("lr_add", "lr_mul", "eps", "tau", "r_max", "eps0", "g_max",
+                            "d_mult_max", "w_max", "rounding", "seed")}
+    hp.update(beta1=g["betas"][0], beta2=g["betas"][1], bias_correction=int(g["bias_correction"]),
+              step=step)
+    return hp
+
+
+def compare(tag, opt, ps, hs, sfmt):
+    torch.cuda.synchronize()
+    for i, (p, h) in enumerate(zip(ps, hs)):
+        fmt, it, nt = CODE[p.dtype]
+        st = opt.state[p]
+        w = to_host(p.detach().view(it).reshape(-1), nt)
+        sn = np.float32 if sfmt == "fp32" else np.uint16
+        m, v, ve = (to_host(st[k], sn) for k in ("m", "v", "ve"))
+        assert_state_equal(f"{tag} param {i}", w, h.w, m, h.m, v, h.v, ve, h.ve)
+
+
+def oracle_steps(opt, ps, hs, gs, gfmt, have=None):
+    for i, (p, h, g) in enumerate(zip(ps, hs, gs)):
+        if have is not None and not have[i]:
+            continue
+        gh = g.reshape(-1).cpu()
+        gh = gh.view(torch.int16).numpy().view(np.uint16) if gfmt == "bf16" else gh.numpy()
+        oracle_step(CODE[p.dtype][0], h, gh.copy(), group_hp(opt, p, opt.state[p]["step"]),
+                    gfmt=gfmt, index_base=opt._base[p])
+
+
+@pytest.mark.parametrize("sfmt", ["fp32", "bf16", "bf16_sr"])
+@pytest.mark.parametrize("gdt", [torch.float32, torch.bfloat16])
+def test_madam_steps_match_the_oracle(sfmt, gdt):
+    ps = make_params(1, grad_dtype=gdt)
+    opt = MAdam([{"params": ps[:3]}, {"params": ps[3:], "lr_add": 3e-3, "lr_mul": 2e-3}],
+                seed=0x5EED, state_format=sfmt)
+    hs = host_states(ps, sfmt)
+    gfmt = "fp32" if gdt == torch.float32 else "bf16"
+    for t in range(1, 4):
+        gs = grads(100 + t, ps, gdt)
+        for p, g in zip(ps, gs):
+            p.grad = g.cuda()
+        opt.step()
+        oracle_steps(opt, ps, hs, gs, gfmt)
+        compare(f"{sfmt} {gfmt} t={t}", opt, ps, hs, sfmt)
+    assert all(opt.state[p]["step"] == 3 for p in ps)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.float8_e4m3fn])
+def test_fp32_and_fp8_parameters(dtype):
+    ps = make_params(2, dtype=dtype, grad_dtype=torch.float32)
+    opt = MAdam(ps, rounding="sr", seed=9)
+    hs = host_states(ps, "fp32")
+    for t in range(1, 3):
+        gs = grads(200 + t, ps, torch.float32)
+        for p, g in zip(ps, gs):
+            p.grad = g.cuda()
+        opt.step()
+        oracle_steps(opt, ps, hs, gs, "fp32")
+        compare(f"{dtype} t={t}", opt, ps, hs, "fp32")
+
+
+def test_parameters_without_gradients_keep_the_others_keyed_by_their_own_bases():
+    ps = make_params(3, grad_dtype=torch.float32)
+    opt = MAdam(ps, seed=77)
+    hs = host_states(ps, "fp32")
+    pattern = [[1, 1, 1, 1, 1], [1, 0, 1, 0, 1], [0, 1, 1, 1, 1]]
+    for t, have in enumerate(pattern, start=101):
+        gs = grads(t, ps, torch.float32)
+        for p, g, h in zip(ps, gs, have):
+            p.grad = g.cuda() if h else None
+        before = [p.detach().clone() for p in ps]
+        opt.step()
+        oracle_steps(opt, ps, hs, gs, "fp32", have=have)
+        compare(f"gaps {have}", opt, ps, hs, "fp32")
+        for p, b, h in zip(ps, before, have):
+            if not h:
+                assert torch.equal(p.detach().view(torch.int16), b.view(torch.int16))
+    assert [opt.state[p]["step"] for p in ps] == [2, 2, 3, 2, 3]
+
+
+def test_state_dict_round_trip_continues_bit_exact():
+    for sfmt in ("fp32", "bf16"):
+        ps = make_params(4, grad_dtype=torch.float32)
+        opt = MAdam(ps, seed=3, state_format=sfmt)
+        all_g = [grads(300 + t, ps, torch.float32) for t in range(4)]
+        for t in range(2):
+            for p, g in zip(ps, all_g[t]):
+                p.grad = g.cuda()
+            opt.step()
+        sd = copy.deepcopy(opt.state_dict())
+        qs = [torch.nn.Parameter(p.detach().clone()) for p in ps]
+        for q in qs:
+            q.grad_dtype = None
+        opt2 = MAdam(qs, seed=3, state_format=sfmt)
+        opt2.load_state_dict(sd)
+        for p, q in zip(ps, qs):
+            for k in ("m", "v", "ve"):
+                assert opt2.state[q][k].dtype == opt.state[p][k].dtype
+                assert torch.equal(opt2.state[q][k], opt.state[p][k])
+        for t in range(2, 4):
+            for p, q, g in zip(ps, qs, all_g[t]):
+                p.grad = g.cuda()
+                q.grad = g.cuda()
+            opt.step()
+            opt2.step()
+        torch.cuda.synchronize()
+        for p, q in zip(ps, qs):
+            assert torch.equal(p.detach().view(torch.int16), q.detach().view(torch.int16))
+            for k in ("m", "v", "ve"):
+                assert torch.equal(opt.state[p][k], opt2.state[q][k])
+
+
+def test_bf16_linear_layer_trained_through_autograd():
+    torch.manual_seed(0)
+    layer = torch.nn.Linear(64, 48, dtype=torch.bfloat16, device="cuda")
+    ps = list(layer.parameters())
+    opt = MAdam(ps, lr_add=1e-2, lr_mul=1e-2, seed=11)
+    hs = host_states(ps, "fp32")
+    x = torch.randn(128, 64, dtype=torch.bfloat16, device="cuda")
+    y = torch.randn(128, 48, dtype=torch.bfloat16, device="cuda")
+    losses = []
+    for t in range(1, 6):
+        opt.zero_grad(set_to_none=True)
+        # fp32 products on the bf16 parameters: their gradients come back in bf16
+        out = torch.nn.functional.linear(x.float(), layer.weight.float(), layer.bias.float())
+        loss = ((out - y.float()) ** 2).mean()
+        loss.backward()
+        losses.append(float(loss.detach()))
+        gs = [p.grad.detach().clone() for p in ps]
+        opt.step()
+        oracle_steps(opt, ps, hs, gs, "bf16")
+        compare(f"linear t={t}", opt, ps, hs, "fp32")
+    assert losses[-1] < losses[0]
+
+
+def test_rejects_a_state_of_the_wrong_format():
+    p = torch.nn.Parameter(torch.zeros(64, dtype=torch.bfloat16, device="cuda"))
+    opt = MAdam([p], state_format="bf16")
+    p.grad = torch.zeros_like(p)
+    opt.step()
+    opt.state[p]["m"] = torch.zeros(64, device="cuda")  # fp32 where bf16 moments live
+    with pytest.raises(ValueError, match="bf16 moments"):
+        opt.step()

@@ -1,0 +1,48 @@
+"""Host-side rules of the torch.optim front end (CPU: no kernel runs)."""
+import pytest
+import torch
+
+from paper_2607_10611_amd.optim import MAdam
+
+
+def test_constructor_rejects_bad_options():
+    p = [torch.nn.Parameter(torch.zeros(4, dtype=torch.bfloat16))]
+    with pytest.raises(ValueError, match="rounding"):
+        MAdam(p, rounding="nearest")
+    with pytest.raises(ValueError, match="state_format"):
+        MAdam(p, state_format="fp16")
+    with pytest.raises(ValueError, match="betas"):
+        MAdam(p, betas=(0.9,))
+
+
+def test_global_index_bases_follow_parameter_order_across_groups():
+    ps = [torch.nn.Parameter(torch.zeros(n, dtype=torch.bfloat16)) for n in (3, 5, 7, 11)]
+    opt = MAdam([{"params": ps[:2]}, {"params": ps[2:3], "lr_add": 1e-2}])
+    opt.add_param_group({"params": ps[3:]})
+    assert [opt._base[p] for p in ps] == [0, 3, 8, 15]
+
+
+def test_step_refuses_host_tensors_and_unsupported_dtypes_before_any_call():
+    p = torch.nn.Parameter(torch.zeros(8, dtype=torch.bfloat16))
+    p.grad = torch.zeros(8, dtype=torch.bfloat16)
+    opt = MAdam([p])
+    with pytest.raises(ValueError, match="GPU tensor"):
+        opt.step()
+    assert not opt.state[p]  # no state was made
+    q = torch.nn.Parameter(torch.zeros(8, dtype=torch.float16))
+    q.grad = torch.zeros(8, dtype=torch.float16)
+    with pytest.raises(TypeError, match="no storage format"):
+        MAdam([q]).step()
+    r = torch.nn.Parameter(torch.zeros(8, dtype=torch.bfloat16))
+    r.grad_dtype = None  # allow a gradient dtype other than the parameter's
+    r.grad = torch.zeros(8, dtype=torch.float64)
+    with pytest.raises(TypeError, match="gradients of dtype"):
+        MAdam([r]).step()
+
+
+def test_step_without_gradients_is_a_no_op():
+    p = torch.nn.Parameter(torch.zeros(8, dtype=torch.bfloat16))
+    opt = MAdam([p])
+    assert opt.step() is None
+    assert opt.step(lambda: 3.0) == 3.0
+    assert not opt.state[p]
