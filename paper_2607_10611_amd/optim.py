@@ -31,6 +31,10 @@ for _name, _fmt in (("float8_e4m3fn", "e4m3"), ("float8_e5m2", "e5m2")):
         _WEIGHTS[getattr(torch, _name)] = (_fmt, torch.uint8)
 _GRADS = {torch.float32: "fp32", torch.bfloat16: "bf16"}
 _STATES = {"fp32": torch.float32, "bf16": torch.int16, "bf16_sr": torch.int16}
+# block-scaled master formats -> elements per block
+_MASTERS = {"e4m3": 128, "e5m2": 128, "mxfp4": B.MX_BLOCK, "nvfp4": B.NV_BLOCK,
+            "nvfp4_current": B.NV_BLOCK}
+_SAVED = ("m", "v", "ve", "q", "scales")  # state tensors whose dtype and bits are kept
 _HP_KEYS = ("lr_add", "lr_mul", "eps", "tau", "r_max", "eps0", "g_max", "d_mult_max", "w_max",
             "rounding", "seed")
 
@@ -45,13 +49,24 @@ class MAdam(torch.optim.Optimizer):
     exponent change (2^+-d); w_max: final clamp of w'; bias_correction;
     rounding: "sr" or "rne"; seed: the stochastic-rounding key; state_format:
     "fp32", "bf16" or "bf16_sr" (bf16 moments rounded to nearest or
-    stochastically)."""
+    stochastically).
+
+    master_format (per group; default None): keep the master weights of the
+    group's bfloat16 parameters in the optimizer state in a block-scaled
+    format -- "e4m3" / "e5m2" (blocks of 128, FP16 scales), "mxfp4", "nvfp4"
+    (its tensor scale kept) or "nvfp4_current" (derived anew every step,
+    which overwrites the fp32 gradient with w') -- encoded from the
+    parameters when the state is made (Section 4.2's FP8-master setting and
+    its 4-bit analogues).  Each step then writes the bf16 compute copy of the
+    new master weights into the parameter (until the first step the
+    parameter keeps its own values).  Such parameters need a size that
+    is a multiple of the block and 16-byte-aligned storage."""
 
     def __init__(self, params, lr_add: float = 1e-3, lr_mul: float = 1e-3,
                  betas=(0.9, 0.999), eps: float = 1e-8, tau: float = 1e-8, r_max: float = 0.75,
                  eps0: float = 0.0, g_max: float = math.inf, d_mult_max: float = math.inf,
                  w_max: float = math.inf, bias_correction: bool = True, rounding: str = "sr",
-                 seed: int = 0, state_format: str = "fp32"):
+                 seed: int = 0, state_format: str = "fp32", master_format: str | None = None):
         if rounding not in B.ROUND:
             raise ValueError(f"rounding must be one of {sorted(B.ROUND)}, not {rounding!r}")
         if state_format not in _STATES:
@@ -59,16 +74,24 @@ class MAdam(torch.optim.Optimizer):
                              f"not {state_format!r}")
         if len(tuple(betas)) != 2:
             raise ValueError("betas must be (beta1, beta2)")
+        self._check_master(master_format)
         defaults = dict(lr_add=lr_add, lr_mul=lr_mul, betas=tuple(betas), eps=eps, tau=tau,
                         r_max=r_max, eps0=eps0, g_max=g_max, d_mult_max=d_mult_max,
                         w_max=w_max, bias_correction=bool(bias_correction), rounding=rounding,
-                        seed=int(seed), state_format=state_format)
+                        seed=int(seed), state_format=state_format, master_format=master_format)
         self._base = {}          # parameter -> global index of its first element
         self._next_base = 0
         self._lists = OrderedDict()  # marshalled lists of recent runs (LRU)
         super().__init__(params, defaults)
 
+    @staticmethod
+    def _check_master(fmt):
+        if fmt is not None and fmt not in _MASTERS:
+            raise ValueError(f"master_format must be None or one of {sorted(_MASTERS)}, "
+                             f"not {fmt!r}")
+
     def add_param_group(self, param_group):
+        self._check_master(param_group.get("master_format"))
         super().add_param_group(param_group)
         for p in self.param_groups[-1]["params"]:
             if p not in self._base:
@@ -85,13 +108,27 @@ class MAdam(torch.optim.Optimizer):
         ids = chain.from_iterable(g["params"] for g in state_dict["param_groups"])
         params = chain.from_iterable(g["params"] for g in self.param_groups)
         for pid, p in zip(ids, params):
-            for k in ("m", "v", "ve"):
+            for k in _SAVED:
                 if pid in saved and k in saved[pid]:
                     self.state[p][k] = saved[pid][k].to(device=p.device, copy=True)
         self._lists.clear()
 
     @staticmethod
-    def _check_param(p):
+    def _check_param(p, master):
+        if master is not None:
+            if p.dtype != torch.bfloat16:
+                raise TypeError(f"MAdam: parameters with a {master} master hold its bf16 "
+                                f"compute copy and must be bfloat16 (got {p.dtype})")
+            if p.numel() % _MASTERS[master] != 0:
+                raise ValueError(f"MAdam: a {master} master needs a multiple of "
+                                 f"{_MASTERS[master]} elements (got {p.numel()})")
+            for what, t in (("parameter", p), ("gradient", p.grad)):
+                if t.data_ptr() % 16 != 0:
+                    raise ValueError(f"MAdam: a block-scaled master needs a 16-byte-aligned "
+                                     f"{what}")
+            if master == "nvfp4_current" and p.grad.dtype != torch.float32:
+                raise TypeError("MAdam: nvfp4_current writes w' over the gradient, which "
+                                "must be float32")
         if p.dtype not in _WEIGHTS:
             raise TypeError(f"MAdam: parameters of dtype {p.dtype} have no storage format "
                             f"(supported: {sorted(str(d) for d in _WEIGHTS)})")
@@ -109,7 +146,7 @@ class MAdam(torch.optim.Optimizer):
         if g.shape != p.shape:
             raise ValueError("MAdam: gradient and parameter shapes differ")
 
-    def _state_of(self, p, sfmt: str):
+    def _state_of(self, p, sfmt: str, master):
         st = self.state[p]
         if not st:
             dt = _STATES[sfmt]
@@ -117,23 +154,39 @@ class MAdam(torch.optim.Optimizer):
             st["m"], st["v"], st["ve"] = (torch.empty(p.numel(), dtype=dt, device=p.device)
                                           for _ in range(3))
             B.madd_init_state(st["m"], st["v"], st["ve"], sfmt=sfmt)
+            if master is not None:
+                n = p.numel()
+                st["q"] = torch.empty(math.ceil(n * B.CODE_BYTES[master]), dtype=torch.uint8,
+                                      device=p.device)
+                st["scales"] = torch.empty(B.scale_bytes(master, n), dtype=torch.uint8,
+                                           device=p.device)
+                x = p.detach().float().reshape(-1).contiguous()
+                B.madd_encode_weights(x, st["q"], master, scales=st["scales"])
+        if (master is not None) != ("q" in st):
+            raise ValueError("MAdam: a parameter's state does not match its group's "
+                             "master_format")
         if st["m"].dtype != _STATES[sfmt] or st["m"].numel() != p.numel():
             raise ValueError(f"MAdam: the state of a parameter does not hold {sfmt} moments of "
                              f"{p.numel()} elements")
         return st
 
-    def _marshal(self, run, sfmt: str):
-        key = (sfmt,) + tuple((p.data_ptr(), p.numel(), p.dtype, self.state[p]["m"].data_ptr(),
-                               self.state[p]["v"].data_ptr(), self.state[p]["ve"].data_ptr())
-                              for p in run)
+    def _marshal(self, run, sfmt: str, master):
+        key = (sfmt, master) + tuple(
+            (p.data_ptr(), p.numel(), p.dtype) +
+            tuple(t.data_ptr() for k, t in self.state[p].items() if k in _SAVED) for p in run)
         tl = self._lists.get(key)
         gs = [p.grad for p in run]
         if tl is None:
-            ws = [p.detach().view(_WEIGHTS[p.dtype][1]).view(-1) for p in run]
             st = [self.state[p] for p in run]
-            tl = B.TensorList(ws, [_WEIGHTS[p.dtype][0] for p in run], gs,
-                              [s["m"] for s in st], [s["v"] for s in st], [s["ve"] for s in st],
-                              sfmt=sfmt)
+            ms, vs, ves = ([s[k] for s in st] for k in ("m", "v", "ve"))
+            if master is None:
+                ws = [p.detach().view(_WEIGHTS[p.dtype][1]).view(-1) for p in run]
+                tl = B.TensorList(ws, [_WEIGHTS[p.dtype][0] for p in run], gs, ms, vs, ves,
+                                  sfmt=sfmt)
+            else:
+                copies = [p.detach().view(torch.int16).view(-1) for p in run]
+                tl = B.TensorList([s["q"] for s in st], [master] * len(run), gs, ms, vs, ves,
+                                  scales=[s["scales"] for s in st], sfmt=sfmt, copies=copies)
             self._lists[key] = tl
             while len(self._lists) > 16:
                 self._lists.popitem(last=False)
@@ -150,13 +203,14 @@ class MAdam(torch.optim.Optimizer):
                 loss = closure()
         for group in self.param_groups:
             sfmt = group["state_format"]
+            master = group.get("master_format")
             runs, cur, cur_key, end = [], None, None, None
             for p in group["params"]:
                 if p.grad is None:
                     cur = None
                     continue
-                self._check_param(p)
-                st = self._state_of(p, sfmt)
+                self._check_param(p, master)
+                st = self._state_of(p, sfmt, master)
                 key = (_GRADS[p.grad.dtype], st["step"])
                 if cur is None or key != cur_key or self._base[p] != end:
                     cur, cur_key = [], key
@@ -168,7 +222,7 @@ class MAdam(torch.optim.Optimizer):
                 hp = {k: group[k] for k in _HP_KEYS}
                 hp.update(beta1=b1, beta2=b2, bias_correction=int(group["bias_correction"]),
                           step=t + 1)
-                tl = self._marshal(run, sfmt)
+                tl = self._marshal(run, sfmt, master)
                 B.madd_multi_tensor_step(tl, hp, gfmt=gfmt, index_base=self._base[run[0]])
                 # the launch is ordered on the current stream: the gradients
                 # need no reference past it

@@ -2,14 +2,16 @@
 CPU oracle (GPU): every parameter's stored codes bit-exact and fp32 moments
 within 2 ulp after each step, each parameter keyed by its own global index
 base, with fp32 or bf16 gradients, fp32 / bf16 / stochastic bf16 moments,
-bf16, fp32 and FP8 parameters, gaps (parameters without gradients), a
-state_dict round trip and a bf16 layer trained through autograd."""
+bf16, fp32 and FP8 parameters, block-scaled master weights (FP8, MXFP4,
+NVFP4) with bf16 compute copies, gaps (parameters without gradients),
+state_dict round trips and a bf16 layer trained through autograd."""
 import copy
 
 import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd.optim import MAdam
 from gpu_parity_util import HostState, assert_state_equal, oracle_step, to_host
@@ -207,3 +209,89 @@ def test_rejects_a_state_of_the_wrong_format():
     opt.state[p]["m"] = torch.zeros(64, device="cuda")  # fp32 where bf16 moments live
     with pytest.raises(ValueError, match="bf16 moments"):
         opt.step()
+
+
+def oracle_master(fmt, x):
+    if fmt in ("e4m3", "e5m2"):
+        return oracle.encode_block(fmt, x)
+    return {"mxfp4": oracle.encode_mx, "nvfp4": oracle.encode_nv,
+            "nvfp4_current": oracle.encode_nv_current}[fmt](x)
+
+
+@pytest.mark.parametrize("master", ["e4m3", "e5m2", "mxfp4", "nvfp4", "nvfp4_current"])
+def test_block_scaled_master_weights_with_bf16_compute_copies(master):
+    """The paper's mixed list through the optimizer: block-scaled master
+    weights for the 'linear' group (bf16 parameters hold the compute copy),
+    bf16 storage for the rest; master codes, scales, compute copies and
+    moments bit-exact against the oracle, which encodes its own starting
+    codes from the same fp32 values."""
+    gen = torch.Generator().manual_seed(5)
+    lin = [torch.nn.Parameter((torch.randn(s, generator=gen) * 0.02).to(torch.bfloat16).cuda())
+           for s in ((8, 128), (3, 512), (2048,))]
+    rest = [torch.nn.Parameter((torch.randn(s, generator=gen) * 0.02).to(torch.bfloat16).cuda())
+            for s in ((1000,), (33,))]
+    for p in lin + rest:
+        p.grad_dtype = None
+    opt = MAdam([{"params": lin, "master_format": master}, {"params": rest}], seed=21,
+                rounding="sr")
+    hl = []
+    for p in lin:
+        q, sc = oracle_master(master, p.detach().float().cpu().numpy().reshape(-1))
+        hl.append(HostState(q, p.numel(), scales=sc, copy=True))
+    hr = host_states(rest, "fp32")
+    for t in range(1, 4):
+        gs = grads(400 + t, lin + rest, torch.float32)
+        for p, g in zip(lin + rest, gs):
+            p.grad = g.cuda()
+        opt.step()
+        for p, h, g in zip(lin, hl, gs[:len(lin)]):
+            oracle_step(master, h, g.reshape(-1).numpy().copy(),
+                        group_hp(opt, p, opt.state[p]["step"]), index_base=opt._base[p])
+        oracle_steps(opt, rest, hr, gs[len(lin):], "fp32")
+        torch.cuda.synchronize()
+        for i, (p, h) in enumerate(zip(lin, hl)):
+            st = opt.state[p]
+            sc = to_host(st["scales"], np.uint8)
+            if master in ("e4m3", "e5m2"):
+                sc = sc.view(np.uint16)
+            assert_state_equal(f"{master} t={t} param {i}", to_host(st["q"], np.uint8), h.w,
+                               to_host(st["m"]), h.m, to_host(st["v"]), h.v, to_host(st["ve"]),
+                               h.ve)
+            assert np.array_equal(sc, h.scales), f"{master} t={t} param {i}: scales"
+            cp = to_host(p.detach().view(torch.int16).reshape(-1), np.uint16)
+            assert np.array_equal(cp, h.copy), f"{master} t={t} param {i}: compute copy"
+        compare(f"{master} rest t={t}", opt, rest, hr, "fp32")
+
+
+def test_state_dict_round_trip_keeps_master_codes_and_scales():
+    gen = torch.Generator().manual_seed(6)
+    ps = [torch.nn.Parameter((torch.randn(s, generator=gen) * 0.02).to(torch.bfloat16).cuda())
+          for s in ((4, 128), (256,))]
+    for p in ps:
+        p.grad_dtype = None
+    opt = MAdam(ps, master_format="nvfp4", seed=8)
+    all_g = [grads(500 + t, ps, torch.float32) for t in range(3)]
+    for p, g in zip(ps, all_g[0]):
+        p.grad = g.cuda()
+    opt.step()
+    sd = copy.deepcopy(opt.state_dict())
+    qs = [torch.nn.Parameter(p.detach().clone()) for p in ps]
+    for q in qs:
+        q.grad_dtype = None
+    opt2 = MAdam(qs, master_format="nvfp4", seed=8)
+    opt2.load_state_dict(sd)
+    for p, q in zip(ps, qs):
+        for k in ("q", "scales", "m", "v", "ve"):
+            assert opt2.state[q][k].dtype == opt.state[p][k].dtype, k
+            assert torch.equal(opt2.state[q][k], opt.state[p][k]), k
+    for t in (1, 2):
+        for p, q, g in zip(ps, qs, all_g[t]):
+            p.grad = g.cuda()
+            q.grad = g.cuda()
+        opt.step()
+        opt2.step()
+    torch.cuda.synchronize()
+    for p, q in zip(ps, qs):
+        assert torch.equal(p.detach().view(torch.int16), q.detach().view(torch.int16))
+        for k in ("q", "scales", "m", "v", "ve"):
+            assert torch.equal(opt.state[p][k], opt2.state[q][k]), k

@@ -46,3 +46,23 @@ def test_step_without_gradients_is_a_no_op():
     assert opt.step() is None
     assert opt.step(lambda: 3.0) == 3.0
     assert not opt.state[p]
+
+
+def test_master_format_rules():
+    p = [torch.nn.Parameter(torch.zeros(128, dtype=torch.bfloat16))]
+    with pytest.raises(ValueError, match="master_format"):
+        MAdam(p, master_format="fp4")
+    with pytest.raises(ValueError, match="master_format"):
+        MAdam([{"params": p, "master_format": "e3m4"}])
+    q = torch.nn.Parameter(torch.zeros(128))
+    q.grad = torch.zeros(128)
+    with pytest.raises(TypeError, match="compute copy"):
+        MAdam([q], master_format="e4m3").step()       # the parameter holds the bf16 copy
+    r = torch.nn.Parameter(torch.zeros(100, dtype=torch.bfloat16))
+    r.grad = torch.zeros(100, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="multiple of 32"):
+        MAdam([r], master_format="mxfp4").step()
+    s = torch.nn.Parameter(torch.zeros(64, dtype=torch.bfloat16))
+    s.grad = torch.zeros(64, dtype=torch.bfloat16)
+    with pytest.raises(TypeError, match="float32"):
+        MAdam([s], master_format="nvfp4_current").step()
