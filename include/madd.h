@@ -270,6 +270,39 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream);
 
+/* Hyper-parameters read from device memory when the kernels run, so that a
+ * captured step (HIP graph) can be replayed step after step: the caller
+ * updates the device copy between replays instead of capturing again.
+ *
+ * madd_scalars_bytes(): size in bytes of the prepared scalars (the fp32
+ *   coefficients of Algorithm 2 for one step -- beta1, beta2, 1 - beta1,
+ *   1 - beta2, the bias-corrected eta_a / (1 - beta1^t) and 1 / (1 - beta2^t),
+ *   eta_m, eps, tau, g_max, the u_m clip bounds, w_max -- and the Philox key
+ *   and counter word: seed and t); the layout is internal to the library.
+ * madd_prepare_scalars(hp, out): validates hp as the step entry points do and
+ *   writes its scalars to `out` (HOST memory of madd_scalars_bytes() bytes),
+ *   computed exactly as madd_step computes them, so a step that reads them
+ *   gives the same bits as one passed hp.  MADD_EINVAL for a NULL `out` or
+ *   an invalid hp.
+ * madd_multi_tensor_step_dev(...): madd_multi_tensor_step, except that the
+ *   kernels read the scalars from `dev_scalars` (DEVICE memory, 4-byte
+ *   aligned, madd_scalars_bytes() bytes written from madd_prepare_scalars'
+ *   output) at run time.  `hp` is still validated and fixes what selects the
+ *   kernels -- the rounding mode and whether g_max / w_max are finite -- which
+ *   the prepared scalars must share; its other fields are not used.  The
+ *   caller keeps dev_scalars allocated while launches that read it are in
+ *   flight.  MADD_EINVAL for a NULL dev_scalars, MADD_EALIGN when it is not
+ *   4-byte aligned; otherwise as madd_multi_tensor_step. */
+int64_t madd_scalars_bytes(void);
+int32_t madd_prepare_scalars(const madd_hparams* hp, void* out);
+int32_t madd_multi_tensor_step_dev(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                                   void* const* scales, uint16_t* const* copy,
+                                   const void* const* g, int32_t gfmt,
+                                   void* const* m, void* const* v, void* const* ve,
+                                   int32_t sfmt, const int64_t* numel, int64_t index_base,
+                                   const madd_hparams* hp, const void* dev_scalars,
+                                   void* stream);
+
 /* One step of the moment-free update rules of Appendix B's BF16-stored
  * matrix-fitting diagnostic, on one tensor of n elements:
  *   additive        u_a = -eta_a g

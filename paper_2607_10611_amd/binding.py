@@ -34,7 +34,8 @@ STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPO
           -4: "MADD_EDEVICE", -5: "MADD_ENOMEM"}
 
 EXPORTS = ("madd_init_state", "madd_encode_weights", "madd_step", "madd_multi_tensor_step",
-           "madd_plain_step", "madd_status_string")
+           "madd_plain_step", "madd_status_string", "madd_scalars_bytes", "madd_prepare_scalars",
+           "madd_multi_tensor_step_dev")
 
 
 class MaddError(RuntimeError):
@@ -117,6 +118,14 @@ def lib():
         L.madd_plain_step.restype = I32
         L.madd_status_string.argtypes = [I32]
         L.madd_status_string.restype = ctypes.c_char_p
+        L.madd_scalars_bytes.argtypes = []
+        L.madd_scalars_bytes.restype = I64
+        L.madd_prepare_scalars.argtypes = [HP, P]
+        L.madd_prepare_scalars.restype = I32
+        L.madd_multi_tensor_step_dev.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, PP, I32,
+                                                 PP, PP, PP, I32, ctypes.POINTER(I64), I64, HP,
+                                                 P, P]
+        L.madd_multi_tensor_step_dev.restype = I32
         _lib = L
     return _lib
 
@@ -321,3 +330,30 @@ def madd_multi_tensor_step(tl: TensorList, hp, gfmt: str = "fp32", index_base: i
                                         cast(tl.g), GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve),
                                         SFMT[tl.sfmt], tl.numel, int(index_base),
                                         ctypes.byref(h), _stream(stream)))
+
+
+def prepare_scalars(hp) -> bytes:
+    """The step's hyper-parameter scalars for hp, as the bytes that
+    madd_multi_tensor_step_dev reads from device memory."""
+    h = _hp(hp)
+    buf = ctypes.create_string_buffer(int(lib().madd_scalars_bytes()))
+    _check("madd_prepare_scalars", lib().madd_prepare_scalars(ctypes.byref(h), buf))
+    return buf.raw
+
+
+def madd_multi_tensor_step_dev(tl: TensorList, hp, dev_scalars, gfmt: str = "fp32",
+                               index_base: int = 0, stream=None):
+    """madd_multi_tensor_step with the scalars read at run time from
+    ``dev_scalars`` (a GPU tensor holding prepare_scalars' bytes); ``hp``
+    selects the kernels (rounding mode, clamps)."""
+    h = _hp(hp)
+    tl.check_grads(gfmt)
+    _need("madd_multi_tensor_step_dev: dev_scalars", dev_scalars, int(lib().madd_scalars_bytes()))
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    cast = lambda a: ctypes.cast(a, PP) if a is not None else None  # noqa: E731
+    _check("madd_multi_tensor_step_dev",
+           lib().madd_multi_tensor_step_dev(tl.n, cast(tl.w), tl.wfmt, cast(tl.scales),
+                                            cast(tl.copy), cast(tl.g), GFMT[gfmt], cast(tl.m),
+                                            cast(tl.v), cast(tl.ve), SFMT[tl.sfmt], tl.numel,
+                                            int(index_base), ctypes.byref(h), _ptr(dev_scalars),
+                                            _stream(stream)))

@@ -708,7 +708,9 @@ constexpr int kStepWaves = (SF == SF_BF16 && !COPY) ? 5 : 1;
 template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_kernel(const TensorDesc* __restrict__ table,
                                                              int ntab, TensorDesc single,
-                                                             Scalars s) {
+                                                             Scalars s_arg,
+                                                             const Scalars* __restrict__ sdev) {
+  const Scalars s = sdev ? *sdev : s_arg;  // uniform: device-resident hyper-parameters
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const int64_t c0 = (chunk - d.chunk0) * kChunk;
@@ -904,7 +906,9 @@ __device__ __forceinline__ uint32_t requant_quad(Quad<WF>& q, const float (&wn)[
 
 template <int WF, int GF, int SF, bool SR, bool CLAMP, bool COPY>
 __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
-    const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s) {
+    const TensorDesc* __restrict__ table, int ntab, TensorDesc single, Scalars s_arg,
+    const Scalars* __restrict__ sdev) {
+  const Scalars s = sdev ? *sdev : s_arg;
   constexpr int kBlk = block_len<WF>();
   constexpr int kLanes = kBlk / kQuad;
   const int64_t chunk = blockIdx.x;
@@ -972,7 +976,7 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
 #if MADD_IN_PART(9)
 __global__ __launch_bounds__(kThreads) void nvcs_clear_kernel(const TensorDesc* __restrict__ table,
                                                               int ntab, TensorDesc single,
-                                                              Scalars) {
+                                                              Scalars, const Scalars*) {
   const int i = (int)(blockIdx.x * kThreads + threadIdx.x);
   if (i >= (ntab == 0 ? 1 : ntab)) return;
   void* scales = ntab == 0 ? single.scales : table[i].scales;
@@ -1014,7 +1018,9 @@ __device__ __forceinline__ uint32_t nvcs_step_quad(const TensorDesc& d, int64_t 
 template <int SF, bool CLAMP>
 __global__ __launch_bounds__(kThreads) void nvcs_pass1_kernel(const TensorDesc* __restrict__ table,
                                                               int ntab, TensorDesc single,
-                                                              Scalars s) {
+                                                              Scalars s_arg,
+                                                              const Scalars* __restrict__ sdev) {
+  const Scalars s = sdev ? *sdev : s_arg;
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float st = *(const float*)d.scales;
@@ -1064,7 +1070,9 @@ __device__ __forceinline__ void nvcs_requant(const TensorDesc& d, int64_t e, f4 
 template <bool SR, bool COPY>
 __global__ __launch_bounds__(kThreads) void nvcs_pass2_kernel(const TensorDesc* __restrict__ table,
                                                               int ntab, TensorDesc single,
-                                                              Scalars s) {
+                                                              Scalars s_arg,
+                                                              const Scalars* __restrict__ sdev) {
+  const Scalars s = sdev ? *sdev : s_arg;
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float amax_t = __uint_as_float(((const uint32_t*)d.scales)[1]);
@@ -1268,7 +1276,7 @@ __global__ __launch_bounds__(kThreads) void encode_nv_kernel(const float* __rest
 // Host side
 // ---------------------------------------------------------------------------
 
-typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars);
+typedef void (*step_fn)(const TensorDesc*, int, TensorDesc, Scalars, const Scalars*);
 
 // Kernel instantiation for (weight format, block-scaled; gradient and moment
 // formats, rounding, optional clamps present, compute copies present).
@@ -1511,10 +1519,11 @@ int32_t get_table(const std::vector<TensorDesc>& descs, TensorDesc** out) {
 }
 
 int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& single,
-               int64_t nchunks, const Scalars& s, hipStream_t stream) {
+               int64_t nchunks, const Scalars& s, const Scalars* sdev, hipStream_t stream) {
   if (nchunks <= 0) return MADD_OK;
   if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-  hipLaunchKernelGGL(fn, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab, single, s);
+  hipLaunchKernelGGL(fn, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab, single, s,
+                     sdev);
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
@@ -1522,15 +1531,16 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
 // then the two passes over the same chunks.
 int32_t launch_nvcs(const NvcsKernels& k, const TensorDesc* table, int ntab,
                     const TensorDesc& single, int64_t nchunks, const Scalars& s,
-                    hipStream_t stream) {
+                    const Scalars* sdev, hipStream_t stream) {
   if (nchunks <= 0) return MADD_OK;
   if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
   const unsigned clear_grid = (unsigned)(((ntab == 0 ? 1 : ntab) + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(k.clear, dim3(clear_grid), dim3(kThreads), 0, stream, table, ntab, single, s);
+  hipLaunchKernelGGL(k.clear, dim3(clear_grid), dim3(kThreads), 0, stream, table, ntab, single, s,
+                     sdev);
   hipLaunchKernelGGL(k.pass1, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
-                     single, s);
+                     single, s, sdev);
   hipLaunchKernelGGL(k.pass2, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
-                     single, s);
+                     single, s, sdev);
   return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
@@ -1629,6 +1639,90 @@ int32_t check_tensor(void* w, int32_t wfmt, void* scales, uint16_t* copy, const 
 // ---------------------------------------------------------------------------
 
 using namespace madd_detail;
+
+// The multi-tensor step; `sdev`, when not null, is the device copy of the
+// hyper-parameter scalars the kernels read when they run (`hp` then only
+// selects the kernels: rounding mode and whether the clamps apply).
+static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                                 void* const* scales, uint16_t* const* copy,
+                                 const void* const* g, int32_t gfmt,
+                                 void* const* m, void* const* v, void* const* ve, int32_t sfmt,
+                                 const int64_t* numel, int64_t index_base,
+                                 const madd_hparams* hp, const Scalars* sdev, void* stream) {
+  int32_t rc = check_hparams(hp);
+  if (rc != MADD_OK) return rc;
+  if (ntensors < 0 || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
+    return MADD_EINVAL;
+  if (ntensors == 0) return MADD_OK;
+  if (!w || !wfmt || !g || !m || !v || !ve || !numel) return MADD_EINVAL;
+  int64_t total = 0;
+  for (int32_t i = 0; i < ntensors; ++i) {
+    if (!valid_wfmt(wfmt[i])) return MADD_EINVAL;
+    if (wfmt[i] == MADD_W_NVFP4_CURRENT && gfmt != MADD_G_FP32 && numel[i] > 0)
+      return MADD_EINVAL;  // w' is written over the fp32 gradient
+    rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, copy ? copy[i] : nullptr, g[i],
+                      gfmt, m[i], v[i], ve[i], sfmt, numel[i]);
+    if (rc != MADD_OK) return rc;
+    if (numel[i] > INT64_MAX - index_base - total) return MADD_EINVAL;
+    total += numel[i];
+  }
+  const Scalars s = make_scalars(*hp);
+  const bool sr = hp->rounding == MADD_ROUND_SR;
+  // One launch per (format, scaled) group; global indices follow list order.
+  // All tables are prepared before the first launch.
+  struct Group {
+    step_fn fn;  // null for NVFP4 with current scaling, which launches `nvcs`
+    NvcsKernels nvcs;
+    TensorDesc* table;
+    int ntab;
+    int64_t nchunks;
+  };
+  std::vector<Group> groups;
+  for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4_CURRENT; ++wf) {
+    for (int blk = 0; blk <= 1; ++blk) {
+      std::vector<TensorDesc> descs;
+      int64_t gbase = index_base, nch = 0;
+      for (int32_t i = 0; i < ntensors; ++i) {
+        const bool is_blk = scales && scales[i];
+        if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
+          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, copy ? copy[i] : nullptr,
+                                   g[i], m[i], v[i], ve[i], numel[i], gbase);
+          d.chunk0 = nch;
+          nch += chunks_of(numel[i]);
+          descs.push_back(d);
+        }
+        gbase += numel[i];
+      }
+      if (descs.empty()) continue;
+      if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+      bool any_copy = false;
+      for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
+      step_fn fn = nullptr;
+      NvcsKernels nvcs = {nullptr, nullptr, nullptr};
+      if (wf == MADD_W_NVFP4_CURRENT) {
+        nvcs = pick_part9(sfmt, sr, needs_clamp(*hp), any_copy);
+      } else {
+        fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
+        if (!fn) return MADD_EUNSUPPORTED;
+      }
+      TensorDesc* table = nullptr;
+      rc = get_table(descs, &table);
+      if (rc != MADD_OK) return rc;
+      groups.push_back(Group{fn, nvcs, table, (int)descs.size(), nch});
+    }
+  }
+  TensorDesc none;
+  memset(&none, 0, sizeof(none));
+  for (const Group& gr : groups) {
+    rc = gr.fn ? launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, sdev,
+                        (hipStream_t)stream)
+               : launch_nvcs(gr.nvcs, gr.table, gr.ntab, none, gr.nchunks, s, sdev,
+                             (hipStream_t)stream);
+    if (rc != MADD_OK) return rc;
+  }
+  return MADD_OK;
+}
+
 
 extern "C" {
 
@@ -1752,13 +1846,13 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
     const NvcsKernels k = pick_part9(sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                                      copy != nullptr);
     const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-    return launch_nvcs(k, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
+    return launch_nvcs(k, nullptr, 0, d, chunks_of(n), s, nullptr, (hipStream_t)stream);
   }
   step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                            copy != nullptr, scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
   const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-  return launch(fn, nullptr, 0, d, chunks_of(n), s, (hipStream_t)stream);
+  return launch(fn, nullptr, 0, d, chunks_of(n), s, nullptr, (hipStream_t)stream);
 }
 
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
@@ -1798,77 +1892,32 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream) {
-  int32_t rc = check_hparams(hp);
+  return multi_tensor_step(ntensors, w, wfmt, scales, copy, g, gfmt, m, v, ve, sfmt, numel,
+                           index_base, hp, nullptr, stream);
+}
+
+int64_t madd_scalars_bytes(void) { return (int64_t)sizeof(Scalars); }
+
+int32_t madd_prepare_scalars(const madd_hparams* hp, void* out) {
+  const int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
-  if (ntensors < 0 || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
-    return MADD_EINVAL;
-  if (ntensors == 0) return MADD_OK;
-  if (!w || !wfmt || !g || !m || !v || !ve || !numel) return MADD_EINVAL;
-  int64_t total = 0;
-  for (int32_t i = 0; i < ntensors; ++i) {
-    if (!valid_wfmt(wfmt[i])) return MADD_EINVAL;
-    if (wfmt[i] == MADD_W_NVFP4_CURRENT && gfmt != MADD_G_FP32 && numel[i] > 0)
-      return MADD_EINVAL;  // w' is written over the fp32 gradient
-    rc = check_tensor(w[i], wfmt[i], scales ? scales[i] : nullptr, copy ? copy[i] : nullptr, g[i],
-                      gfmt, m[i], v[i], ve[i], sfmt, numel[i]);
-    if (rc != MADD_OK) return rc;
-    if (numel[i] > INT64_MAX - index_base - total) return MADD_EINVAL;
-    total += numel[i];
-  }
+  if (!out) return MADD_EINVAL;
   const Scalars s = make_scalars(*hp);
-  const bool sr = hp->rounding == MADD_ROUND_SR;
-  // One launch per (format, scaled) group; global indices follow list order.
-  // All tables are prepared before the first launch.
-  struct Group {
-    step_fn fn;  // null for NVFP4 with current scaling, which launches `nvcs`
-    NvcsKernels nvcs;
-    TensorDesc* table;
-    int ntab;
-    int64_t nchunks;
-  };
-  std::vector<Group> groups;
-  for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4_CURRENT; ++wf) {
-    for (int blk = 0; blk <= 1; ++blk) {
-      std::vector<TensorDesc> descs;
-      int64_t gbase = index_base, nch = 0;
-      for (int32_t i = 0; i < ntensors; ++i) {
-        const bool is_blk = scales && scales[i];
-        if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
-          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, copy ? copy[i] : nullptr,
-                                   g[i], m[i], v[i], ve[i], numel[i], gbase);
-          d.chunk0 = nch;
-          nch += chunks_of(numel[i]);
-          descs.push_back(d);
-        }
-        gbase += numel[i];
-      }
-      if (descs.empty()) continue;
-      if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-      bool any_copy = false;
-      for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
-      step_fn fn = nullptr;
-      NvcsKernels nvcs = {nullptr, nullptr, nullptr};
-      if (wf == MADD_W_NVFP4_CURRENT) {
-        nvcs = pick_part9(sfmt, sr, needs_clamp(*hp), any_copy);
-      } else {
-        fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
-        if (!fn) return MADD_EUNSUPPORTED;
-      }
-      TensorDesc* table = nullptr;
-      rc = get_table(descs, &table);
-      if (rc != MADD_OK) return rc;
-      groups.push_back(Group{fn, nvcs, table, (int)descs.size(), nch});
-    }
-  }
-  TensorDesc none;
-  memset(&none, 0, sizeof(none));
-  for (const Group& gr : groups) {
-    rc = gr.fn ? launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, (hipStream_t)stream)
-               : launch_nvcs(gr.nvcs, gr.table, gr.ntab, none, gr.nchunks, s,
-                             (hipStream_t)stream);
-    if (rc != MADD_OK) return rc;
-  }
+  memcpy(out, &s, sizeof(s));
   return MADD_OK;
+}
+
+int32_t madd_multi_tensor_step_dev(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                                   void* const* scales, uint16_t* const* copy,
+                                   const void* const* g, int32_t gfmt,
+                                   void* const* m, void* const* v, void* const* ve,
+                                   int32_t sfmt, const int64_t* numel, int64_t index_base,
+                                   const madd_hparams* hp, const void* dev_scalars,
+                                   void* stream) {
+  if (!dev_scalars) return MADD_EINVAL;
+  if (((uintptr_t)dev_scalars & 3u) != 0) return MADD_EALIGN;
+  return multi_tensor_step(ntensors, w, wfmt, scales, copy, g, gfmt, m, v, ve, sfmt, numel,
+                           index_base, hp, (const Scalars*)dev_scalars, stream);
 }
 
 }  // extern "C"

@@ -306,3 +306,34 @@ def test_scale_bytes():
     assert B.scale_bytes("mxfp4", 1024) == 32
     assert B.scale_bytes("nvfp4", 1024) == 68
     assert B.scale_bytes("nvfp4_current", 1024) == 72
+
+
+def test_prepared_scalars():
+    lib = B.lib()
+    assert lib.madd_scalars_bytes() == 64
+    ref, _h = _hp(step=5, seed=2 ** 40 + 7)
+    buf = ctypes.create_string_buffer(64)
+    assert lib.madd_prepare_scalars(ref, buf) == 0
+    import struct
+    *_f, key0, key1, t = struct.unpack("13f3I", buf.raw)
+    assert (key0, key1, t) == (7, 2 ** 8, 5)
+    assert lib.madd_prepare_scalars(ref, None) == -1
+    bad, _h2 = _hp(beta1=1.0)
+    assert lib.madd_prepare_scalars(bad, buf) == -1
+    assert lib.madd_prepare_scalars(None, buf) == -1
+
+
+@fake_addresses
+def test_device_scalars_step_rejects_bad_arguments():
+    lib = B.lib()
+    ref, _h = _hp()
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    arr = lambda *x: ctypes.cast((ctypes.c_void_p * len(x))(*x), PP)  # noqa: E731
+    fm = (ctypes.c_int32 * 1)(0)
+    ne = (ctypes.c_int64 * 1)(256)
+    w, g, m, v, ve = (arr(p) for p in (W_, G_, M_, V_, E_))
+    mt = lib.madd_multi_tensor_step_dev
+    assert mt(1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref, None, None) == -1  # no scalars
+    assert mt(1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref, S_ + 2, None) == -2  # unaligned
+    assert mt(1, w, fm, None, None, g, 0, m, v, ve, 3, ne, 0, ref, S_, None) == -1     # bad sfmt
+    assert mt(1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, None, S_, None) == -1    # no hp

@@ -3,7 +3,9 @@ table is cached (first, eager call), a call only enqueues kernels, so it can
 be captured; each replay repeats the captured step (same step counter and
 seed) on the evolving state.  Checked replay by replay against the same
 steps run eagerly on a copy, with eager work and synchronizations between
-the replays; the NVFP4 current-scaling format's three kernels included."""
+the replays; the NVFP4 current-scaling format's three kernels included.
+With madd_multi_tensor_step_dev the hyper-parameters come from device
+memory, so one capture replays successive steps."""
 import numpy as np
 import pytest
 import torch
@@ -83,3 +85,74 @@ def test_captured_step_replays_equal_eager_steps():
             for x, y in zip(a[k], b[k]):
                 if x is not None:
                     assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (r, k)
+
+
+def dev_scalars(h):
+    raw = np.frombuffer(B.prepare_scalars(h), dtype=np.uint8).copy()
+    return torch.from_numpy(raw).cuda()
+
+
+def assert_lists_equal(a, b, tag):
+    for k in ("w", "s", "c", "m", "v", "ve", "g"):
+        for x, y in zip(a[k], b[k]):
+            if x is not None:
+                assert torch.equal(x.view(torch.uint8), y.view(torch.uint8)), (tag, k)
+
+
+def test_device_scalars_give_the_bits_of_host_scalars():
+    """Eager madd_multi_tensor_step_dev steps equal madd_multi_tensor_step
+    steps, step counter and learning rate changing from step to step."""
+    a, fmts = state(5)
+    b, _ = state(5)
+    tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
+    gen = torch.Generator(device="cuda")
+    for t in range(1, 4):
+        gen.manual_seed(t)
+        for ga, gb in zip(a["g"], b["g"]):
+            ga.normal_(0, 1e-3, generator=gen)
+            gb.copy_(ga)
+        h = W.hparams("c2", step=t, lr_add=1e-3 * t, lr_mul=2e-3 / t)
+        B.madd_multi_tensor_step_dev(tla, h, dev_scalars(h))
+        B.madd_multi_tensor_step(tlb, h)
+        torch.cuda.synchronize()
+        assert_lists_equal(a, b, t)
+
+
+def test_captured_step_with_device_scalars_replays_successive_steps():
+    """One capture of madd_multi_tensor_step_dev; before each replay the
+    device scalars are rewritten for the next step (counter, learning rates),
+    and every replay equals an eager step with those hyper-parameters."""
+    a, fmts = state(6)
+    b, _ = state(6)
+    tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
+    h0 = W.hparams("c2", step=1)
+    sc = dev_scalars(h0)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    for ga, gb in zip(a["g"], b["g"]):
+        ga.normal_(0, 1e-3, generator=gen)
+        gb.copy_(ga)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        B.madd_multi_tensor_step_dev(tla, h0, sc)    # eager: caches the descriptor tables
+    torch.cuda.current_stream().wait_stream(s)
+    B.madd_multi_tensor_step(tlb, h0)
+    torch.cuda.synchronize()
+    assert_lists_equal(a, b, "eager")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        B.madd_multi_tensor_step_dev(tla, h0, sc)
+    for t in range(2, 7):
+        h = W.hparams("c2", step=t, lr_add=1e-3 / t, seed=1000 + t)
+        sc.copy_(dev_scalars(h))                     # the next step's scalars, written eagerly
+        gen.manual_seed(t)
+        for ga, gb in zip(a["g"], b["g"]):
+            ga.normal_(0, 1e-3, generator=gen)
+            gb.copy_(ga)
+        torch.cuda.synchronize()
+        graph.replay()
+        B.madd_multi_tensor_step(tlb, h)
+        torch.cuda.synchronize()
+        assert_lists_equal(a, b, t)
