@@ -60,13 +60,23 @@ class MAdam(torch.optim.Optimizer):
     its 4-bit analogues).  Each step then writes the bf16 compute copy of the
     new master weights into the parameter (until the first step the
     parameter keeps its own values).  Such parameters need a size that
-    is a multiple of the block and 16-byte-aligned storage."""
+    is a multiple of the block and 16-byte-aligned storage.
+
+    capturable: the kernels read each group's hyper-parameters from a small
+    device buffer, so that a step captured in a graph can be replayed for
+    the steps that follow.  Take at least one eager step first (it makes
+    the state and caches the launch tables), keep the gradient tensors in
+    place (write new gradients into them), and call prepare_replay() before
+    each replay: it advances the step counters and writes the next step's
+    hyper-parameters.  Every parameter of a group then needs a gradient at
+    every step, of one dtype."""
 
     def __init__(self, params, lr_add: float = 1e-3, lr_mul: float = 1e-3,
                  betas=(0.9, 0.999), eps: float = 1e-8, tau: float = 1e-8, r_max: float = 0.75,
                  eps0: float = 0.0, g_max: float = math.inf, d_mult_max: float = math.inf,
                  w_max: float = math.inf, bias_correction: bool = True, rounding: str = "sr",
-                 seed: int = 0, state_format: str = "fp32", master_format: str | None = None):
+                 seed: int = 0, state_format: str = "fp32", master_format: str | None = None,
+                 capturable: bool = False):
         if rounding not in B.ROUND:
             raise ValueError(f"rounding must be one of {sorted(B.ROUND)}, not {rounding!r}")
         if state_format not in _STATES:
@@ -82,6 +92,8 @@ class MAdam(torch.optim.Optimizer):
         self._base = {}          # parameter -> global index of its first element
         self._next_base = 0
         self._lists = OrderedDict()  # marshalled lists of recent runs (LRU)
+        self._capturable = bool(capturable)
+        self._scalars = {}       # group index -> device buffer of its prepared scalars
         super().__init__(params, defaults)
 
     @staticmethod
@@ -195,38 +207,96 @@ class MAdam(torch.optim.Optimizer):
             tl.set_grads(gs)
         return tl
 
+    @staticmethod
+    def _hparams(group, t):
+        hp = {k: group[k] for k in _HP_KEYS}
+        b1, b2 = group["betas"]
+        hp.update(beta1=b1, beta2=b2, bias_correction=int(group["bias_correction"]), step=t)
+        return hp
+
+    def _write_scalars(self, gi, group, t):
+        """The group's hyper-parameters for step t into its device buffer
+        (ordered on the current stream)."""
+        buf = self._scalars.get(gi)
+        dev = group["params"][0].device
+        if buf is None:
+            buf = self._scalars[gi] = torch.empty(int(B.lib().madd_scalars_bytes()),
+                                                  dtype=torch.uint8, device=dev)
+        raw = torch.frombuffer(bytearray(B.prepare_scalars(self._hparams(group, t))),
+                               dtype=torch.uint8)
+        buf.copy_(raw)
+        return buf
+
+    def _runs(self, group, capturing):
+        sfmt = group["state_format"]
+        master = group.get("master_format")
+        runs, cur, cur_key, end = [], None, None, None
+        for p in group["params"]:
+            if p.grad is None:
+                if self._capturable:
+                    raise ValueError("MAdam(capturable=True): every parameter of a group "
+                                     "needs a gradient at every step")
+                cur = None
+                continue
+            self._check_param(p, master)
+            if capturing and not self.state[p]:
+                raise RuntimeError("MAdam: take an eager step before capturing one")
+            st = self._state_of(p, sfmt, master)
+            key = (_GRADS[p.grad.dtype], st["step"])
+            if cur is None or key != cur_key or self._base[p] != end:
+                cur, cur_key = [], key
+                runs.append((key, cur))
+            cur.append(p)
+            end = self._base[p] + p.numel()
+        if self._capturable and len(runs) > 1:
+            raise ValueError("MAdam(capturable=True): the parameters of a group need one "
+                             "gradient dtype and one step count")
+        return runs
+
     @torch.no_grad()
     def step(self, closure=None):
         loss = None
         if closure is not None:
             with torch.enable_grad():
                 loss = closure()
-        for group in self.param_groups:
+        capturing = torch.cuda.is_available() and torch.cuda.is_current_stream_capturing()
+        if capturing and not self._capturable:
+            raise RuntimeError("MAdam: capturing a step needs MAdam(capturable=True)")
+        for gi, group in enumerate(self.param_groups):
             sfmt = group["state_format"]
             master = group.get("master_format")
-            runs, cur, cur_key, end = [], None, None, None
-            for p in group["params"]:
-                if p.grad is None:
-                    cur = None
-                    continue
-                self._check_param(p, master)
-                st = self._state_of(p, sfmt, master)
-                key = (_GRADS[p.grad.dtype], st["step"])
-                if cur is None or key != cur_key or self._base[p] != end:
-                    cur, cur_key = [], key
-                    runs.append((key, cur))
-                cur.append(p)
-                end = self._base[p] + p.numel()
-            b1, b2 = group["betas"]
-            for (gfmt, t), run in runs:
-                hp = {k: group[k] for k in _HP_KEYS}
-                hp.update(beta1=b1, beta2=b2, bias_correction=int(group["bias_correction"]),
-                          step=t + 1)
+            for (gfmt, t), run in self._runs(group, capturing):
+                hp = self._hparams(group, t + 1)
                 tl = self._marshal(run, sfmt, master)
-                B.madd_multi_tensor_step(tl, hp, gfmt=gfmt, index_base=self._base[run[0]])
+                base = self._base[run[0]]
+                if self._capturable:
+                    # captured: the replays read what prepare_replay() writes
+                    buf = self._scalars[gi] if capturing else self._write_scalars(gi, group, t + 1)
+                    B.madd_multi_tensor_step_dev(tl, hp, buf, gfmt=gfmt, index_base=base)
+                else:
+                    B.madd_multi_tensor_step(tl, hp, gfmt=gfmt, index_base=base)
                 # the launch is ordered on the current stream: the gradients
                 # need no reference past it
                 tl.set_grads([None] * tl.n)
-                for p in run:
-                    self.state[p]["step"] = t + 1
+                if not capturing:
+                    for p in run:
+                        self.state[p]["step"] = t + 1
         return loss
+
+    @torch.no_grad()
+    def prepare_replay(self):
+        """Before replaying a captured step: advance every step counter and
+        write the next step's hyper-parameters (capturable optimizers)."""
+        if not self._capturable:
+            raise RuntimeError("prepare_replay() is for MAdam(capturable=True)")
+        for gi, group in enumerate(self.param_groups):
+            steps = {self.state[p]["step"] for p in group["params"] if self.state[p]}
+            if not steps:
+                continue
+            if len(steps) > 1 or gi not in self._scalars:
+                raise RuntimeError("MAdam: prepare_replay() needs every group stepped together "
+                                   "at least once")
+            t = steps.pop() + 1
+            self._write_scalars(gi, group, t)
+            for p in group["params"]:
+                self.state[p]["step"] = t

@@ -295,3 +295,60 @@ def test_state_dict_round_trip_keeps_master_codes_and_scales():
         assert torch.equal(p.detach().view(torch.int16), q.detach().view(torch.int16))
         for k in ("q", "scales", "m", "v", "ve"):
             assert torch.equal(opt.state[p][k], opt2.state[q][k]), k
+
+
+def test_capturable_step_replays_equal_eager_steps():
+    """MAdam(capturable=True): one eager step, one captured step, then
+    prepare_replay() + replay for the following steps; every replay equals
+    an eager MAdam step on a copy (a bf16 group and an E4M3-master group)."""
+    def build(seed):
+        gen = torch.Generator().manual_seed(seed)
+        lin = [torch.nn.Parameter((torch.randn(s, generator=gen) * 0.02).to(torch.bfloat16).cuda())
+               for s in ((4, 128), (1024,))]
+        rest = [torch.nn.Parameter((torch.randn(s, generator=gen) * 0.02).to(torch.bfloat16).cuda())
+                for s in ((1000,), (33,))]
+        for p in lin + rest:
+            p.grad_dtype = None
+            p.grad = torch.zeros(p.shape, device="cuda")
+        return lin, rest
+    la, ra = build(7)
+    lb, rb = build(7)
+    groups = lambda lin, rest: [{"params": lin, "master_format": "e4m3"},  # noqa: E731
+                                {"params": rest, "lr_add": 2e-3}]
+    opt_a = MAdam(groups(la, ra), seed=31, capturable=True)
+    opt_b = MAdam(groups(lb, rb), seed=31)
+    pa, pb = la + ra, lb + rb
+
+    def new_grads(t):
+        for p, q, g in zip(pa, pb, grads(600 + t, pa, torch.float32)):
+            p.grad.copy_(g)   # in place: the captured step reads these tensors
+            q.grad.copy_(g)
+
+    def check(tag):
+        torch.cuda.synchronize()
+        for p, q in zip(pa, pb):
+            assert torch.equal(p.detach().view(torch.int16), q.detach().view(torch.int16)), tag
+            for k in ("m", "v", "ve", "q", "scales"):
+                if k in opt_a.state[p]:
+                    assert torch.equal(opt_a.state[p][k], opt_b.state[q][k]), (tag, k)
+            assert opt_a.state[p]["step"] == opt_b.state[q]["step"], tag
+
+    new_grads(1)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        opt_a.step()                    # eager: state, tables, scalars of step 1
+    torch.cuda.current_stream().wait_stream(side)
+    opt_b.step()
+    check("eager")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        opt_a.step()
+    check("after capture")              # capturing ran nothing
+    for t in range(2, 6):
+        new_grads(t)
+        opt_a.prepare_replay()
+        graph.replay()
+        opt_b.step()
+        check(f"replay t={t}")

@@ -66,3 +66,13 @@ def test_master_format_rules():
     s.grad = torch.zeros(64, dtype=torch.bfloat16)
     with pytest.raises(TypeError, match="float32"):
         MAdam([s], master_format="nvfp4_current").step()
+
+
+def test_capturable_rules():
+    p = [torch.nn.Parameter(torch.zeros(8, dtype=torch.bfloat16)) for _ in range(2)]
+    with pytest.raises(RuntimeError, match="capturable"):
+        MAdam(p).prepare_replay()
+    p[0].grad = torch.zeros(8, dtype=torch.bfloat16)   # p[1] has none
+    with pytest.raises(ValueError, match="needs a gradient"):
+        MAdam(p, capturable=True).step()
+    MAdam(p, capturable=True).prepare_replay()         # nothing stepped yet: nothing to do
