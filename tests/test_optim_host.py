@@ -72,7 +72,7 @@ def test_capturable_rules():
     p = [torch.nn.Parameter(torch.zeros(8, dtype=torch.bfloat16)) for _ in range(2)]
     with pytest.raises(RuntimeError, match="capturable"):
         MAdam(p).prepare_replay()
-    p[0].grad = torch.zeros(8, dtype=torch.bfloat16)   # p[1] has none
+    p[1].grad = torch.zeros(8, dtype=torch.bfloat16)   # p[0] has none
     with pytest.raises(ValueError, match="needs a gradient"):
         MAdam(p, capturable=True).step()
     MAdam(p, capturable=True).prepare_replay()         # nothing stepped yet: nothing to do
