@@ -154,7 +154,26 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
             "kind": "oracle",
             "sample": f"first {sample:,} parameters of the list, {done} steps cycling "
                       f"{steps} gradient sets ({dt:.1f} s on {threads} thread(s), scalar C, "
-                      "one contiguous index range per thread)"}
+                      "one contiguous index range per thread)",
+            "host": host_cpu()}
+
+
+def host_cpu() -> str:
+    """The host CPU model and how many logical CPUs this process may use."""
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return f"{model}, {n} logical CPUs available to the process"
 
 
 def main():

@@ -72,3 +72,4 @@ def test_cpu_baseline_record():
     rec = bench.cpu_baseline("c5", 1 << 12, 2, "fp32", threads=2, seconds=0.0)
     assert rec["kind"] == "oracle" and rec["unit"] == "Gparam/s" and rec["cores"] == 2
     assert rec["value"] > 0 and "2 steps" in rec["sample"]
+    assert "logical CPUs" in rec["host"]
