@@ -67,6 +67,7 @@ WORKLOAD_NAMES = {
     "c3": "llama-1.1b-shaped list (22 layers, d=2048, GQA 32/4, SwiGLU 5632, vocab 32000)",
     "c4": "llama-1.1b-shaped list in fp8 e4m3",
     "c2": "gpt2-small-shaped list (12 layers, d=768, vocab 50257)",
+    "c1": "one 1024x1024 bf16 tensor (33.6 MB per step: cache-resident, a latency figure)",
 }
 
 
@@ -124,6 +125,7 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
 
     specs = W.specs(cfg)
     wfmt = W.CONFIGS[cfg]["wfmt"]
+    sample = min(sample, W.total_params(cfg))
     xs, gs, left = [], [], sample
     for i, s in enumerate(specs):
         k = min(left, s.numel)
