@@ -111,9 +111,9 @@ class MAdam(torch.optim.Optimizer):
                 self._next_base += p.numel()
 
     def load_state_dict(self, state_dict):
-        """As torch.optim.Optimizer's, except that the moments keep the dtype
-        and bits they were saved with (the base class casts every state
-        tensor to its parameter's dtype)."""
+        """As torch.optim.Optimizer's, except that the moments and any master
+        codes and scales keep the dtype and bits they were saved with (the
+        base class casts every state tensor to its parameter's dtype)."""
         from itertools import chain
         saved = state_dict["state"]
         super().load_state_dict(state_dict)
