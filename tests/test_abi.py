@@ -337,3 +337,28 @@ def test_device_scalars_step_rejects_bad_arguments():
     assert mt(1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, ref, S_ + 2, None) == -2  # unaligned
     assert mt(1, w, fm, None, None, g, 0, m, v, ve, 3, ne, 0, ref, S_, None) == -1     # bad sfmt
     assert mt(1, w, fm, None, None, g, 0, m, v, ve, 0, ne, 0, None, S_, None) == -1    # no hp
+
+
+@pytest.mark.parametrize("kw", [dict(step=1), dict(step=37, lr_add=3e-4, lr_mul=2e-3),
+                                dict(step=5, bias_correction=0, eps0=0.05, d_mult_max=0.25,
+                                     g_max=2.0, w_max=8.0, beta1=0.8, beta2=0.95)])
+def test_prepared_scalars_follow_algorithm_2(kw):
+    """The fp32 coefficients the kernels use (Section 3.1 / Algorithm 2,
+    derived in double and rounded once), restated here from the update rule:
+    bias-corrected eta_a and 1/(1 - beta2^t), the u_m clip bounds narrowed by
+    the exponent cap 2^+-d, the Philox key and counter."""
+    import struct
+    import numpy as np
+    h = B.HParams(**kw)
+    got = struct.unpack("13f3I", B.prepare_scalars(h))
+    t = h.step
+    bc = h.bias_correction
+    sa = h.lr_add / (1 - h.beta1 ** t) if bc else h.lr_add
+    ibc2 = 1 / (1 - h.beta2 ** t) if bc else 1.0
+    lo, hi = -(h.r_max - h.eps0), h.r_max
+    if math.isfinite(h.d_mult_max):
+        lo, hi = max(lo, 2.0 ** -h.d_mult_max - 1), min(hi, 2.0 ** h.d_mult_max - 1)
+    want = [h.beta1, h.beta2, 1 - h.beta1, 1 - h.beta2, sa, ibc2, h.lr_mul, h.eps, h.tau,
+            h.g_max, lo, hi, h.w_max]
+    assert [float(np.float32(x)) for x in want] == list(got[:13])
+    assert got[13:] == (h.seed & 0xFFFFFFFF, h.seed >> 32, t)
