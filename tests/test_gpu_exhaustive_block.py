@@ -1,4 +1,5 @@
-"""The block-scale rules of the 4-bit encoders on every fp32 magnitude (GPU).
+"""The block-scale rules of the block-scaled encoders on every fp32 magnitude
+(GPU).
 
 MXFP4 (OCP MX): a block whose largest |x| is a has the shared exponent
 s = floor(log2 a) - 2 (2 = the exponent of E2M1's largest value, 6), clamped
@@ -16,7 +17,12 @@ factor is 0), for every fp32 a in [0, 2688].  torch's float8_e4m3fn cast and
 fp32 division give the reference; the division is tensor by tensor, since
 torch divides a device tensor by a Python scalar as a product with the
 rounded reciprocal, one ulp off the quotient at times (which moves a ratio
-onto an E4M3 midpoint)."""
+onto an E4M3 midpoint).
+
+Block-scaled FP8 (blocks of 128): the FP16 scale code of fp32(a / max)
+rounded to nearest-even (1.0 for a zero block, never 0 or infinity) and the
+payload of a / scale, saturating, for every finite fp32 a, in E4M3 and E5M2.
+Each reference is also checked against the oracle on a seeded sample."""
 import pytest
 import torch
 
@@ -176,3 +182,71 @@ def test_references_agree_with_the_oracle_on_a_sample():
     assert np.array_equal(code.view(torch.uint8).cpu().numpy(), sc[4:4 + a.size])
     assert np.array_equal(want_q.cpu().numpy(),
                           (q.reshape(a.size + 1, 8)[:-1, 0] & 0xF).astype(np.int64))
+
+
+FP8 = {"e4m3": (torch.float8_e4m3fn, 448.0), "e5m2": (torch.float8_e5m2, 57344.0)}
+
+
+def fp8_block_reference(a, fmt):
+    """Block-scaled FP8 of a block led by a (the rest 0): the FP16 scale
+    code of fp32(a / max) rounded to nearest-even (1.0 for a zero block, the
+    smallest subnormal instead of 0, the largest finite instead of infinity)
+    and the payload code of a / scale, saturating at the format's maximum."""
+    ft, fmax = FP8[fmt]
+    ratio = a / torch.full_like(a, fmax)
+    sc = ratio.to(torch.float16).view(torch.int16).to(torch.int64) & 0xFFFF
+    sc = torch.where(a == 0, torch.full_like(sc, 0x3C00), sc)
+    sc = torch.where(sc == 0, torch.ones_like(sc), sc)
+    sc = torch.where(sc == 0x7C00, torch.full_like(sc, 0x7BFF), sc)
+    sf = sc.to(torch.int16).view(torch.float16).to(torch.float32)
+    code = (a / sf).clamp(max=fmax).to(ft).view(torch.uint8).to(torch.int64)
+    return sc, code
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_block_fp8_scale_and_payload_of_every_fp32_magnitude(fmt):
+    per_call = 1 << 24
+    top = 0x7F800000
+    bad, examples = 0, []
+    for start in range(0, top, per_call):
+        nb = min(per_call, top - start)
+        bits = torch.arange(start, start + nb, dtype=torch.int64, device="cuda")
+        a = bits.to(torch.int32).view(torch.float32)
+        x = torch.zeros(nb, 128, device="cuda")
+        x[:, 0] = a
+        q = torch.empty(nb * 128, dtype=torch.uint8, device="cuda")
+        sc = torch.empty(nb, dtype=torch.int16, device="cuda")
+        B.madd_encode_weights(x.view(-1), q, fmt, scales=sc)
+        want_sc, want_q = fp8_block_reference(a, fmt)
+        got_sc = sc.to(torch.int64) & 0xFFFF
+        qv = q.view(nb, 128)
+        got_q = qv[:, 0].to(torch.int64)
+        rest_zero = bool((qv[:, 1:] == 0).all())
+        mism = (got_sc != want_sc) | (got_q != want_q)
+        n = int(mism.sum()) + (0 if rest_zero else 1)
+        if n and not examples:
+            i = torch.nonzero(mism)[:5, 0]
+            examples = [(hex(start + int(j)), hex(int(got_sc[j])), hex(int(want_sc[j])),
+                         int(got_q[j]), int(want_q[j])) for j in i] or ["nonzero zero element"]
+        bad += n
+        del bits, a, x, q, sc, want_sc, want_q, got_sc, qv, got_q, mism
+    assert bad == 0, f"{fmt}: {bad} magnitudes encode differently (bits, scale got/want, " \
+                     f"code got/want): {examples}"
+
+
+def test_fp8_block_reference_agrees_with_the_oracle_on_a_sample():
+    import numpy as np
+
+    import oracle
+    rng = np.random.default_rng(23)
+    bits = np.concatenate([[0, 1, 0x7FFFFF, 0x800000, 0x3F800000, 0x43E00000, 0x4B7FE000,
+                            0x7F7FFFFF], rng.integers(1, 0x7F800000, 20000)]).astype(np.int64)
+    a = bits.astype(np.uint32).view(np.float32)
+    at = torch.from_numpy(a.copy()).cuda()
+    for fmt in FP8:
+        x = np.zeros((a.size, 128), np.float32)
+        x[:, 0] = a
+        q, sc = oracle.encode_block(fmt, x.reshape(-1))
+        want_sc, want_q = fp8_block_reference(at, fmt)
+        assert np.array_equal(want_sc.cpu().numpy(), sc.astype(np.int64)), fmt
+        assert np.array_equal(want_q.cpu().numpy(), q.reshape(a.size, 128)[:, 0].astype(np.int64)), fmt
