@@ -15,7 +15,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "madd_oracle.c")
 PINS = ["tests/test_oracle_step.py", "tests/test_oracle_block.py", "tests/test_oracle_sr_rng.py",
-        "tests/test_oracle_formats.py", "tests/test_oracle_mx.py", "tests/test_oracle_nv.py"]
+        "tests/test_oracle_formats.py", "tests/test_oracle_mx.py", "tests/test_oracle_nv.py",
+        "tests/test_oracle_hypothesis.py"]
 
 MUTANTS = {
     "additive sign": ("const float ua = -((s->SA * m) / den_a);",
@@ -91,6 +92,11 @@ MUTANTS = {
     "NV current scaling keeps the old scale": (
         "  const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;\n  memcpy(scales, &stn, 4);",
         "  const float stn = st;\n  memcpy(scales, &stn, 4);"),
+    "tau replaced by eps in the relative update": (
+        "const float rho = aw > s->TAU ? aw : s->TAU;", "const float rho = aw > s->EPS ? aw : s->EPS;"),
+    "eps replaced by tau in the multiplicative denominator": (
+        "const float den_m = sqrtf(ve * s->IBC2) + s->EPS;",
+        "const float den_m = sqrtf(ve * s->IBC2) + s->TAU;"),
     "no FP8 saturation": ("if (f->satfinite && a >= f->max) return sign | f->max_code;",
                           "if (f->satfinite && a > 2 * f->max) return sign | f->max_code;"),
 }
