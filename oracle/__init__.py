@@ -107,7 +107,7 @@ def lib():
         L.oracle_encode_mx.restype = I
         L.oracle_step_nv.argtypes = [P, P, P, I, P, I, P, P, P, I64, P, I64] + hp_args
         L.oracle_step_nv.restype = I
-        L.oracle_step_nv_current.argtypes = [P, P, P, P, I, P, P, P, I64, P, I64] + hp_args
+        L.oracle_step_nv_current.argtypes = [P, P, P, P, P, I, P, P, P, I64, P, I64, P] + hp_args
         L.oracle_step_nv_current.restype = I
         L.oracle_encode_nv.argtypes = [P, P, P, I64]
         L.oracle_encode_nv.restype = I
@@ -257,39 +257,31 @@ def step_nv(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray, v: 
 def step_nv_current(q: np.ndarray, scales: np.ndarray, g: np.ndarray, m: np.ndarray,
                     v: np.ndarray, ve: np.ndarray, hp: dict, index_base: int = 0,
                     gidx: np.ndarray | None = None, sfmt: str = "fp32",
-                    copy: np.ndarray | None = None):
-    """NVFP4 step with current scaling: ``scales`` holds 8 + n/16 bytes (the
-    fp32 per-tensor scale, a word receiving the bits of the largest finite
-    |w'|, then the E4M3 block codes); the per-tensor scale is derived anew
-    from the updated tensor.  ``g`` (fp32) receives the updated weights w'."""
+                    copy: np.ndarray | None = None) -> np.ndarray:
+    """NVFP4 step with current scaling: the per-tensor scale is derived anew
+    from the updated tensor.  ``q`` and ``scales`` are NVFP4 storage as
+    ``encode_nv`` lays it out (4 + n/16 scale bytes: the fp32 per-tensor
+    scale, then the E4M3 block codes), updated in place; ``g`` (fp32) is only
+    read.  Returns the FP32 step's updated weights w' (before re-quantization)."""
     n = 2 * q.size
-    if q.dtype != np.uint8 or scales.dtype != np.uint8 or scales.size != 8 + n // 16:
-        raise OracleError("q must be n/2 packed bytes and scales 8 + n/16 bytes")
+    if q.dtype != np.uint8 or scales.dtype != np.uint8 or scales.size != 4 + n // 16:
+        raise OracleError("q must be n/2 packed bytes and scales 4 + n/16 bytes")
     if g.dtype != np.float32:
-        raise OracleError("current scaling needs fp32 gradients (they receive w')")
+        raise OracleError("current scaling takes fp32 gradients")
     _check_state(n, g, m, v, ve, "fp32", sfmt)
     if gidx is not None:
         gidx = np.ascontiguousarray(gidx, dtype=np.int64)
         assert gidx.size == n
     _check_copy(copy, n)
-    rc = lib().oracle_step_nv_current(_ptr(q), _ptr(scales), _ptr(copy), _ptr(g), SFMT[sfmt],
-                                      _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
-                                      int(index_base), *_hp_args(hp))
+    assert scales.flags.c_contiguous
+    wn = np.empty(n, np.float32)
+    codes = ctypes.c_void_p(scales.ctypes.data + 4)
+    rc = lib().oracle_step_nv_current(_ptr(q), _ptr(scales), codes, _ptr(copy), _ptr(g),
+                                      SFMT[sfmt], _ptr(m), _ptr(v), _ptr(ve), n, _ptr(gidx),
+                                      int(index_base), _ptr(wn), *_hp_args(hp))
     if rc != 0:
         raise OracleError(f"oracle_step_nv_current returned {rc}")
-
-
-def encode_nv_current(x: np.ndarray):
-    """NVFP4 encoding for the current-scaling layout: the encode_nv payloads,
-    and the scale array with a zero word between the tensor scale and the
-    block codes."""
-    q, s = encode_nv(x)
-    return q, np.concatenate([s[:4], np.zeros(4, np.uint8), s[4:]])
-
-
-def nv_current_values(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
-    """Stored weights of the current-scaling layout."""
-    return nv_values(q, np.concatenate([scales[:4], scales[8:]]))
+    return wn
 
 
 def encode_nv(x: np.ndarray):

@@ -849,48 +849,46 @@ int oracle_step_nv(uint8_t *q, uint8_t *scales, uint16_t *copy, int gfmt, const 
  * same: every w' of the tensor first (moments updated as in every step),
  * then s_t' = fp32(amax / 2688) over the finite |w'| (1 when none is
  * nonzero), then every block by the NVFP4 rule above with s_t'.
- * Layout: q n/2 bytes; scales 8 + n/16 bytes: s_t (fp32), then a word that
- * receives the bits of the tensor's largest finite |w'|, then the block
- * codes.  The gradient array (fp32 only) receives w'. */
-int oracle_step_nv_current(uint8_t *q, uint8_t *scales, uint16_t *copy, float *g, int sfmt,
-                           void *m, void *v, void *ve, int64_t n, const int64_t *gidx,
-                           int64_t index_base, double lr_add, double lr_mul, double beta1,
-                           double beta2, double eps, double tau, double r_max, double eps0,
-                           double g_max, double d_mult_max, double w_max, int bias_correction,
-                           int rounding, uint64_t seed, int64_t step) {
+ * State: q (n/2 packed payload bytes), st (4 bytes: the fp32 per-tensor
+ * scale) and codes (n/16 E4M3 block codes), all updated in place; g (fp32)
+ * is only read.  wn (n floats, output) receives the FP32 step's w' of every element,
+ * the values the re-quantization starts from. */
+int oracle_step_nv_current(uint8_t *q, uint8_t *st, uint8_t *codes, uint16_t *copy,
+                           const float *g, int sfmt, void *m, void *v, void *ve, int64_t n,
+                           const int64_t *gidx, int64_t index_base, float *wn, double lr_add,
+                           double lr_mul, double beta1, double beta2, double eps, double tau,
+                           double r_max, double eps0, double g_max, double d_mult_max,
+                           double w_max, int bias_correction, int rounding, uint64_t seed,
+                           int64_t step) {
   init_formats();
   ohp h;
   if (fill_hp(&h, lr_add, lr_mul, beta1, beta2, eps, tau, r_max, eps0, g_max, d_mult_max,
               w_max, bias_correction, rounding, seed, step) != ORACLE_OK)
     return ORACLE_EINVAL;
   if (sfmt != OS_FP32 && sfmt != OS_BF16 && sfmt != OS_BF16_SR) return ORACLE_EINVAL;
-  if (n < 0 || n % NV_BLOCK != 0) return ORACLE_EINVAL;
+  if (n < 0 || n % NV_BLOCK != 0 || !st || !wn) return ORACLE_EINVAL;
   oscal s;
   make_scalars(&h, &s);
-  const float st = nv_get_st(scales);
-  uint8_t *codes = scales + 8;
-  /* the FP32 step on every dequantized weight; w' replaces the gradient */
+  const float sto = nv_get_st(st);
+  /* the FP32 step on every dequantized weight */
   float amax = 0.0f;
   for (int64_t i = 0; i < n; ++i) {
-    const float wv = (float)decode(OF_E2M1, mx_get(q, i)) * nv_den(codes[i / NV_BLOCK], st);
-    const float wn = step_stored(wv, g[i], sfmt, m, v, ve, i, &s, &h,
-                                 gidx ? gidx[i] : index_base + i);
-    g[i] = wn;
-    if (isfinite(wn) && fabsf(wn) > amax) amax = fabsf(wn);
+    const float wv = (float)decode(OF_E2M1, mx_get(q, i)) * nv_den(codes[i / NV_BLOCK], sto);
+    wn[i] = step_stored(wv, g[i], sfmt, m, v, ve, i, &s, &h, gidx ? gidx[i] : index_base + i);
+    if (isfinite(wn[i]) && fabsf(wn[i]) > amax) amax = fabsf(wn[i]);
   }
   /* the new per-tensor scale, then every block with it */
   const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;
-  memcpy(scales, &stn, 4);
-  memcpy(scales + 4, &amax, 4);
+  memcpy(st, &stn, 4);
   for (int64_t b = 0; b < n / NV_BLOCK; ++b) {
-    const float *wn = g + b * NV_BLOCK;
-    const uint32_t c = nv_block_code(wn, stn);
+    const float *wb = wn + b * NV_BLOCK;
+    const uint32_t c = nv_block_code(wb, stn);
     const float den = nv_den(c, stn);
     for (int k = 0; k < NV_BLOCK; ++k) {
       const int64_t i = b * NV_BLOCK + k;
       const int64_t idx = gidx ? gidx[i] : index_base + i;
       const uint32_t r16 = (h.rounding == OR_SR) ? draw16(h.seed, h.step, 0u, idx) : 0u;
-      const uint32_t pc = nv_payload(wn[k], c, den, h.rounding, r16);
+      const uint32_t pc = nv_payload(wb[k], c, den, h.rounding, r16);
       mx_put(q, i, pc);
       if (copy) copy[i] = compute_copy((float)decode(OF_E2M1, pc) * den);
     }
@@ -899,7 +897,6 @@ int oracle_step_nv_current(uint8_t *q, uint8_t *scales, uint16_t *copy, float *g
   return ORACLE_OK;
 }
 
-/* NVFP4 encoding of fp32 values (nearest-even), per-tensor scale included. */
 int oracle_encode_nv(const float *x, uint8_t *q, uint8_t *scales, int64_t n) {
   init_formats();
   if (n < 0 || n % NV_BLOCK != 0) return ORACLE_EINVAL;

@@ -94,13 +94,48 @@ class HostState:
         self.scales = scales.copy() if scales is not None else None
 
 
+# NVFP4 with current scaling, device layout: the kernels' scale array holds
+# the fp32 tensor scale, a 4-byte word in which pass 1 gathers the largest
+# finite |w'| of the tensor, then the E4M3 block codes; pass 1 also writes w'
+# over the fp32 gradient buffer.  The oracle keeps NVFP4 storage as the
+# format defines it (tensor scale, block codes) and returns w'; these helpers
+# map one onto the other on the test side.
+
+def nvcs_device_scales(s_nv: np.ndarray, amax_bits: int = 0) -> np.ndarray:
+    """Device scale array from NVFP4 storage (4 + n/16 bytes) and an amax word."""
+    word = np.array([amax_bits], np.uint32).view(np.uint8)
+    return np.concatenate([s_nv[:4], word, s_nv[4:]])
+
+
+def nvcs_storage_scales(s_dev: np.ndarray) -> np.ndarray:
+    """NVFP4 storage (tensor scale, block codes) from a device scale array."""
+    return np.concatenate([s_dev[:4], s_dev[8:]])
+
+
+def encode_nv_current(x: np.ndarray):
+    """The oracle's NVFP4 encoding in the device layout (amax word zero)."""
+    q, s = oracle.encode_nv(x)
+    return q, nvcs_device_scales(s)
+
+
+def finite_amax_bits(wn: np.ndarray) -> int:
+    """Bits of the largest finite |w'| (0 when there is none)."""
+    fin = np.abs(wn[np.isfinite(wn)]).astype(np.float32)
+    return int(fin.max().view(np.uint32)) if fin.size else 0
+
+
 def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None):
-    """One oracle step on hs.  For nvfp4_current, g (fp32) receives w' as the
-    device's gradient buffer does."""
+    """One oracle step on hs.  For nvfp4_current hs.scales is in the device
+    layout: the oracle steps the storage part, and the test side writes the
+    amax word of the returned w' and, as the device's pass 1 does, w' over
+    g (fp32)."""
     if wfmt == "nvfp4_current":
         assert gfmt == "fp32"
-        oracle.step_nv_current(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, index_base=index_base,
-                               gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
+        s_nv = nvcs_storage_scales(hs.scales)
+        wn = oracle.step_nv_current(hs.w, s_nv, g, hs.m, hs.v, hs.ve, hp, index_base=index_base,
+                                    gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
+        hs.scales = nvcs_device_scales(s_nv, finite_amax_bits(wn))
+        g[:] = wn
     elif wfmt == "mxfp4":
         oracle.step_mx(hs.w, hs.scales, g, hs.m, hs.v, hs.ve, hp, gfmt=gfmt,
                        index_base=index_base, gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)

@@ -13,6 +13,7 @@ import torch
 import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
+from gpu_parity_util import encode_nv_current
 
 pytestmark = pytest.mark.gpu
 
@@ -36,7 +37,7 @@ def state(seed):
             st["s"].append(None)
             st["c"].append(None)
         else:
-            q, s = oracle.encode_nv_current(x) if f == "nvfp4_current" else oracle.encode_nv(x)
+            q, s = encode_nv_current(x) if f == "nvfp4_current" else oracle.encode_nv(x)
             st["w"].append(torch.from_numpy(q).cuda())
             st["s"].append(torch.from_numpy(s).cuda())
             st["c"].append(torch.zeros(n, dtype=torch.int16, device="cuda"))

@@ -1,9 +1,12 @@
 """Parity of the HIP step on NVFP4 storage with current scaling (the
 per-tensor scale derived anew from the updated tensor every step: clear,
-pass 1, pass 2) with the CPU oracle, through the C ABI.  Bar: payload bytes,
-the whole scale array (tensor scale, amax word, block codes), the gradient
-buffer (which receives w') and bf16 compute copies bit-exact; fp32 moments
-within 2 ulp; bf16 moment codes bit-exact.
+pass 1, pass 2) with the CPU oracle, through the C ABI.  The oracle returns
+w' and the new NVFP4 storage (tensor scale, block codes); the device's
+buffers are compared with them: payload bytes, tensor scale and block codes
+bit-exact, the gradient buffer (pass 1 writes w' over it) bit-exact against
+the returned w', the amax word against the largest finite |w'|, bf16
+compute copies bit-exact; fp32 moments within 2 ulp; bf16 moment codes
+bit-exact.
 """
 import numpy as np
 import pytest
@@ -13,10 +16,14 @@ import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
 from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
-                             free_device_bytes, gpu_step, oracle_step, to_dev, to_host, ulp_dist)
+                             encode_nv_current, free_device_bytes, gpu_step, oracle_step, to_dev,
+                             to_host, ulp_dist)
 from test_oracle_nv import e4m3_code
 
 pytestmark = pytest.mark.gpu
+# steps of the full 7B master-weight list (Algorithm 1 changes its bias
+# corrections and draws with t)
+MASTER_STEPS = 10
 FMT = "nvfp4_current"
 
 
@@ -52,7 +59,7 @@ def grad(rng, n):
 
 
 def encode_both(x):
-    q_ref, s_ref = oracle.encode_nv_current(x)
+    q_ref, s_ref = encode_nv_current(x)
     q = torch.empty(x.size // 2, dtype=torch.uint8, device="cuda")
     s = torch.full((8 + x.size // 16,), 0xAB, dtype=torch.uint8, device="cuda")
     B.madd_encode_weights(torch.from_numpy(x).cuda(), q, FMT, scales=s)
@@ -236,7 +243,7 @@ def test_nvfp4_current_master_llama7b_sampled():
     tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
                       scales=dev["sc"], copies=dev["cp"])
     hm = [None] * len(specs)
-    for t in (1, 2):
+    for t in range(1, MASTER_STEPS + 1):
         # the sampled old weights and gradients, before the step
         before = []
         for i, (idx, idx_t, bidx) in enumerate(samples):

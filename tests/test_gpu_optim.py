@@ -14,7 +14,7 @@ import torch
 import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd.optim import MAdam
-from gpu_parity_util import HostState, assert_state_equal, oracle_step, to_host
+from gpu_parity_util import HostState, assert_state_equal, encode_nv_current, oracle_step, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -215,7 +215,7 @@ def oracle_master(fmt, x):
     if fmt in ("e4m3", "e5m2"):
         return oracle.encode_block(fmt, x)
     return {"mxfp4": oracle.encode_mx, "nvfp4": oracle.encode_nv,
-            "nvfp4_current": oracle.encode_nv_current}[fmt](x)
+            "nvfp4_current": encode_nv_current}[fmt](x)
 
 
 @pytest.mark.parametrize("master", ["e4m3", "e5m2", "mxfp4", "nvfp4", "nvfp4_current"])

@@ -14,7 +14,7 @@ import oracle
 from paper_2607_10611_amd import binding as B
 from paper_2607_10611_amd import workloads as W
 from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_state_equal,
-                             gpu_step, oracle_step, to_dev, to_host)
+                             encode_nv_current, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -66,7 +66,7 @@ def encode(wfmt, kind, x):
         return oracle.encode_mx(x)
     if kind == "nv":
         return oracle.encode_nv(x)
-    return oracle.encode_nv_current(x)
+    return encode_nv_current(x)
 
 
 @pytest.mark.parametrize("case", range(160))

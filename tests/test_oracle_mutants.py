@@ -87,11 +87,11 @@ MUTANTS = {
     "NV NaN block payload": ("if (code == 0x7Fu || den == 0.0f) return 0u;",
                              "if (code == 0x7Fu || den == 0.0f) return 7u;"),
     "NV current scale over non-finite values too": (
-        "    if (isfinite(wn) && fabsf(wn) > amax) amax = fabsf(wn);",
-        "    if (fabsf(wn) > amax) amax = fabsf(wn);"),
+        "    if (isfinite(wn[i]) && fabsf(wn[i]) > amax) amax = fabsf(wn[i]);",
+        "    if (fabsf(wn[i]) > amax) amax = fabsf(wn[i]);"),
     "NV current scaling keeps the old scale": (
-        "  const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;\n  memcpy(scales, &stn, 4);",
-        "  const float stn = st;\n  memcpy(scales, &stn, 4);"),
+        "  const float stn = amax > 0.0f ? amax / 2688.0f : 1.0f;\n  memcpy(st, &stn, 4);",
+        "  const float stn = sto;\n  memcpy(st, &stn, 4);"),
     "tau replaced by eps in the relative update": (
         "const float rho = aw > s->TAU ? aw : s->TAU;", "const float rho = aw > s->EPS ? aw : s->EPS;"),
     "eps replaced by tau in the multiplicative denominator": (

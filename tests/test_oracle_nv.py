@@ -205,8 +205,7 @@ def test_nv_zero_learning_rates_keep_blocks_whose_largest_payload_is_six():
 # --------------------------------------------------------------------------
 
 def _cs_setup(rng, n, scale=0.05):
-    q, s = oracle.encode_nv_current(rng.normal(0, scale, n).astype(np.float32))
-    return q, s
+    return oracle.encode_nv(rng.normal(0, scale, n).astype(np.float32))
 
 
 @pytest.mark.parametrize("rounding", ["rne", "sr"])
@@ -220,19 +219,19 @@ def test_current_scaling_is_fp32_step_then_encoding_with_the_new_tensor_scale(ro
         g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-5, -1, n)).astype(np.float32)
         h = hp(step=t, lr_add=3e-2, lr_mul=3e-2, rounding=rounding, seed=12)
         # w' by the unscaled FP32 step on the stored values (an independent path)
-        codes32 = oracle.nv_current_values(q, s).view(np.uint32).copy()
+        codes32 = oracle.nv_values(q, s).view(np.uint32).copy()
         oracle.step("fp32", codes32, g.copy(), *z2, h)
         wn = codes32.view(np.float32)
         gg = g.copy()
-        oracle.step_nv_current(q, s, gg, *z1, h)
-        assert gg.tobytes() == wn.tobytes()                        # g receives w'
+        got_wn = oracle.step_nv_current(q, s, gg, *z1, h)
+        assert got_wn.tobytes() == wn.tobytes()                    # w' returned
+        assert gg.tobytes() == g.tobytes()                         # g only read
         fin = wn[np.isfinite(wn)]
         amax = np.float32(np.abs(fin).max())
         st = np.float32(amax / np.float32(2688.0))
-        assert np.frombuffer(s[:4].tobytes(), np.float32)[0] == st
-        assert np.frombuffer(s[4:8].tobytes(), np.float32)[0] == amax
+        assert tensor_scale(s) == st
         codes, pay = reference_blocks(wn, st)
-        assert (s[8:] == codes).all()
+        assert (s[4:] == codes).all()
         got = oracle.unpack_e2m1(q)
         if rounding == "rne":
             assert (got == pay).all()
@@ -258,53 +257,50 @@ def test_current_scaling_follows_growing_weights():
     rng = np.random.default_rng(26)
     n = 32 * 16
     x = rng.normal(0, 0.05, n).astype(np.float32)
-    qc, sc = oracle.encode_nv_current(x)
+    qc, sc = oracle.encode_nv(x)
     qf, sf = oracle.encode_nv(x)
     zc = [np.zeros(n, np.float32) for _ in range(3)]
     zf = [np.zeros(n, np.float32) for _ in range(3)]
     g0 = -np.sign(x).astype(np.float32) * 1e-2
     for t in range(1, 30):
         h = hp(step=t, lr_add=0.0, lr_mul=0.5, r_max=0.75, rounding="rne")
-        oracle.step_nv_current(qc, sc, g0.copy(), *zc, h)
+        oracle.step_nv_current(qc, sc, g0, *zc, h)
         oracle.step_nv(qf, sf, g0, *zf, h)
-    assert np.frombuffer(sc[:4].tobytes(), np.float32)[0] > 50 * tensor_scale(sf)
+    assert tensor_scale(sc) > 50 * tensor_scale(sf)
     assert (sf[4:] == 0x7E).mean() > 0.5            # fixed scale: block codes saturated
-    assert (sc[8:] == 0x7E).mean() < 0.2
+    assert (sc[4:] == 0x7E).mean() < 0.2
 
 
 def test_current_scaling_special_cases():
     rng = np.random.default_rng(27)
     n = 8 * 16
     # everything zero: the scale falls back to 1
-    q, s = oracle.encode_nv_current(np.zeros(n, np.float32))
+    q, s = oracle.encode_nv(np.zeros(n, np.float32))
     z = [np.zeros(n, np.float32) for _ in range(3)]
-    oracle.step_nv_current(q, s, np.zeros(n, np.float32), *z, hp())
-    assert np.frombuffer(s[:4].tobytes(), np.float32)[0] == 1.0 and (q == 0).all()
+    wn = oracle.step_nv_current(q, s, np.zeros(n, np.float32), *z, hp())
+    assert tensor_scale(s) == 1.0 and (q == 0).all() and (wn == 0).all()
     # a non-finite gradient: its block takes the NaN code, the scale comes
     # from the finite values
     q, s = _cs_setup(rng, n)
     g = rng.normal(0, 1e-3, n).astype(np.float32)
     g[37] = np.inf
-    gg = g.copy()
     z = [np.zeros(n, np.float32) for _ in range(3)]
-    oracle.step_nv_current(q, s, gg, *z, hp())
-    assert not np.isfinite(gg[37]) and s[8 + 37 // 16] == 0x7F
-    fin = gg[np.isfinite(gg)]
-    assert np.frombuffer(s[:4].tobytes(), np.float32)[0] == np.float32(
-        np.float32(np.abs(fin).max()) / np.float32(2688.0))
+    wn = oracle.step_nv_current(q, s, g, *z, hp())
+    assert not np.isfinite(wn[37]) and s[4 + 37 // 16] == 0x7F
+    fin = wn[np.isfinite(wn)]
+    assert tensor_scale(s) == np.float32(np.float32(np.abs(fin).max()) / np.float32(2688.0))
     # an update that overflows to infinity from finite inputs: that block
     # takes the NaN code and the infinity does not enter the scale
     x = rng.normal(0, 1e36, n).astype(np.float32)
     x[5] = 3.0e38
-    q, s = oracle.encode_nv_current(x)
+    q, s = oracle.encode_nv(x)
     g = (-np.sign(x) * 1e-3).astype(np.float32)   # the additive step grows every |w|
-    gg = g.copy()
     z = [np.zeros(n, np.float32) for _ in range(3)]
     # without bias correction u_a = -eta_a m / sqrt(v) = 0.1 / sqrt(0.001) eta_a = 9.5e37
-    oracle.step_nv_current(q, s, gg, *z, hp(lr_add=3e37, lr_mul=0.0, bias_correction=0))
-    assert np.isinf(gg).any() and s[8 + 5 // 16] == 0x7F
-    fin = gg[np.isfinite(gg)]
-    assert np.frombuffer(s[4:8].tobytes(), np.float32)[0] == np.float32(np.abs(fin).max())
+    wn = oracle.step_nv_current(q, s, g, *z, hp(lr_add=3e37, lr_mul=0.0, bias_correction=0))
+    assert np.isinf(wn).any() and s[4 + 5 // 16] == 0x7F
+    fin = wn[np.isfinite(wn)]
+    assert tensor_scale(s) == np.float32(np.float32(np.abs(fin).max()) / np.float32(2688.0))
 
 
 def test_current_scaling_keys_by_global_index():
@@ -314,18 +310,18 @@ def test_current_scaling_keys_by_global_index():
     g = rng.normal(0, 1e-2, n).astype(np.float32)
     outs = []
     for kw in (dict(index_base=512), dict(gidx=512 + np.arange(n))):
-        q, s = oracle.encode_nv_current(x)
+        q, s = oracle.encode_nv(x)
         z = [np.zeros(n, np.float32) for _ in range(3)]
-        oracle.step_nv_current(q, s, g.copy(), *z, hp(rounding="sr", seed=3, lr_add=1e-2), **kw)
+        oracle.step_nv_current(q, s, g, *z, hp(rounding="sr", seed=3, lr_add=1e-2), **kw)
         outs.append((q.copy(), s.copy()))
     assert (outs[0][0] == outs[1][0]).all() and (outs[0][1] == outs[1][1]).all()
 
 
 def test_current_scaling_validation():
     z = [np.zeros(32, np.float32) for _ in range(3)]
-    with pytest.raises(oracle.OracleError):   # 4-byte header is the fixed-scale layout
-        oracle.step_nv_current(np.zeros(16, np.uint8), np.zeros(6, np.uint8),
+    with pytest.raises(oracle.OracleError):   # scale array of the wrong size
+        oracle.step_nv_current(np.zeros(16, np.uint8), np.zeros(10, np.uint8),
                                np.zeros(32, np.float32), *z, hp())
     with pytest.raises(oracle.OracleError):   # gradients must be fp32
-        oracle.step_nv_current(np.zeros(16, np.uint8), np.zeros(10, np.uint8),
+        oracle.step_nv_current(np.zeros(16, np.uint8), np.zeros(6, np.uint8),
                                np.zeros(32, np.uint16), *z, hp())
