@@ -31,9 +31,12 @@
  *     pointers owned by the caller.  Pointer arrays, numel arrays and the
  *     hyper-parameter struct are HOST memory, read during the call only.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *     Work is enqueued asynchronously on it; no call synchronizes the host
- *     except madd_multi_tensor_step the first time it sees a given tensor
- *     list (it uploads a descriptor table; see that function).
+ *     Work is enqueued asynchronously on it; no call synchronizes the
+ *     device.  The only host waits and device allocations are those of
+ *     madd_multi_tensor_step's descriptor-table cache (see that function).
+ *   - A failed launch is reported as MADD_EDEVICE from the launch's own
+ *     return status; the calling thread's HIP last-error state is neither
+ *     read nor cleared.
  *   - Updates are in place on w, m, v, ve and scales; g is read-only
  *     (except for NVFP4_CURRENT tensors, whose step writes w' over g).
  *     Buffers must not alias each other: each call checks that the byte
@@ -63,7 +66,9 @@ typedef enum madd_status {
   MADD_EALIGN = -2,      /* block-scaled buffers not 16-byte aligned          */
   MADD_EUNSUPPORTED = -3,/* valid request the library does not implement      */
   MADD_EDEVICE = -4,     /* a HIP runtime call or kernel launch failed         */
-  MADD_ENOMEM = -5       /* device allocation for the descriptor table failed  */
+  MADD_ENOMEM = -5,      /* device allocation for the descriptor table failed  */
+  MADD_ECAPTURE = -6     /* a multi-tensor list seen for the first time while
+                            its stream is capturing a graph                    */
 } madd_status;
 
 /* Weight storage formats.
@@ -257,12 +262,27 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
  * layers (or MXFP4 / NVFP4 ones) with BF16 embeddings, norms and head, the paper's
  * FP8-master (4-bit-master) setting (Section 4.2).  Tensor i's elements have global
  * indices index_base + sum_{j<i} numel[j] + local index.
- * The first call with a given list (same pointers and sizes) uploads a device
- * descriptor table (88 bytes per tensor) with a synchronous copy and caches it
- * (up to 32 lists per process; evicting one drains the device first).  Later
- * calls with the same list enqueue only the kernels, so such a call can be
- * captured into a HIP graph (no call records a memset); the hyper-parameters,
- * step counter included, are kernel arguments fixed at capture. */
+ * Descriptor tables.  The kernels read a device table of the list (88 bytes
+ * per tensor: pointers, sizes, index bases) that the library caches by
+ * content, per device:
+ *   - The first call with a given list (same pointers and sizes) allocates
+ *     the table's device memory (hipMalloc) and writes it on `stream` with a
+ *     small kernel (asynchronous); later calls with the same list enqueue
+ *     only the step kernels.
+ *   - At most 32 lists per device are cached besides pinned ones.  A new list
+ *     past that recycles the least recently used table: the host waits for
+ *     the last launch that read it (an event recorded after that launch, not
+ *     a device-wide synchronization), then reuses its memory, or frees it
+ *     when too small for the new list.
+ *   - Graph capture.  A call made while `stream` is capturing a graph only
+ *     enqueues kernels, and its tables are pinned: never recycled or freed
+ *     until the process ends, so every replay of the graph reads a live,
+ *     unchanged table.  A list must have been stepped once outside the
+ *     capture; a list first seen during a capture returns MADD_ECAPTURE and
+ *     enqueues nothing (no allocation or upload inside a capture).  No call
+ *     records a memset.  The hyper-parameters, step counter included, are
+ *     kernel arguments fixed at capture (see madd_multi_tensor_step_dev for
+ *     replaying successive steps). */
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,
                                void* const* scales, uint16_t* const* copy,
                                const void* const* g, int32_t gfmt,

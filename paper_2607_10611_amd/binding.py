@@ -31,7 +31,7 @@ SFMT = {"fp32": S_FP32, "bf16": S_BF16, "bf16_sr": S_BF16_SR}
 ROUND = {"rne": ROUND_RNE, "sr": ROUND_SR}
 
 STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPORTED",
-          -4: "MADD_EDEVICE", -5: "MADD_ENOMEM"}
+          -4: "MADD_EDEVICE", -5: "MADD_ENOMEM", -6: "MADD_ECAPTURE"}
 
 EXPORTS = ("madd_init_state", "madd_encode_weights", "madd_step", "madd_multi_tensor_step",
            "madd_plain_step", "madd_status_string", "madd_scalars_bytes", "madd_prepare_scalars",

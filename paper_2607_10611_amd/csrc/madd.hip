@@ -43,9 +43,12 @@
 #include <string.h>
 
 #include <mutex>
+#include <tuple>
+#include <utility>
 #include <vector>
 
 #include "madd.h"
+#include "table_cache.h"
 
 // The library is built from this one source compiled as several parts
 // (-DMADD_PART=k, in parallel): part 0 holds the host code, the ABI and the
@@ -65,7 +68,12 @@ constexpr int kQuad = 4;                     // consecutive elements per thread 
 constexpr int kSub = kThreads * kQuad;       // 1024 elements per sub-tile
 constexpr int kTile = 2 * kSub;              // sub-tiles A and B
 constexpr int kTilesPerChunk = 1;
-constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
+[[maybe_unused]] constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
+// Launches of fewer chunks than this (fewer than 16 workgroups per CU) give
+// each workgroup one sub-tile instead of two: twice the workgroups, each
+// thread one quad, so that one wave's arithmetic overlaps other waves'
+// memory traffic when there is too little work to hide it otherwise.
+[[maybe_unused]] constexpr int64_t kSmallLaunchChunks = 4096;
 constexpr int kBlock = 128;                  // block-scaled FP8 block length
 constexpr int kMxBlock = 32;                 // MXFP4 block length (OCP MX)
 constexpr int kNvBlock = 16;                 // NVFP4 block length
@@ -98,7 +106,7 @@ struct TensorDesc {
   int64_t gbase;   // global index of element 0
   int64_t chunk0;  // first chunk of this tensor within the launch
   int32_t vec_ok;  // buffers 16-byte aligned and gbase a multiple of 8
-  int32_t pad;
+  int32_t chunk_len;  // elements per chunk: kChunk, or kSub for small launches
 };
 
 typedef float f4 __attribute__((ext_vector_type(4)));
@@ -713,8 +721,8 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
   const Scalars s = sdev ? *sdev : s_arg;  // uniform: device-resident hyper-parameters
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
-  const int64_t c0 = (chunk - d.chunk0) * kChunk;
-  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
+  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
     const int64_t tb = c0 + (int64_t)tile * kTile;
@@ -914,8 +922,8 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float st = WF == WF_NVFP4 ? *(const float*)d.scales : 1.0f;  // NVFP4 tensor scale
-  const int64_t c0 = (chunk - d.chunk0) * kChunk;
-  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
+  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
     const int64_t tb = c0 + (int64_t)tile * kTile;
@@ -1024,8 +1032,8 @@ __global__ __launch_bounds__(kThreads) void nvcs_pass1_kernel(const TensorDesc* 
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float st = *(const float*)d.scales;
-  const int64_t c0 = (chunk - d.chunk0) * kChunk;
-  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
+  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
   const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
   MDraws mA, mB;
   if (d.vec_ok) {  // uniform: index base a multiple of 8
@@ -1078,8 +1086,8 @@ __global__ __launch_bounds__(kThreads) void nvcs_pass2_kernel(const TensorDesc* 
   const float amax_t = __uint_as_float(((const uint32_t*)d.scales)[1]);
   const float st = amax_t > 0.0f ? amax_t / 2688.0f : 1.0f;
   if (chunk == d.chunk0 && threadIdx.x == 0) *(float*)d.scales = st;  // pass 2 reads only the amax word
-  const int64_t c0 = (chunk - d.chunk0) * kChunk;
-  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
+  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
   const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
   const bool actA = eA < cend, actB = eB < cend;  // whole lane groups of a block agree
   f4 wa = f4{0.0f, 0.0f, 0.0f, 0.0f}, wb = wa;
@@ -1467,54 +1475,96 @@ Scalars make_scalars(const madd_hparams& hp) {
   return s;
 }
 
-int64_t chunks_of(int64_t n) { return (n + kChunk - 1) / kChunk; }
+int64_t chunks_of(int64_t n, int64_t len = kChunk) { return (n + len - 1) / len; }
 
-// Device descriptor tables, cached by content.
-struct TableEntry {
-  int device;
-  std::vector<TensorDesc> host;
-  TensorDesc* dev;
-  uint64_t last_use;
+// Chunk length of a launch over `total` elements' worth of chunks: the
+// half-size chunk when the full-size ones would leave the CUs short of
+// workgroups (the results do not depend on it: every draw is keyed by the
+// element's global index).
+int32_t chunk_len_for(int64_t full_chunks) {
+  return full_chunks < kSmallLaunchChunks ? (int32_t)kSub : (int32_t)kChunk;
+}
+
+// Kernel launch that reports the launch's own status.  hipLaunchKernel
+// returns it directly, so the thread's last-error state, which belongs to
+// the caller, is neither read nor cleared.
+template <typename Tuple, size_t... I>
+void kernel_argv(void** argv, Tuple& t, std::index_sequence<I...>) {
+  ((argv[I] = (void*)&std::get<I>(t)), ...);
+}
+template <typename... P, typename... A>
+int32_t launch_k(void (*k)(P...), dim3 grid, dim3 block, hipStream_t stream, A&&... a) {
+  std::tuple<P...> args(std::forward<A>(a)...);
+  void* argv[sizeof...(P) > 0 ? sizeof...(P) : 1];
+  kernel_argv(argv, args, std::index_sequence_for<P...>{});
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, argv, 0, stream) ==
+                 hipSuccess
+             ? MADD_OK
+             : MADD_EDEVICE;
+}
+
+// Device tables are written by a kernel that carries the bytes in its
+// arguments: stream-ordered, asynchronous, free of host-memory lifetimes
+// (the arguments are copied at launch) and recordable in a graph.
+constexpr int kFillWords = 352;  // 16 descriptors of 88 bytes per launch
+constexpr int kFillThreads = 384;
+struct FillArgs {
+  uint32_t nwords;
+  uint32_t word[kFillWords];
 };
-std::mutex g_mu;
-std::vector<TableEntry> g_tables;
-uint64_t g_clock = 0;
-constexpr size_t kMaxTables = 32;
+static_assert(sizeof(TensorDesc) == 88, "descriptor layout");
+static_assert(sizeof(TensorDesc) % 4 == 0, "descriptors are whole words");
 
-int32_t get_table(const std::vector<TensorDesc>& descs, TensorDesc** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return MADD_EDEVICE;
-  std::lock_guard<std::mutex> lock(g_mu);
-  ++g_clock;
-  const size_t bytes = descs.size() * sizeof(TensorDesc);
-  for (auto& t : g_tables) {
-    if (t.device == dev && t.host.size() == descs.size() &&
-        memcmp(t.host.data(), descs.data(), bytes) == 0) {
-      t.last_use = g_clock;
-      *out = t.dev;
-      return MADD_OK;
-    }
+__global__ __launch_bounds__(kFillThreads) void table_fill_kernel(uint32_t* dst, FillArgs a) {
+  const uint32_t i = threadIdx.x;
+  if (i < a.nwords) dst[i] = a.word[i];
+}
+
+// Copy `bytes` (a multiple of 4) from host memory to device memory `dst`
+// on `stream`.
+int32_t fill_device(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  const uint32_t* w = (const uint32_t*)src;
+  const size_t nw = bytes / 4;
+  for (size_t off = 0; off < nw; off += kFillWords) {
+    FillArgs a;
+    a.nwords = (uint32_t)(nw - off < (size_t)kFillWords ? nw - off : (size_t)kFillWords);
+    memcpy(a.word, w + off, a.nwords * 4u);
+    const int32_t rc = launch_k(table_fill_kernel, dim3(1), dim3(kFillThreads), stream,
+                                (uint32_t*)dst + off, a);
+    if (rc != MADD_OK) return rc;
   }
-  if (g_tables.size() >= kMaxTables) {
-    size_t victim = 0;
-    for (size_t i = 1; i < g_tables.size(); ++i)
-      if (g_tables[i].last_use < g_tables[victim].last_use) victim = i;
-    int cur = dev;
-    if (hipSetDevice(g_tables[victim].device) != hipSuccess) return MADD_EDEVICE;
-    // A launch still in flight may read the table: drain the device first.
-    if (hipDeviceSynchronize() != hipSuccess) return MADD_EDEVICE;
-    (void)hipFree(g_tables[victim].dev);
-    if (hipSetDevice(cur) != hipSuccess) return MADD_EDEVICE;
-    g_tables.erase(g_tables.begin() + (long)victim);
+  return MADD_OK;
+}
+
+// The HIP side of the descriptor-table cache (policy in table_cache.h).
+struct HipTables {
+  using Event = hipEvent_t;
+  bool alloc(size_t bytes, void** p) { return hipMalloc(p, bytes) == hipSuccess; }
+  void free(void* p) { (void)hipFree(p); }
+  bool upload(void* dst, const void* src, size_t bytes, void* stream) {
+    return fill_device(dst, src, bytes, (hipStream_t)stream) == MADD_OK;
   }
-  TensorDesc* d = nullptr;
-  if (hipMalloc((void**)&d, bytes) != hipSuccess) return MADD_ENOMEM;
-  if (hipMemcpy(d, descs.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
-    (void)hipFree(d);
-    return MADD_EDEVICE;
+  bool new_event(Event* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess; }
+  bool record(Event e, void* stream) { return hipEventRecord(e, (hipStream_t)stream) == hipSuccess; }
+  bool wait(Event e) { return hipEventSynchronize(e) == hipSuccess; }
+};
+HipTables g_hip_tables;
+madd_cache::TableCache<HipTables> g_tables;
+
+int32_t cache_status(int rc) {
+  switch (rc) {
+    case madd_cache::kOk: return MADD_OK;
+    case madd_cache::kCaptureMiss: return MADD_ECAPTURE;
+    case madd_cache::kNoMem: return MADD_ENOMEM;
+    default: return MADD_EDEVICE;
   }
-  g_tables.push_back(TableEntry{dev, descs, d, g_clock});
-  *out = d;
+}
+
+// Whether `stream` is capturing a graph.
+int32_t capturing(hipStream_t stream, bool* cap) {
+  hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &st) != hipSuccess) return MADD_EDEVICE;
+  *cap = st != hipStreamCaptureStatusNone;
   return MADD_OK;
 }
 
@@ -1522,9 +1572,8 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
                int64_t nchunks, const Scalars& s, const Scalars* sdev, hipStream_t stream) {
   if (nchunks <= 0) return MADD_OK;
   if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-  hipLaunchKernelGGL(fn, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab, single, s,
-                     sdev);
-  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  return launch_k(fn, dim3((unsigned)nchunks), dim3(kThreads), stream, table, ntab, single, s,
+                  sdev);
 }
 
 // NVFP4 with current scaling: clear the amax words (one thread per tensor),
@@ -1535,13 +1584,15 @@ int32_t launch_nvcs(const NvcsKernels& k, const TensorDesc* table, int ntab,
   if (nchunks <= 0) return MADD_OK;
   if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
   const unsigned clear_grid = (unsigned)(((ntab == 0 ? 1 : ntab) + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(k.clear, dim3(clear_grid), dim3(kThreads), 0, stream, table, ntab, single, s,
-                     sdev);
-  hipLaunchKernelGGL(k.pass1, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
-                     single, s, sdev);
-  hipLaunchKernelGGL(k.pass2, dim3((unsigned)nchunks), dim3(kThreads), 0, stream, table, ntab,
-                     single, s, sdev);
-  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  int32_t rc = launch_k(k.clear, dim3(clear_grid), dim3(kThreads), stream, table, ntab, single, s,
+                        sdev);
+  if (rc == MADD_OK)
+    rc = launch_k(k.pass1, dim3((unsigned)nchunks), dim3(kThreads), stream, table, ntab, single,
+                  s, sdev);
+  if (rc == MADD_OK)
+    rc = launch_k(k.pass2, dim3((unsigned)nchunks), dim3(kThreads), stream, table, ntab, single,
+                  s, sdev);
+  return rc;
 }
 
 TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void* m, void* v,
@@ -1558,6 +1609,7 @@ TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void*
   d.n = n;
   d.gbase = gbase;
   d.chunk0 = 0;
+  d.chunk_len = (int32_t)kChunk;
   d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy)) &&
              (gbase & 7) == 0;
   return d;
@@ -1673,28 +1725,29 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
   struct Group {
     step_fn fn;  // null for NVFP4 with current scaling, which launches `nvcs`
     NvcsKernels nvcs;
-    TensorDesc* table;
-    int ntab;
+    std::vector<TensorDesc> descs;
     int64_t nchunks;
+    const TensorDesc* table;
+    size_t slot;
   };
   std::vector<Group> groups;
+  int64_t full_total = 0;
   for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4_CURRENT; ++wf) {
     for (int blk = 0; blk <= 1; ++blk) {
       std::vector<TensorDesc> descs;
-      int64_t gbase = index_base, nch = 0;
+      int64_t gbase = index_base, full = 0;
       for (int32_t i = 0; i < ntensors; ++i) {
         const bool is_blk = scales && scales[i];
         if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
-          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, copy ? copy[i] : nullptr,
-                                   g[i], m[i], v[i], ve[i], numel[i], gbase);
-          d.chunk0 = nch;
-          nch += chunks_of(numel[i]);
-          descs.push_back(d);
+          descs.push_back(make_desc(w[i], is_blk ? scales[i] : nullptr,
+                                    copy ? copy[i] : nullptr, g[i], m[i], v[i], ve[i], numel[i],
+                                    gbase));
+          full += chunks_of(numel[i]);
         }
         gbase += numel[i];
       }
       if (descs.empty()) continue;
-      if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+      full_total += full;
       bool any_copy = false;
       for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
       step_fn fn = nullptr;
@@ -1705,22 +1758,52 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
         fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
         if (!fn) return MADD_EUNSUPPORTED;
       }
-      TensorDesc* table = nullptr;
-      rc = get_table(descs, &table);
-      if (rc != MADD_OK) return rc;
-      groups.push_back(Group{fn, nvcs, table, (int)descs.size(), nch});
+      groups.push_back(Group{fn, nvcs, std::move(descs), 0, nullptr, 0});
     }
+  }
+  // One chunk length for the whole call, from its total size.
+  const int32_t len = chunk_len_for(full_total);
+  for (Group& gr : groups) {
+    int64_t nch = 0;
+    for (TensorDesc& d : gr.descs) {
+      d.chunk_len = len;
+      d.chunk0 = nch;
+      nch += chunks_of(d.n, len);
+    }
+    if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+    gr.nchunks = nch;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  bool cap = false;
+  rc = capturing(st, &cap);
+  if (rc != MADD_OK) return rc;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MADD_EDEVICE;
+  size_t acquired = 0;
+  for (; acquired < groups.size(); ++acquired) {
+    Group& gr = groups[acquired];
+    void* t = nullptr;
+    rc = cache_status(g_tables.acquire(g_hip_tables, dev, gr.descs.data(),
+                                       gr.descs.size() * sizeof(TensorDesc), cap, st, &t,
+                                       &gr.slot));
+    if (rc != MADD_OK) break;
+    gr.table = (const TensorDesc*)t;
   }
   TensorDesc none;
   memset(&none, 0, sizeof(none));
-  for (const Group& gr : groups) {
-    rc = gr.fn ? launch(gr.fn, gr.table, gr.ntab, none, gr.nchunks, s, sdev,
-                        (hipStream_t)stream)
-               : launch_nvcs(gr.nvcs, gr.table, gr.ntab, none, gr.nchunks, s, sdev,
-                             (hipStream_t)stream);
-    if (rc != MADD_OK) return rc;
+  for (size_t k = 0; k < acquired && rc == MADD_OK; ++k) {
+    const Group& gr = groups[k];
+    const int ntab = (int)gr.descs.size();
+    rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
+               : launch_nvcs(gr.nvcs, gr.table, ntab, none, gr.nchunks, s, sdev, st);
   }
-  return MADD_OK;
+  const bool launched = rc == MADD_OK;
+  for (size_t k = 0; k < acquired; ++k) {
+    const int32_t r = cache_status(g_tables.release(g_hip_tables, groups[k].slot, cap, st,
+                                                    launched));
+    if (rc == MADD_OK) rc = r;
+  }
+  return rc;
 }
 
 
@@ -1734,6 +1817,9 @@ const char* madd_status_string(int32_t status) {
     case MADD_EUNSUPPORTED: return "MADD_EUNSUPPORTED: request not implemented";
     case MADD_EDEVICE: return "MADD_EDEVICE: HIP runtime or launch failure";
     case MADD_ENOMEM: return "MADD_ENOMEM: device allocation failed";
+    case MADD_ECAPTURE:
+      return "MADD_ECAPTURE: a tensor list's first step cannot run inside a graph capture "
+             "(step it once outside the capture)";
     default: return "unknown madd status";
   }
 }
@@ -1753,11 +1839,11 @@ int32_t madd_init_state(void* m, void* v, void* ve, int32_t sfmt, int64_t n, voi
   hipStream_t st = (hipStream_t)stream;
   void* arr[3] = {m, v, ve};
   for (void* p : arr) {
-    if (sfmt == MADD_S_FP32)
-      hipLaunchKernelGGL(zero_kernel<float>, dim3(grid), dim3(kThreads), 0, st, (float*)p, n);
-    else
-      hipLaunchKernelGGL(zero_kernel<uint16_t>, dim3(grid), dim3(kThreads), 0, st, (uint16_t*)p, n);
-    if (hipGetLastError() != hipSuccess) return MADD_EDEVICE;
+    const int32_t rc =
+        sfmt == MADD_S_FP32
+            ? launch_k(zero_kernel<float>, dim3(grid), dim3(kThreads), st, (float*)p, n)
+            : launch_k(zero_kernel<uint16_t>, dim3(grid), dim3(kThreads), st, (uint16_t*)p, n);
+    if (rc != MADD_OK) return rc;
   }
   return MADD_OK;
 }
@@ -1791,42 +1877,39 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
     const int64_t want_x = (n + kThreads - 1) / kThreads, want_b = (nb + kThreads - 1) / kThreads;
     const unsigned grid_x = (unsigned)(want_x < 4096 ? want_x : 4096);
     const unsigned grid_b = (unsigned)(want_b < 65536 ? want_b : 65536);
-    hipLaunchKernelGGL(nv_clear_kernel, dim3(1), dim3(64), 0, st, slot, head / 4);
-    hipLaunchKernelGGL(nv_amax_kernel, dim3(grid_x), dim3(kThreads), 0, st, x, n, slot);
-    hipLaunchKernelGGL(nv_scale_kernel, dim3(1), dim3(64), 0, st, slot);
-    hipLaunchKernelGGL(encode_nv_kernel, dim3(grid_b), dim3(kThreads), 0, st, x, (uint8_t*)w,
-                       (uint8_t*)scales, nb, head);
-    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+    int32_t rc = launch_k(nv_clear_kernel, dim3(1), dim3(64), st, slot, head / 4);
+    if (rc == MADD_OK) rc = launch_k(nv_amax_kernel, dim3(grid_x), dim3(kThreads), st, x, n, slot);
+    if (rc == MADD_OK) rc = launch_k(nv_scale_kernel, dim3(1), dim3(64), st, slot);
+    if (rc == MADD_OK)
+      rc = launch_k(encode_nv_kernel, dim3(grid_b), dim3(kThreads), st, x, (uint8_t*)w,
+                    (uint8_t*)scales, nb, head);
+    return rc;
   }
   if (wfmt == MADD_W_MXFP4) {
     const int64_t nb = n / kMxBlock;
     const int64_t want = (nb + kThreads - 1) / kThreads;
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
-    hipLaunchKernelGGL(encode_mx_kernel, dim3(grid), dim3(kThreads), 0, st, x, (uint8_t*)w,
-                       (uint8_t*)scales, nb);
-    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+    return launch_k(encode_mx_kernel, dim3(grid), dim3(kThreads), st, x, (uint8_t*)w,
+                    (uint8_t*)scales, nb);
   }
   if (scales) {
     const int64_t nb = n / kBlock;
     const int64_t want = (nb + kThreads - 1) / kThreads;
     const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
-    if (wfmt == MADD_W_FP8_E4M3)
-      hipLaunchKernelGGL(encode_block_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), 0, st, x,
-                         (uint8_t*)w, (uint16_t*)scales, nb);
-    else
-      hipLaunchKernelGGL(encode_block_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), 0, st, x,
-                         (uint8_t*)w, (uint16_t*)scales, nb);
-    return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+    return wfmt == MADD_W_FP8_E4M3
+               ? launch_k(encode_block_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), st, x,
+                          (uint8_t*)w, (uint16_t*)scales, nb)
+               : launch_k(encode_block_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), st, x,
+                          (uint8_t*)w, (uint16_t*)scales, nb);
   }
   const int64_t want = (n + kThreads - 1) / kThreads;
-  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  const dim3 grid((unsigned)(want < 65536 ? want : 65536)), block(kThreads);
   switch (wfmt) {
-    case MADD_W_BF16: hipLaunchKernelGGL(encode_kernel<WF_BF16>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
-    case MADD_W_FP8_E4M3: hipLaunchKernelGGL(encode_kernel<WF_E4M3>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
-    case MADD_W_FP8_E5M2: hipLaunchKernelGGL(encode_kernel<WF_E5M2>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
-    default: hipLaunchKernelGGL(encode_kernel<WF_FP32>, dim3(grid), dim3(kThreads), 0, st, x, w, n); break;
+    case MADD_W_BF16: return launch_k(encode_kernel<WF_BF16>, grid, block, st, x, w, n);
+    case MADD_W_FP8_E4M3: return launch_k(encode_kernel<WF_E4M3>, grid, block, st, x, w, n);
+    case MADD_W_FP8_E5M2: return launch_k(encode_kernel<WF_E5M2>, grid, block, st, x, w, n);
+    default: return launch_k(encode_kernel<WF_FP32>, grid, block, st, x, w, n);
   }
-  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
 }
 
 int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const void* g,
@@ -1845,14 +1928,17 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
     if (gfmt != MADD_G_FP32) return MADD_EINVAL;  // w' is written over the fp32 gradient
     const NvcsKernels k = pick_part9(sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                                      copy != nullptr);
-    const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-    return launch_nvcs(k, nullptr, 0, d, chunks_of(n), s, nullptr, (hipStream_t)stream);
+    TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
+    d.chunk_len = chunk_len_for(chunks_of(n));
+    return launch_nvcs(k, nullptr, 0, d, chunks_of(n, d.chunk_len), s, nullptr,
+                       (hipStream_t)stream);
   }
   step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                            copy != nullptr, scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
-  const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-  return launch(fn, nullptr, 0, d, chunks_of(n), s, nullptr, (hipStream_t)stream);
+  TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
+  d.chunk_len = chunk_len_for(chunks_of(n));
+  return launch(fn, nullptr, 0, d, chunks_of(n, d.chunk_len), s, nullptr, (hipStream_t)stream);
 }
 
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
@@ -1881,9 +1967,8 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
   }
   const int64_t want = (n + (int64_t)kThreads * kQuad - 1) / ((int64_t)kThreads * kQuad);
   const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(kThreads), 0, (hipStream_t)stream, w, g, n, index_base,
-                     (float)hp->lr_add, s);
-  return hipGetLastError() == hipSuccess ? MADD_OK : MADD_EDEVICE;
+  return launch_k(fn, dim3(grid), dim3(kThreads), (hipStream_t)stream, w, g, n, index_base,
+                  (float)hp->lr_add, s);
 }
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,

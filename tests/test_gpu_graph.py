@@ -157,3 +157,72 @@ def test_captured_step_with_device_scalars_replays_successive_steps():
         B.madd_multi_tensor_step(tlb, h)
         torch.cuda.synchronize()
         assert_lists_equal(a, b, t)
+
+
+def other_lists(k, n=2048 + 8):
+    """k small lists of their own buffers (each a distinct descriptor table)."""
+    out = []
+    for i in range(k):
+        w = torch.zeros(n, dtype=torch.int16, device="cuda")
+        g, m, v, ve = (torch.full((n,), 1e-3 * (i + 1), device="cuda") for _ in range(4))
+        out.append(B.TensorList([w], ["bf16"], [g], [m], [v], [ve]))
+    return out
+
+
+def test_captured_step_survives_forty_other_lists():
+    """The descriptor table a captured step reads is pinned: after 40 other
+    lists are stepped eagerly (more than the cache keeps unpinned, so tables
+    are recycled meanwhile), replays still equal eager steps."""
+    a, fmts = state(8)
+    b, _ = state(8)
+    tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
+    h = W.hparams("c2", step=3)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        B.madd_multi_tensor_step(tla, h)          # eager: caches the table
+    torch.cuda.current_stream().wait_stream(s)
+    B.madd_multi_tensor_step(tlb, h)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        B.madd_multi_tensor_step(tla, h)
+    others = other_lists(40)
+    gen = torch.Generator(device="cuda")
+    for r in range(3):
+        for tl in others:                         # 40 eager steps of other lists
+            B.madd_multi_tensor_step(tl, W.hparams("c2", step=r + 1))
+        gen.manual_seed(50 + r)
+        for ga, gb in zip(a["g"], b["g"]):
+            ga.normal_(0, 1e-3, generator=gen)
+            gb.copy_(ga)
+        torch.cuda.synchronize()
+        graph.replay()
+        B.madd_multi_tensor_step(tlb, h)
+        torch.cuda.synchronize()
+        assert_lists_equal(a, b, f"replay {r}")
+
+
+def test_list_first_seen_during_capture_is_refused():
+    """A list the library has not seen before cannot be captured (its table
+    would have to be allocated and written inside the capture): the call
+    returns MADD_ECAPTURE and touches nothing; stepped once outside the
+    capture, the list captures."""
+    a, fmts = state(9)
+    b, _ = state(9)
+    tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
+    for ga, gb in zip(a["g"], b["g"]):
+        ga.fill_(1e-3)
+        gb.fill_(1e-3)
+    torch.cuda.synchronize()
+    h = W.hparams("c2", step=1)
+    graph = torch.cuda.CUDAGraph()
+    with pytest.raises(B.MaddError, match="ECAPTURE"):
+        with torch.cuda.graph(graph):
+            B.madd_multi_tensor_step(tla, h)
+    torch.cuda.synchronize()
+    assert_lists_equal(a, b, "refused capture")
+    B.madd_multi_tensor_step(tla, h)
+    B.madd_multi_tensor_step(tlb, h)
+    torch.cuda.synchronize()
+    assert_lists_equal(a, b, "eager after refusal")
