@@ -1,4 +1,5 @@
-// Device probes declared in include/madd_probes.h.
+// Device probes declared in madd_probes.h (measurement only; not part of the
+// optimizer library).
 //
 // Plain read-only, write-only and copy streams (madd_stream_modes) measure
 // what HBM delivers for each direction alone in the same access shape.

@@ -1,7 +1,9 @@
 """Build of the HIP libraries (gfx950), in-tree: ``libmadd.so`` (the
-optimizer step, include/madd.h) and ``libmadd_probes.so`` (device probes:
-the streaming ceiling the benchmark reports beside the HBM peak, and the
-exhaustive check of the bf16 conversion instructions; include/madd_probes.h).
+optimizer step, include/madd.h) and, outside the package,
+``bench_probes/libmadd_probes.so`` (measurement probes, not part of the
+optimizer: the streaming ceiling the benchmark reports beside the HBM peak,
+and the exhaustive check of the bf16 conversion instructions;
+bench_probes/madd_probes.h).
 
 The flags are part of the numerical contract of the kernels:
   * ``-ffp-contract=off``: only the fmaf calls written in the source fuse;
@@ -21,10 +23,12 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "madd.hip")
 HDR = os.path.join(ROOT, "include", "madd.h")
+CACHE_HDR = os.path.join(PKG, "csrc", "table_cache.h")
 LIB = os.path.join(PKG, "libmadd.so")
-PROBE_SRC = os.path.join(PKG, "csrc", "probes.hip")
-PROBE_HDR = os.path.join(ROOT, "include", "madd_probes.h")
-PROBE_LIB = os.path.join(PKG, "libmadd_probes.so")
+PROBE_DIR = os.path.join(ROOT, "bench_probes")
+PROBE_SRC = os.path.join(PROBE_DIR, "probes.hip")
+PROBE_HDR = os.path.join(PROBE_DIR, "madd_probes.h")
+PROBE_LIB = os.path.join(PROBE_DIR, "libmadd_probes.so")
 TARGETS = ((SRC, HDR, LIB), (PROBE_SRC, PROBE_HDR, PROBE_LIB))
 ARCH = "gfx950"
 
@@ -60,7 +64,7 @@ def build(verbose: bool = False) -> str:
         objs = [os.path.join(tmpdir, f"madd_part{k}.o") for k in range(NPARTS)]
         cmds = [[hipcc(), *compile_flags, *inc, f"-DMADD_PART={k}", "-c", "-o", objs[k], SRC]
                 for k in range(NPARTS)]
-        cmds.append([hipcc(), *HIPCC_FLAGS, *inc, "-o", PROBE_LIB + ".tmp", PROBE_SRC])
+        cmds.append([hipcc(), *HIPCC_FLAGS, "-I", PROBE_DIR, "-o", PROBE_LIB + ".tmp", PROBE_SRC])
         workers = max(1, min(len(cmds), os.cpu_count() or 1))
         with ThreadPoolExecutor(workers) as ex:
             list(ex.map(lambda c: _run(c, verbose), cmds))
@@ -75,7 +79,8 @@ def is_stale() -> bool:
         if not os.path.exists(lib):
             return True
         t = os.path.getmtime(lib)
-        if any(os.path.getmtime(p) > t for p in (src, hdr)):
+        deps = (src, hdr, CACHE_HDR) if lib == LIB else (src, hdr)
+        if any(os.path.getmtime(p) > t for p in deps):
             return True
     return False
 
