@@ -14,6 +14,9 @@ from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_stat
                              free_device_bytes, gpu_step, oracle_step, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
+# steps of the full 7B master-weight list (Algorithm 1 changes its bias
+# corrections and draws with t)
+MASTER_STEPS = 10
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -71,7 +74,7 @@ def check(tag, ds, hs):
 
 
 def run_mx(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
-           grad=mx_grad):
+           grad=mx_grad, full=False):
     rng = np.random.default_rng(seed)
     q, s = encode_mx_both(mx_weights(rng, n))
     ds = DevState("mxfp4", q, n, s, sfmt=sfmt, copy=copy)
@@ -81,7 +84,7 @@ def run_mx(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=Fa
         if gfmt == "bf16":
             g = oracle.encode_array("bf16", g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base, full_chunks=full)
         oracle_step("mxfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
         torch.cuda.synchronize()
         check(f"mxfp4 n={n} t={t}", ds, hs)
@@ -98,12 +101,14 @@ def test_encode_matches_oracle():
     encode_mx_both(x)
 
 
+@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
                                                  ("sr", "bf16", True), ("rne", "bf16", False),
                                                  ("sr", "bf16_sr", True)])
-def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy, full):
     # five whole 2048-element tiles, then 3 blocks of a sixth
-    run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
+    run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy,
+           full=full)
 
 
 @pytest.mark.parametrize("n", [32, 64, 992, 2048 + 32, 4096 + 1024 + 96])
@@ -234,7 +239,7 @@ def test_fp4_master_llama7b_sampled():
         hosts.append(hs)
     tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
                       scales=dev["sc"], copies=dev["cp"])
-    for t in (1, 2, 3):
+    for t in range(1, MASTER_STEPS + 1):
         for i in range(len(specs)):
             W.grad_fp32_device_(cfg, i, t, dev["g"][i])
         h = W.hparams(cfg, step=t)

@@ -16,6 +16,9 @@ from gpu_parity_util import (DevState, HostState, assert_copy_equal, assert_stat
 from test_oracle_nv import reference_blocks
 
 pytestmark = pytest.mark.gpu
+# steps of the full 7B master-weight list (Algorithm 1 changes its bias
+# corrections and draws with t)
+MASTER_STEPS = 10
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -72,7 +75,7 @@ def check(tag, ds, hs):
 
 
 def run_nv(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
-           grad=nv_grad):
+           grad=nv_grad, full=False):
     rng = np.random.default_rng(seed)
     q, s = encode_nv_both(nv_weights(rng, n))
     ds = DevState("nvfp4", q, n, s, sfmt=sfmt, copy=copy)
@@ -82,7 +85,7 @@ def run_nv(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=Fa
         if gfmt == "bf16":
             g = oracle.encode_array("bf16", g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base, full_chunks=full)
         oracle_step("nvfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
         torch.cuda.synchronize()
         check(f"nvfp4 n={n} t={t}", ds, hs)
@@ -98,10 +101,12 @@ def test_encode_matches_oracle():
     encode_nv_both(np.zeros(64, np.float32))        # no finite nonzero value: st = 1
 
 
+@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
                                                  ("sr", "bf16", True), ("sr", "bf16_sr", True)])
-def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
-    run_nv(5 * 8192 + 7 * 16, 4, 32, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy, full):
+    run_nv(5 * 8192 + 7 * 16, 4, 32, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy,
+           full=full)
 
 
 @pytest.mark.parametrize("n", [16, 48, 1008, 2048 + 16, 4096 + 1024 + 80])
@@ -239,7 +244,7 @@ def test_nvfp4_master_llama7b_sampled():
         hosts.append(hs)
     tl = B.TensorList(dev["w"], [p[0] for p in plan], dev["g"], dev["m"], dev["v"], dev["ve"],
                       scales=dev["sc"], copies=dev["cp"])
-    for t in (1, 2, 3):
+    for t in range(1, MASTER_STEPS + 1):
         for i in range(len(specs)):
             W.grad_fp32_device_(cfg, i, t, dev["g"][i])
         h = W.hparams(cfg, step=t)
