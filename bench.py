@@ -8,11 +8,14 @@ write back.  Default workload: the Llama-7B-shaped list (291 tensors,
 6,738,415,616 parameters, bf16 weights, fp32 gradients and m / v / v_e),
 all resident in HBM before timing starts, in flat per-role buffers (weights,
 gradients, m, v, v_e each one allocation, tensors as views).  Gradients are
-synthetic (two pre-generated sets, alternating between steps).
+synthetic: before every step the gradient buffer is filled anew on the
+device from that step's seeds (outside the timed events; each step is
+bracketed by its own pair of events on the launching stream).
 
 Prints one JSON line with optimizer-step throughput (Gparam/s), the achieved
 HBM bandwidth of the step kernel against the 8 TB/s peak, and the CPU oracle
-timed on a bounded sample on this host.
+timed on a bounded sample on this host, on all of the process's cores (up
+to 16) and on one thread.
 """
 from __future__ import annotations
 
@@ -46,21 +49,27 @@ def bytes_per_param(wfmt: str, sfmt: str) -> float:
 
 
 def algorithmic_bytes(sizes, plan, sfmt: str) -> float:
-    """Bytes one step over a tensor list must move: every array read and
-    written once, plus per tensor its bf16 compute copy (written) and its
-    block scales (read and written: FP16 per 128 elements for FP8, E8M0 per
-    32 for MXFP4, E4M3 per 16 for NVFP4, whose fp32 tensor scale is read).
-    NVFP4 with current scaling also writes w' over the fp32 gradient in its
-    first pass and reads it back in its second (8 B per element), and per
-    tensor reads and writes its scale and amax words (16 B).
+    """Bytes one step over a tensor list must move (the method's bytes):
+    every array read and written once, plus per tensor its bf16 compute copy
+    (written) and its block scales (read and written: FP16 per 128 elements
+    for FP8, E8M0 per 32 for MXFP4, E4M3 per 16 for NVFP4, whose fp32 tensor
+    scale is read, and with current scaling also written).
     `plan` holds (weight format, block-scaled, compute copy) per tensor."""
     total = 0.0
     for n, (wf, blk, cp) in zip(sizes, plan):
         total += n * bytes_per_param(wf, sfmt) + (n * 2 if cp else 0)
         if blk:
             total += {"mxfp4": (n // 32) * 2, "nvfp4": (n // 16) * 2 + 4,
-                      "nvfp4_current": (n // 16) * 2 + 16 + 8 * n}.get(wf, (n // 128) * 4)
+                      "nvfp4_current": (n // 16) * 2 + 8}.get(wf, (n // 128) * 4)
     return total
+
+
+def scratch_bytes(sizes, plan) -> float:
+    """Bytes the two-pass NVFP4 current-scaling step moves beyond the
+    method's: w' written over the fp32 gradient by pass 1 and read back by
+    pass 2 (8 B per element), and per tensor the amax word (cleared, folded
+    into, read: 12 B)."""
+    return sum(8 * n + 12 for n, (wf, blk, _) in zip(sizes, plan) if wf == "nvfp4_current")
 
 WORKLOAD_NAMES = {
     "c5": "llama-7b-shaped list (32 layers, d=4096, SwiGLU 11008, vocab 32000)",
@@ -160,6 +169,23 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
             "host": host_cpu()}
 
 
+def cpu_full_configs(threads: int) -> dict:
+    """The oracle on whole lists: the 1024x1024 tensor, GPT-2-small and
+    Llama-1.1B (every parameter; fp32 moments; two steps with their own
+    gradient sets), on one thread and on `threads` threads."""
+    from paper_2607_10611_amd import workloads as W
+
+    out = {"kind": "oracle", "unit": "Gparam/s", "host": host_cpu(), "configs": []}
+    for cfg in ("c1", "c2", "c3"):
+        n = W.total_params(cfg)
+        for th in sorted({1, threads}):
+            log(f"oracle on the whole {cfg} list ({n:,} parameters), {th} thread(s)")
+            r = cpu_baseline(cfg, n, 2, "fp32", th, seconds=0.0)
+            out["configs"].append({"config": cfg, "workload": WORKLOAD_NAMES[cfg], "params": n,
+                                   "cores": th, "value": r["value"], "sample": r["sample"]})
+    return out
+
+
 def host_cpu() -> str:
     """The host CPU model and how many logical CPUs this process may use."""
     model = "unknown CPU"
@@ -204,6 +230,10 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="host threads for the oracle (default: this process's CPUs, at most 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="instead of timing the GPU, time the oracle on the 1024x1024, GPT-2 "
+                         "and Llama-1.1B lists in full (every parameter, two steps each), on "
+                         "one thread and on all of the process's cores (up to 16)")
     ap.add_argument("--no-ceiling", action="store_true",
                     help="skip the streaming-ceiling probe (same buffers and bytes, no arithmetic)")
     ap.add_argument("--shard", default=None, metavar="K/P",
@@ -220,6 +250,9 @@ def main():
               "are not implemented (the step shards by index range without communication: "
               "use --shard K/P to time one GPU's share).", file=sys.stderr)
         sys.exit(2)
+    if args.cpu_full:
+        print(json.dumps(cpu_full_configs(args.cpu_threads or cpu_threads())), flush=True)
+        return
 
     import torch
 
@@ -296,31 +329,23 @@ def main():
         else:
             sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
         cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
-    gbufs, grad_sets = [], []
-    gb, gl = flat(torch.float32)
-    gbufs.append(gb)
-    grad_sets.append(gl)
+    gbuf, gl = flat(torch.float32)
     st_dt = torch.float32 if args.states == "fp32" else torch.int16
     mbuf, ms = flat(st_dt)
     vbuf, vs = flat(st_dt)
     vebuf, ves = flat(st_dt)
-    gb, gl = flat(torch.float32)
-    gbufs.append(gb)
-    grad_sets.append(gl)
     for i in range(len(specs)):
         x = W.init_fp32_device(cfg, i, dev)
         B.madd_encode_weights(x, ws[i], plan[i][0], scales=scales[i] if scales else None)
         del x
         B.madd_init_state(ms[i], vs[i], ves[i])
-        for k in range(2):
-            W.grad_fp32_device_(cfg, i, k + 1, grad_sets[k][i])
     torch.cuda.synchronize()
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
         f"{time.perf_counter() - t0:.1f} s")
 
     sfmt = args.states.replace("-", "_")
-    lists = [B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
-                          copies=copies, sfmt=sfmt) for gl in grad_sets]
+    tlist = B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
+                         copies=copies, sfmt=sfmt)
     stream = torch.cuda.current_stream()
     step_no = 0
     lo, hi = 0, nparam
@@ -332,38 +357,45 @@ def main():
         hi = nparam if shard[0] == shard[1] - 1 else lo + per
         log(f"shard {shard[0]}/{shard[1]}: elements [{lo:,}, {hi:,})")
 
+    def new_gradients(t):
+        """Step t's gradients, generated on the device (not timed)."""
+        for i in range(len(specs)):
+            W.grad_fp32_device_(cfg, i, t, gl[i])
+
     def one_step():
-        nonlocal step_no
-        step_no += 1
         h = W.hparams(cfg, step=step_no)
         if shard:
-            B.madd_step(wbuf[lo:hi], wfmt, gbufs[step_no % 2][lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+            B.madd_step(wbuf[lo:hi], wfmt, gbuf[lo:hi], mbuf[lo:hi], vbuf[lo:hi],
                         vebuf[lo:hi], h, index_base=lo, sfmt=sfmt, stream=stream)
         else:
-            B.madd_multi_tensor_step(lists[step_no % 2], h, stream=stream)
+            B.madd_multi_tensor_step(tlist, h, stream=stream)
 
     for _ in range(args.warmup):
+        step_no += 1
+        new_gradients(step_no)
         one_step()
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")
 
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    ev[0].record(stream)
     for k in range(args.steps):
+        step_no += 1
+        new_gradients(step_no)
+        ev[k][0].record(stream)
         one_step()
-        ev[k + 1].record(stream)
+        ev[k][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    per_launch_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
-    total_ms = ev[0].elapsed_time(ev[-1])
-    ms_per_step = total_ms / args.steps
-    avg_launch_ms = sum(per_launch_ms) / len(per_launch_ms)
+    per_launch_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = sum(per_launch_ms) / args.steps
+    avg_launch_ms = ms_per_step
     median_ms = statistics.median(per_launch_ms)
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / args.steps:.3f})"
-        f", launches min {min(per_launch_ms):.3f} median {median_ms:.3f} "
-        f"max {max(per_launch_ms):.3f} ms")
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall with gradient generation "
+        f"{wall * 1e3 / args.steps:.3f}), launches min {min(per_launch_ms):.3f} median "
+        f"{median_ms:.3f} max {max(per_launch_ms):.3f} ms")
 
     n_step = hi - lo
     if shard:
@@ -375,7 +407,7 @@ def main():
 
     ceiling = None
     if not args.no_ceiling and args.weights == "list" and wfmt == "bf16":
-        ceiling = stream_ceiling(wbuf[lo:hi], gbufs[1][lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+        ceiling = stream_ceiling(wbuf[lo:hi], gbuf[lo:hi], mbuf[lo:hi], vbuf[lo:hi],
                                  vebuf[lo:hi], 4 if args.states == "fp32" else 2, args.steps,
                                  stream, alg_bytes, achieved)
         log(f"streaming ceiling: {ceiling['achieved']:.1f} GB/s; the step reaches "
@@ -415,6 +447,11 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic, "algorithmic_bytes_per_launch": int(round(alg_bytes)),
                 "kernel": kname, "avg_launch_ms": round(avg_launch_ms, 4)}
+    extra = 0 if shard else scratch_bytes(sizes, plan)
+    if extra:
+        roofline["scratch_bytes_per_launch"] = int(extra)
+        roofline["achieved_with_scratch"] = round((alg_bytes + extra) / (avg_launch_ms / 1e3)
+                                                  / 1e9, 1)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -422,6 +459,10 @@ def main():
         log(f"timing the CPU oracle on a sample ({threads} threads)")
         steps = args.cpu_steps or (10 if args.states == "fp32" else 4)
         cpu = cpu_baseline(cfg, args.cpu_sample, steps, sfmt, threads, args.cpu_seconds)
+        if threads > 1:
+            log("timing the CPU oracle on the same sample, one thread")
+            one = cpu_baseline(cfg, args.cpu_sample, steps, sfmt, 1, args.cpu_seconds)
+            cpu["one_thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
 
     workload = WORKLOAD_NAMES[cfg]
     if shard:

@@ -41,7 +41,9 @@ def test_algorithmic_bytes_of_the_7b_settings():
     assert nv == nl * (29 + 2) + rest * 32 + nl // 16 * 2 + 4 * nt
     cs = bench.algorithmic_bytes(sizes, W.low_precision_master_plan("c5", "nvfp4_current"),
                                  "fp32")
-    assert cs == nl * (29 + 2 + 8) + rest * 32 + nl // 16 * 2 + 16 * nt
+    assert cs == nl * (29 + 2) + rest * 32 + nl // 16 * 2 + 8 * nt
+    plan = W.low_precision_master_plan("c5", "nvfp4_current")
+    assert bench.scratch_bytes(sizes, plan) == 8 * nl + 12 * nt
 
 
 def test_traffic_is_reported_only_for_the_profiled_kernel_source(monkeypatch, tmp_path):
