@@ -8,9 +8,12 @@ write back.  Default workload: the Llama-7B-shaped list (291 tensors,
 6,738,415,616 parameters, bf16 weights, fp32 gradients and m / v / v_e),
 all resident in HBM before timing starts, in flat per-role buffers (weights,
 gradients, m, v, v_e each one allocation, tensors as views).  Gradients are
-synthetic: before every step the gradient buffer is filled anew on the
-device from that step's seeds (outside the timed events; each step is
-bracketed by its own pair of events on the launching stream).
+synthetic: for the 7B list the gradient buffer is filled anew on the device
+from each step's seeds before the step (outside the timed events; each step
+is bracketed by its own pair of events on the launching stream); the smaller
+lists cycle through up to eight sets made up front, with the steps queued
+back to back behind a short GPU-side delay so that the events between them
+time the GPU alone.
 
 Prints one JSON line with optimizer-step throughput (Gparam/s), the achieved
 HBM bandwidth of the step kernel against the 8 TB/s peak, and the CPU oracle
@@ -229,6 +232,11 @@ def main():
                     help="time the oracle steps the sample for (at least two steps)")
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="host threads for the oracle (default: this process's CPUs, at most 16)")
+    ap.add_argument("--grads", default=None, choices=["regen", "cycle"],
+                    help="regen: fill the gradients anew on the device before every step "
+                         "(default when one gradient set exceeds 8 GiB); cycle: generate up to "
+                         "8 sets up front and cycle through them, steps queued back to back "
+                         "(default for the smaller lists)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-full", action="store_true",
                     help="instead of timing the GPU, time the oracle on the 1024x1024, GPT-2 "
@@ -329,7 +337,15 @@ def main():
         else:
             sbuf, scales = flat_subset(torch.int16, lambda p: p[1], per_elem=128)
         cbuf, copies = flat_subset(torch.int16, lambda p: p[2])
-    gbuf, gl = flat(torch.float32)
+    # Gradients: regenerated on the device before every step (outside the
+    # events) when one set is large enough that its generation keeps the GPU
+    # busy while the host queues the next step; otherwise a few sets made up
+    # front and cycled, with the steps queued behind a short GPU-side delay so
+    # that the events between back-to-back steps time the GPU alone.
+    grads = args.grads or ("regen" if nparam * 4 > (8 << 30) else "cycle")
+    nsets = 1 if grads == "regen" else max(1, min(8, args.steps))
+    gsets = [flat(torch.float32) for _ in range(nsets)]
+    gbuf = gsets[0][0]
     st_dt = torch.float32 if args.states == "fp32" else torch.int16
     mbuf, ms = flat(st_dt)
     vbuf, vs = flat(st_dt)
@@ -339,13 +355,17 @@ def main():
         B.madd_encode_weights(x, ws[i], plan[i][0], scales=scales[i] if scales else None)
         del x
         B.madd_init_state(ms[i], vs[i], ves[i])
+        if grads == "cycle":
+            for k, (_, gl) in enumerate(gsets):
+                W.grad_fp32_device_(cfg, i, k + 1, gl[i])
     torch.cuda.synchronize()
     log(f"resident: {torch.cuda.memory_allocated() / 2**30:.1f} GiB in "
-        f"{time.perf_counter() - t0:.1f} s")
+        f"{time.perf_counter() - t0:.1f} s; gradients: {grads}"
+        + (f" ({nsets} sets)" if grads == "cycle" else ""))
 
     sfmt = args.states.replace("-", "_")
-    tlist = B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
-                         copies=copies, sfmt=sfmt)
+    tlists = [B.TensorList(ws, [p[0] for p in plan], gl, ms, vs, ves, scales=scales,
+                           copies=copies, sfmt=sfmt) for _, gl in gsets]
     stream = torch.cuda.current_stream()
     step_no = 0
     lo, hi = 0, nparam
@@ -359,16 +379,19 @@ def main():
 
     def new_gradients(t):
         """Step t's gradients, generated on the device (not timed)."""
-        for i in range(len(specs)):
-            W.grad_fp32_device_(cfg, i, t, gl[i])
+        if grads == "regen":
+            for i in range(len(specs)):
+                W.grad_fp32_device_(cfg, i, t, gsets[0][1][i])
 
     def one_step():
         h = W.hparams(cfg, step=step_no)
+        k = (step_no - 1) % nsets
         if shard:
-            B.madd_step(wbuf[lo:hi], wfmt, gbuf[lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+            gb = gsets[k][0]
+            B.madd_step(wbuf[lo:hi], wfmt, gb[lo:hi], mbuf[lo:hi], vbuf[lo:hi],
                         vebuf[lo:hi], h, index_base=lo, sfmt=sfmt, stream=stream)
         else:
-            B.madd_multi_tensor_step(tlist, h, stream=stream)
+            B.madd_multi_tensor_step(tlists[k], h, stream=stream)
 
     for _ in range(args.warmup):
         step_no += 1
@@ -377,25 +400,36 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    for k in range(args.steps):
-        step_no += 1
-        new_gradients(step_no)
-        ev[k][0].record(stream)
-        one_step()
-        ev[k][1].record(stream)
-    torch.cuda.synchronize()
+    if grads == "regen":
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for k in range(args.steps):
+            step_no += 1
+            new_gradients(step_no)
+            ev[k][0].record(stream)
+            one_step()
+            ev[k][1].record(stream)
+        torch.cuda.synchronize()
+        per_launch_ms = [a.elapsed_time(b) for a, b in ev]
+    else:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        gpu_delay(stream, args.steps)
+        ev[0].record(stream)
+        for k in range(args.steps):
+            step_no += 1
+            one_step()
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        per_launch_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
     wall = time.perf_counter() - wall0
-    per_launch_ms = [a.elapsed_time(b) for a, b in ev]
     ms_per_step = sum(per_launch_ms) / args.steps
     avg_launch_ms = ms_per_step
     median_ms = statistics.median(per_launch_ms)
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (wall with gradient generation "
-        f"{wall * 1e3 / args.steps:.3f}), launches min {min(per_launch_ms):.3f} median "
-        f"{median_ms:.3f} max {max(per_launch_ms):.3f} ms")
+    log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step (wall {wall * 1e3 / args.steps:.3f}"
+        f"{' with gradient generation' if grads == 'regen' else ''}), launches min "
+        f"{min(per_launch_ms):.4f} median {median_ms:.4f} max {max(per_launch_ms):.4f} ms")
 
     n_step = hi - lo
     if shard:
@@ -499,6 +533,21 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def gpu_delay(stream, steps: int):
+    """Queue a bounded GPU-side wait (madd_probe_delay) long enough for the
+    host to enqueue `steps` short steps behind it: about 5 ms plus 100 us
+    per step."""
+    import ctypes
+
+    from paper_2607_10611_amd import _build
+
+    lib = ctypes.CDLL(_build.PROBE_LIB)
+    lib.madd_probe_delay.argtypes = [ctypes.c_int32, ctypes.c_void_p]
+    lib.madd_probe_delay.restype = ctypes.c_int32
+    sleeps = int((5e-3 + 1e-4 * steps) / 3.4e-6)
+    assert lib.madd_probe_delay(min(sleeps, 1 << 20), stream.cuda_stream) == 0
+
+
 def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_gbs) -> dict:
     """Time the streaming-ceiling probe (libmadd_probes.so) on the step's own
     buffers: the same bytes and access pattern without the arithmetic."""
@@ -517,6 +566,7 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
         assert lib.madd_ceiling_stream(*args) == 0
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
+    gpu_delay(stream, steps)
     ev[0].record(stream)
     for k in range(steps):
         assert lib.madd_ceiling_stream(*args) == 0

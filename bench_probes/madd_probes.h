@@ -71,6 +71,13 @@ int32_t madd_stream_modes(int32_t mode, const void* a, void* b, int64_t bytes, v
  * launch fails. */
 int32_t madd_probe_bf16_rounding(uint64_t* counters, void* stream);
 
+/* madd_probe_delay: one wave on `stream` that sleeps `sleeps` times (each
+ * s_sleep 127, about 8k cycles, ~3.5 us) and exits.  The benchmark enqueues
+ * it ahead of a run of short steps so that the host has queued them all
+ * before the first starts, and the events between steps time the GPU alone.
+ * Returns -1 for sleeps outside [0, 2^20], -3 if the launch fails. */
+int32_t madd_probe_delay(int32_t sleeps, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -190,6 +190,18 @@ extern "C" int32_t madd_stream_modes(int32_t mode, const void* a, void* b, int64
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
+// One wave that sleeps `sleeps` times (s_sleep 127: about 8k cycles each)
+// and exits: a bounded wait that keeps the stream busy.
+__global__ __launch_bounds__(64) void delay_kernel(int32_t sleeps) {
+  for (int32_t i = 0; i < sleeps; ++i) __builtin_amdgcn_s_sleep(127);
+}
+
+extern "C" int32_t madd_probe_delay(int32_t sleeps, void* stream) {
+  if (sleeps < 0 || sleeps > (1 << 20)) return -1;
+  hipLaunchKernelGGL(delay_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, sleeps);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
 extern "C" int32_t madd_probe_bf16_rounding(uint64_t* counters, void* stream) {
   if (!counters) return -1;
   hipLaunchKernelGGL(bf16_rounding_kernel, dim3(65536), dim3(256), 0, (hipStream_t)stream,

@@ -78,6 +78,10 @@ def test_ceiling_probe_rejects_bad_arguments():
     L.madd_probe_bf16_rounding.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     L.madd_probe_bf16_rounding.restype = ctypes.c_int32
     assert L.madd_probe_bf16_rounding(None, None) == -1
+    L.madd_probe_delay.argtypes = [ctypes.c_int32, ctypes.c_void_p]
+    L.madd_probe_delay.restype = ctypes.c_int32
+    assert L.madd_probe_delay(-1, None) == -1
+    assert L.madd_probe_delay((1 << 20) + 1, None) == -1
 
 
 def test_library_exports_every_declared_symbol():
