@@ -67,8 +67,10 @@ typedef enum madd_status {
   MADD_EUNSUPPORTED = -3,/* valid request the library does not implement      */
   MADD_EDEVICE = -4,     /* a HIP runtime call or kernel launch failed         */
   MADD_ENOMEM = -5,      /* device allocation for the descriptor table failed  */
-  MADD_ECAPTURE = -6     /* a multi-tensor list seen for the first time while
+  MADD_ECAPTURE = -6,    /* a multi-tensor list seen for the first time while
                             its stream is capturing a graph                    */
+  MADD_ESCRATCH = -7     /* more tensors than madd_multi_tensor_step_noalloc's
+                            fixed descriptor table holds                       */
 } madd_status;
 
 /* Weight storage formats.
@@ -289,6 +291,28 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
                                void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                const int64_t* numel, int64_t index_base, const madd_hparams* hp,
                                void* stream);
+
+/* madd_multi_tensor_step without any device allocation, for callers that
+ * cannot allocate device memory (code running under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  Same arguments, results
+ * (bit for bit) and validation as madd_multi_tensor_step.  The descriptor
+ * tables of the call are written into a fixed device array that the library
+ * holds on each GPU until the process ends (4096 descriptors of 88 bytes,
+ * 352 KiB per GPU), with small kernels on `stream` ahead of the step kernels:
+ * nothing is cached, allocated, freed or waited for, and a captured call
+ * records the table writes too, so its replays need no earlier eager call.
+ * Limits: at most 4096 nonempty tensors per call (else MADD_ESCRATCH, nothing
+ * enqueued).  Every call on one GPU shares that array: calls on one GPU that
+ * can run at the same time (different streams or threads, or graphs replayed
+ * concurrently) race and must be ordered by the caller.  The first call on a
+ * GPU looks up the array's device address (hipGetSymbolAddress) with that GPU
+ * current. */
+int32_t madd_multi_tensor_step_noalloc(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                                       void* const* scales, uint16_t* const* copy,
+                                       const void* const* g, int32_t gfmt, void* const* m,
+                                       void* const* v, void* const* ve, int32_t sfmt,
+                                       const int64_t* numel, int64_t index_base,
+                                       const madd_hparams* hp, void* stream);
 
 /* Hyper-parameters read from device memory when the kernels run, so that a
  * captured step (HIP graph) can be replayed step after step: the caller

@@ -31,11 +31,11 @@ SFMT = {"fp32": S_FP32, "bf16": S_BF16, "bf16_sr": S_BF16_SR}
 ROUND = {"rne": ROUND_RNE, "sr": ROUND_SR}
 
 STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPORTED",
-          -4: "MADD_EDEVICE", -5: "MADD_ENOMEM", -6: "MADD_ECAPTURE"}
+          -4: "MADD_EDEVICE", -5: "MADD_ENOMEM", -6: "MADD_ECAPTURE", -7: "MADD_ESCRATCH"}
 
 EXPORTS = ("madd_init_state", "madd_encode_weights", "madd_step", "madd_multi_tensor_step",
            "madd_plain_step", "madd_status_string", "madd_scalars_bytes", "madd_prepare_scalars",
-           "madd_multi_tensor_step_dev")
+           "madd_multi_tensor_step_dev", "madd_multi_tensor_step_noalloc")
 
 
 class MaddError(RuntimeError):
@@ -114,6 +114,8 @@ def lib():
         L.madd_multi_tensor_step.argtypes = [I32, PP, ctypes.POINTER(I32), PP, PP, PP, I32, PP, PP,
                                              PP, I32, ctypes.POINTER(I64), I64, HP, P]
         L.madd_multi_tensor_step.restype = I32
+        L.madd_multi_tensor_step_noalloc.argtypes = L.madd_multi_tensor_step.argtypes
+        L.madd_multi_tensor_step_noalloc.restype = I32
         L.madd_plain_step.argtypes = [P, I32, P, I32, I64, I64, HP, P]
         L.madd_plain_step.restype = I32
         L.madd_status_string.argtypes = [I32]
@@ -330,6 +332,22 @@ def madd_multi_tensor_step(tl: TensorList, hp, gfmt: str = "fp32", index_base: i
                                         cast(tl.g), GFMT[gfmt], cast(tl.m), cast(tl.v), cast(tl.ve),
                                         SFMT[tl.sfmt], tl.numel, int(index_base),
                                         ctypes.byref(h), _stream(stream)))
+
+
+def madd_multi_tensor_step_noalloc(tl: TensorList, hp, gfmt: str = "fp32", index_base: int = 0,
+                                   stream=None):
+    """madd_multi_tensor_step without device allocation: the descriptor
+    tables go to the library's fixed per-GPU array (at most 4096 tensors)."""
+    h = _hp(hp)
+    tl.check_grads(gfmt)
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    cast = lambda a: ctypes.cast(a, PP) if a is not None else None  # noqa: E731
+    _check("madd_multi_tensor_step_noalloc",
+           lib().madd_multi_tensor_step_noalloc(tl.n, cast(tl.w), tl.wfmt, cast(tl.scales),
+                                                cast(tl.copy), cast(tl.g), GFMT[gfmt],
+                                                cast(tl.m), cast(tl.v), cast(tl.ve),
+                                                SFMT[tl.sfmt], tl.numel, int(index_base),
+                                                ctypes.byref(h), _stream(stream)))
 
 
 def prepare_scalars(hp) -> bytes:

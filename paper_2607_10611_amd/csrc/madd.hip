@@ -1551,6 +1551,32 @@ struct HipTables {
 HipTables g_hip_tables;
 madd_cache::TableCache<HipTables> g_tables;
 
+// Descriptor tables of madd_multi_tensor_step_noalloc: a fixed device array,
+// one per GPU the library runs on, held until the process ends.  Every call on
+// a GPU rewrites it on its stream before its launches read it, so calls on one
+// GPU that overlap in time (other streams, other threads) race.
+constexpr int kScratchTensors = 4096;
+static __device__ __align__(256) TensorDesc scratch[kScratchTensors];
+
+// The array's device address on each GPU (host code must not pass the
+// array's name to a kernel: that is a host-side stand-in).  Looked up once per
+// device, with that device current.
+std::mutex g_scratch_mu;
+std::vector<TensorDesc*> g_scratch_ptr;
+
+int32_t scratch_on_device(int dev, TensorDesc** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (dev < 0) return MADD_EDEVICE;
+  if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MADD_EDEVICE;
+    g_scratch_ptr[dev] = (TensorDesc*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MADD_OK;
+}
+
 int32_t cache_status(int rc) {
   switch (rc) {
     case madd_cache::kOk: return MADD_OK;
@@ -1700,7 +1726,8 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
                                  const void* const* g, int32_t gfmt,
                                  void* const* m, void* const* v, void* const* ve, int32_t sfmt,
                                  const int64_t* numel, int64_t index_base,
-                                 const madd_hparams* hp, const Scalars* sdev, void* stream) {
+                                 const madd_hparams* hp, const Scalars* sdev, void* stream,
+                                 bool noalloc = false) {
   int32_t rc = check_hparams(hp);
   if (rc != MADD_OK) return rc;
   if (ntensors < 0 || !valid_gfmt(gfmt) || !valid_sfmt(sfmt) || index_base < 0)
@@ -1774,11 +1801,39 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     gr.nchunks = nch;
   }
   hipStream_t st = (hipStream_t)stream;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return MADD_EDEVICE;
+  TensorDesc none;
+  memset(&none, 0, sizeof(none));
+  if (noalloc) {
+    // The tables of every group, back to back in this GPU's scratch array,
+    // written on the stream ahead of the launches that read them.
+    size_t total = 0;
+    for (const Group& gr : groups) total += gr.descs.size();
+    if (total > (size_t)kScratchTensors) return MADD_ESCRATCH;
+    TensorDesc* base = nullptr;
+    rc = scratch_on_device(dev, &base);
+    if (rc != MADD_OK) return rc;
+    size_t off = 0;
+    for (Group& gr : groups) {
+      gr.table = base + off;
+      off += gr.descs.size();
+    }
+    for (const Group& gr : groups) {
+      rc = fill_device((void*)gr.table, gr.descs.data(), gr.descs.size() * sizeof(TensorDesc), st);
+      if (rc != MADD_OK) return rc;
+    }
+    for (const Group& gr : groups) {
+      const int ntab = (int)gr.descs.size();
+      rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
+                 : launch_nvcs(gr.nvcs, gr.table, ntab, none, gr.nchunks, s, sdev, st);
+      if (rc != MADD_OK) return rc;
+    }
+    return MADD_OK;
+  }
   bool cap = false;
   rc = capturing(st, &cap);
   if (rc != MADD_OK) return rc;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return MADD_EDEVICE;
   size_t acquired = 0;
   for (; acquired < groups.size(); ++acquired) {
     Group& gr = groups[acquired];
@@ -1789,8 +1844,6 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     if (rc != MADD_OK) break;
     gr.table = (const TensorDesc*)t;
   }
-  TensorDesc none;
-  memset(&none, 0, sizeof(none));
   for (size_t k = 0; k < acquired && rc == MADD_OK; ++k) {
     const Group& gr = groups[k];
     const int ntab = (int)gr.descs.size();
@@ -1817,6 +1870,9 @@ const char* madd_status_string(int32_t status) {
     case MADD_EUNSUPPORTED: return "MADD_EUNSUPPORTED: request not implemented";
     case MADD_EDEVICE: return "MADD_EDEVICE: HIP runtime or launch failure";
     case MADD_ENOMEM: return "MADD_ENOMEM: device allocation failed";
+    case MADD_ESCRATCH:
+      return "MADD_ESCRATCH: more tensors than the allocation-free step's fixed table holds "
+             "(4096)";
     case MADD_ECAPTURE:
       return "MADD_ECAPTURE: a tensor list's first step cannot run inside a graph capture "
              "(step it once outside the capture)";
@@ -2003,6 +2059,16 @@ int32_t madd_multi_tensor_step_dev(int32_t ntensors, void* const* w, const int32
   if (((uintptr_t)dev_scalars & 3u) != 0) return MADD_EALIGN;
   return multi_tensor_step(ntensors, w, wfmt, scales, copy, g, gfmt, m, v, ve, sfmt, numel,
                            index_base, hp, (const Scalars*)dev_scalars, stream);
+}
+
+int32_t madd_multi_tensor_step_noalloc(int32_t ntensors, void* const* w, const int32_t* wfmt,
+                                       void* const* scales, uint16_t* const* copy,
+                                       const void* const* g, int32_t gfmt, void* const* m,
+                                       void* const* v, void* const* ve, int32_t sfmt,
+                                       const int64_t* numel, int64_t index_base,
+                                       const madd_hparams* hp, void* stream) {
+  return multi_tensor_step(ntensors, w, wfmt, scales, copy, g, gfmt, m, v, ve, sfmt, numel,
+                           index_base, hp, nullptr, stream, true);
 }
 
 }  // extern "C"
