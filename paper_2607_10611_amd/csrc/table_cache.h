@@ -5,25 +5,28 @@
 // the tensors (pointers, sizes, index bases).  Lists repeat from one training
 // step to the next, so tables are kept by content and a repeated list enqueues
 // only its kernels.  Rules:
-//   - A hit returns the cached device table; nothing is uploaded.
+//   - A hit returns the cached device table; nothing is uploaded.  The entry
+//     remembers the stream of its latest use.
 //   - A miss uploads the table asynchronously on the caller's stream (the
 //     backend's upload is stream-ordered, so the launches that follow on that
-//     stream see it).  Any later step of the same tensors must already be
-//     ordered after this one by the caller (both update the same buffers), so
-//     it is ordered after the upload as well.
-//   - At most kMaxUnpinned unpinned tables per device.  On a miss past that
-//     limit the least recently used unpinned table is recycled: the host
-//     waits for the event recorded after that table's last launch (only that
-//     launch, not the device), then reuses its memory when large enough, or
-//     frees it and allocates anew.  A table between acquire() and release()
-//     (its launches not yet enqueued) is never recycled; when every table is
-//     pinned or held the cache grows instead.
+//     stream see it).
+//   - Recycling needs no event and no host wait: a table is only ever
+//     recycled by a call on the stream of its latest use, so the new upload is
+//     queued behind every launch that read it there.  Launches of the same
+//     table on other streams came earlier and were ordered before that latest
+//     one by the caller, who must order any two steps of the same tensors
+//     (both update the same buffers).
+//   - Up to kMaxUnpinned unpinned tables per (device, stream); a miss past that
+//     recycles the least recently used idle table of that stream whose memory
+//     is large enough, else it allocates a new one.  Memory is never freed,
+//     so nothing ever waits for the device.
+//   - A table between acquire() and release() (its launches not yet
+//     enqueued) is never recycled.
 //   - A table hit while the caller's stream is capturing a graph is pinned:
-//     the graph holds its address, so it is never recycled or freed.
-//   - A miss while capturing is refused (kCaptureMiss): allocating, uploading
-//     or waiting inside a capture would break it or record work the replays
-//     repeat.  The caller steps the list once outside the capture first.
-//   - Events are recorded only outside captures (pinned tables need none).
+//     the graph holds its address, so it is never recycled.
+//   - A miss while capturing is refused (kCaptureMiss): allocating or
+//     uploading inside a capture would break it or add work to every replay.
+//     The caller steps the list once outside the capture first.
 #ifndef MADD_TABLE_CACHE_H
 #define MADD_TABLE_CACHE_H
 
@@ -39,42 +42,47 @@ namespace madd_cache {
 enum Status : int { kOk = 0, kCaptureMiss = 1, kNoMem = 2, kDevice = 3 };
 
 // Backend interface (duck-typed):
-//   using Event = ...;                      copyable handle
 //   bool alloc(size_t bytes, void** p);     device memory on the current device
-//   void free(void* p);
 //   bool upload(void* dst, const void* src, size_t bytes, void* stream);  async, stream-ordered
-//   bool new_event(Event* e);
-//   bool record(Event e, void* stream);
-//   bool wait(Event e);                     host waits until e has completed
 template <class Backend>
 class TableCache {
  public:
   static constexpr size_t kMaxUnpinned = 32;
-  static constexpr size_t kGranule = 64 * 88;  // capacity rounding (64 descriptors)
+  static constexpr size_t kMinCap = 64 * 88;  // smallest table capacity (64 descriptors)
 
   struct Entry {
     int device;
-    std::vector<uint8_t> key;  // the table's bytes
+    uint64_t stream;           // identity of the stream of the latest use
+    std::vector<uint8_t> key;  // the table's bytes; empty while being refilled
     void* mem;
     size_t cap;
     uint64_t last_use;
     bool pinned;
-    bool has_event;
     int holds;  // acquire() calls not yet released
-    typename Backend::Event ev;
   };
 
-  // The device table for `bytes`; `*slot` identifies the entry, which the
-  // caller passes to release() once the launches reading it are enqueued
-  // (or have failed).  Entries are never removed, so a slot stays valid.
-  int acquire(Backend& be, int device, const void* bytes, size_t nbytes, bool capturing,
-              void* stream, void** out, size_t* slot) {
+  // Capacity class of a table of `bytes`: a power-of-two multiple of kMinCap.
+  static size_t capacity_for(size_t bytes) {
+    size_t c = kMinCap;
+    while (c < bytes) c *= 2;
+    return c;
+  }
+
+  // The device table for `bytes`, used on the stream identified by `stream`
+  // (`stream_handle` is passed to the backend's upload).  `*slot` identifies
+  // the entry, which the caller passes to release() once the launches reading
+  // it are enqueued (or have failed).  Entries are never removed, so a slot
+  // stays valid.
+  int acquire(Backend& be, int device, uint64_t stream, const void* bytes, size_t nbytes,
+              bool capturing, void* stream_handle, void** out, size_t* slot) {
     std::lock_guard<std::mutex> lock(mu_);
     ++clock_;
     for (size_t i = 0; i < entries_.size(); ++i) {
       Entry& e = entries_[i];
-      if (e.device == device && e.key.size() == nbytes && memcmp(e.key.data(), bytes, nbytes) == 0) {
+      if (e.device == device && e.key.size() == nbytes &&
+          memcmp(e.key.data(), bytes, nbytes) == 0) {
         e.last_use = clock_;
+        e.stream = stream;
         if (capturing) e.pinned = true;
         ++e.holds;
         *out = e.mem;
@@ -83,51 +91,34 @@ class TableCache {
       }
     }
     if (capturing) return kCaptureMiss;
-    const size_t cap = (nbytes + kGranule - 1) / kGranule * kGranule;
-    size_t unpinned = 0, victim = entries_.size();
+    const size_t cap = capacity_for(nbytes);
+    size_t same = 0, victim = entries_.size();
     for (size_t i = 0; i < entries_.size(); ++i) {
       const Entry& e = entries_[i];
-      if (e.device != device || e.pinned) continue;
-      ++unpinned;
-      if (e.holds > 0) continue;
+      if (e.device != device || e.stream != stream || e.pinned) continue;
+      ++same;
+      if (e.holds > 0 || e.cap < cap) continue;
       if (victim == entries_.size() || e.last_use < entries_[victim].last_use) victim = i;
     }
     size_t idx;
-    if (unpinned >= kMaxUnpinned && victim < entries_.size()) {
-      Entry& v = entries_[victim];
-      if (v.has_event && !be.wait(v.ev)) return kDevice;
-      v.has_event = false;
-      v.key.clear();  // matches nothing until refilled
-      if (v.cap < cap) {
-        be.free(v.mem);
-        v.mem = nullptr;
-        v.cap = 0;
-        if (!be.alloc(cap, &v.mem)) {
-          v.mem = nullptr;
-          return kNoMem;
-        }
-        v.cap = cap;
-      }
+    if (same >= kMaxUnpinned && victim < entries_.size()) {
       idx = victim;
     } else {
       Entry e;
       e.device = device;
+      e.stream = stream;
       e.mem = nullptr;
       e.cap = cap;
       e.pinned = false;
-      e.has_event = false;
       e.holds = 0;
       if (!be.alloc(cap, &e.mem)) return kNoMem;
-      if (!be.new_event(&e.ev)) {
-        be.free(e.mem);
-        return kDevice;
-      }
       entries_.push_back(e);
       idx = entries_.size() - 1;
     }
     Entry& e = entries_[idx];
+    e.key.clear();  // matches nothing unless the upload is enqueued
     e.last_use = clock_;
-    if (!be.upload(e.mem, bytes, nbytes, stream)) return kDevice;
+    if (!be.upload(e.mem, bytes, nbytes, stream_handle)) return kDevice;
     e.key.assign((const uint8_t*)bytes, (const uint8_t*)bytes + nbytes);
     ++e.holds;
     *out = e.mem;
@@ -135,18 +126,10 @@ class TableCache {
     return kOk;
   }
 
-  // The launches that read the table of `slot` are enqueued on `stream`
-  // (launched = true) or were not (an error): outside a capture, record the
-  // event a later recycling waits for.
-  int release(Backend& be, size_t slot, bool capturing, void* stream, bool launched) {
+  // The launches that read the table of `slot` are enqueued (or failed).
+  void release(size_t slot) {
     std::lock_guard<std::mutex> lock(mu_);
-    if (slot >= entries_.size()) return kOk;
-    Entry& e = entries_[slot];
-    if (e.holds > 0) --e.holds;
-    if (capturing || !launched || e.pinned) return kOk;
-    if (!be.record(e.ev, stream)) return kDevice;
-    e.has_event = true;
-    return kOk;
+    if (slot < entries_.size() && entries_[slot].holds > 0) --entries_[slot].holds;
   }
 
   // Introspection for tests.

@@ -150,40 +150,9 @@ def oracle_step(wfmt, hs: HostState, g, hp, gfmt="fp32", index_base=0, gidx=None
                     gidx=gidx, sfmt=hs.sfmt, copy=hs.copy)
 
 
-# A call over fewer than 4096 chunks of 2048 elements gives each workgroup
-# one 1024-element sub-tile instead of two (more workgroups for small
-# calls).  Small parity cases cover the two-sub-tile mapping by sharing
-# their call with a pad tensor large enough to switch to it.
-PAD_N = 4096 * 2048
-_PADS = {}
-
-
-def _pad(gfmt, sfmt):
-    if (gfmt, sfmt) not in _PADS:
-        st = STATE_T[sfmt]
-        _PADS[(gfmt, sfmt)] = dict(
-            w=torch.zeros(PAD_N, dtype=torch.int16, device="cuda"),
-            g=torch.zeros(PAD_N, dtype=torch.float32 if gfmt == "fp32" else torch.int16,
-                          device="cuda"),
-            m=torch.zeros(PAD_N, dtype=st, device="cuda"),
-            v=torch.zeros(PAD_N, dtype=st, device="cuda"),
-            ve=torch.zeros(PAD_N, dtype=st, device="cuda"))
-    return _PADS[(gfmt, sfmt)]
-
-
-def gpu_step(ds: DevState, g_dev, hp, gfmt="fp32", index_base=0, full_chunks=False):
-    """One step of ds on the GPU: madd_step, or with full_chunks a
-    multi-tensor call of ds followed by a bf16 pad tensor, which runs the
-    two-sub-tile workgroups on ds (same bits: draws are keyed by index)."""
-    if not full_chunks:
-        B.madd_step(ds.w, ds.wfmt, g_dev, ds.m, ds.v, ds.ve, hp, gfmt=gfmt, scales=ds.scales,
-                    index_base=index_base, sfmt=ds.sfmt, copy=ds.copy)
-        return
-    p = _pad(gfmt, ds.sfmt)
-    tl = B.TensorList([ds.w, p["w"]], [ds.wfmt, "bf16"], [g_dev, p["g"]], [ds.m, p["m"]],
-                      [ds.v, p["v"]], [ds.ve, p["ve"]], scales=[ds.scales, None],
-                      copies=[ds.copy, None], sfmt=ds.sfmt)
-    B.madd_multi_tensor_step(tl, hp, gfmt=gfmt, index_base=index_base)
+def gpu_step(ds: DevState, g_dev, hp, gfmt="fp32", index_base=0):
+    B.madd_step(ds.w, ds.wfmt, g_dev, ds.m, ds.v, ds.ve, hp, gfmt=gfmt, scales=ds.scales,
+                index_base=index_base, sfmt=ds.sfmt, copy=ds.copy)
 
 
 def assert_copy_equal(tag, ds: DevState, hs: HostState):

@@ -93,8 +93,7 @@ def start_state(rng, wfmt, sfmt, n, state):
     return codes, mom
 
 
-def run(wfmt, sfmt, state, grads, h_list, n=4 * 2048 + 1000 + 5, index_base=0, seed=0,
-        full_chunks=False):
+def run(wfmt, sfmt, state, grads, h_list, n=4 * 2048 + 1000 + 5, index_base=0, seed=0):
     rng = np.random.default_rng(seed)
     codes, mom = start_state(rng, wfmt, sfmt, n, state)
     ds = DevState(wfmt, codes, n, sfmt=sfmt)
@@ -107,7 +106,7 @@ def run(wfmt, sfmt, state, grads, h_list, n=4 * 2048 + 1000 + 5, index_base=0, s
             g = full_range_f32(rng, n)
         else:
             g = (rng.normal(0, 1, n) * 10.0 ** rng.uniform(-6, -1, n)).astype(np.float32)
-        gpu_step(ds, to_dev(g), h, index_base=index_base, full_chunks=full_chunks)
+        gpu_step(ds, to_dev(g), h, index_base=index_base)
         oracle_step(wfmt, hs, g.copy(), h, index_base=index_base)
         torch.cuda.synchronize()
         w_g, m_g, v_g, ve_g = ds.host()
@@ -131,15 +130,14 @@ HPARAM_SETS = {
                                          ("full", "full"), ("zero_v", "normal")])
 def test_full_range_fp32_moments(wfmt, hset, state, grads):
     seed = zlib.crc32(f"{wfmt} {hset} {state}".encode())
-    run(wfmt, "fp32", state, grads, HPARAM_SETS[hset], seed=seed, full_chunks=seed % 2 == 1)
+    run(wfmt, "fp32", state, grads, HPARAM_SETS[hset], seed=seed)
 
 
 @pytest.mark.parametrize("wfmt", ["fp32", "bf16"])
 @pytest.mark.parametrize("sfmt", ["bf16", "bf16_sr"])
 @pytest.mark.parametrize("state,grads", [("full", "normal"), ("full", "full")])
 def test_full_range_bf16_moments(wfmt, sfmt, state, grads):
-    run(wfmt, sfmt, state, grads, HPARAM_SETS["default"] + HPARAM_SETS["eps0"][:1], seed=31,
-        full_chunks=state == "full")
+    run(wfmt, sfmt, state, grads, HPARAM_SETS["default"] + HPARAM_SETS["eps0"][:1], seed=31)
 
 
 def test_full_range_unaligned_index_base_per_element_path():

@@ -226,3 +226,33 @@ def test_list_first_seen_during_capture_is_refused():
     B.madd_multi_tensor_step(tlb, h)
     torch.cuda.synchronize()
     assert_lists_equal(a, b, "eager after refusal")
+
+
+def test_allocation_free_step_captures_a_list_never_stepped_before():
+    """madd_multi_tensor_step_noalloc writes its tables on the stream, so a
+    graph can capture a list the library has never seen; each replay rewrites
+    the tables and equals an eager step, with other lists stepped through the
+    same entry point (same fixed table array) between the replays."""
+    a, fmts = state(10)
+    b, _ = state(10)
+    tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
+    h = W.hparams("c2", step=4)
+    others = other_lists(3)
+    B.madd_multi_tensor_step_noalloc(others[0], W.hparams("c2", step=1))  # first call on the GPU
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        B.madd_multi_tensor_step_noalloc(tla, h)
+    gen = torch.Generator(device="cuda")
+    for r in range(3):
+        for tl in others:
+            B.madd_multi_tensor_step_noalloc(tl, W.hparams("c2", step=r + 1))
+        gen.manual_seed(70 + r)
+        for ga, gb in zip(a["g"], b["g"]):
+            ga.normal_(0, 1e-3, generator=gen)
+            gb.copy_(ga)
+        torch.cuda.synchronize()
+        graph.replay()
+        B.madd_multi_tensor_step(tlb, h)
+        torch.cuda.synchronize()
+        assert_lists_equal(a, b, f"replay {r}")

@@ -74,7 +74,7 @@ def check(tag, ds, hs):
 
 
 def run_mx(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
-           grad=mx_grad, full=False):
+           grad=mx_grad):
     rng = np.random.default_rng(seed)
     q, s = encode_mx_both(mx_weights(rng, n))
     ds = DevState("mxfp4", q, n, s, sfmt=sfmt, copy=copy)
@@ -84,7 +84,7 @@ def run_mx(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=Fa
         if gfmt == "bf16":
             g = oracle.encode_array("bf16", g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base, full_chunks=full)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
         oracle_step("mxfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
         torch.cuda.synchronize()
         check(f"mxfp4 n={n} t={t}", ds, hs)
@@ -101,14 +101,12 @@ def test_encode_matches_oracle():
     encode_mx_both(x)
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
                                                  ("sr", "bf16", True), ("rne", "bf16", False),
                                                  ("sr", "bf16_sr", True)])
-def test_step_tiles_and_ragged_tail(rounding, sfmt, copy, full):
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
     # five whole 2048-element tiles, then 3 blocks of a sixth
-    run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy,
-           full=full)
+    run_mx(5 * 8192 + 3 * 32, 4, 11, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
 
 
 @pytest.mark.parametrize("n", [32, 64, 992, 2048 + 32, 4096 + 1024 + 96])

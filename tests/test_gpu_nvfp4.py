@@ -75,7 +75,7 @@ def check(tag, ds, hs):
 
 
 def run_nv(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=False,
-           grad=nv_grad, full=False):
+           grad=nv_grad):
     rng = np.random.default_rng(seed)
     q, s = encode_nv_both(nv_weights(rng, n))
     ds = DevState("nvfp4", q, n, s, sfmt=sfmt, copy=copy)
@@ -85,7 +85,7 @@ def run_nv(n, steps, seed, hpkw, gfmt="fp32", index_base=0, sfmt="fp32", copy=Fa
         if gfmt == "bf16":
             g = oracle.encode_array("bf16", g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base, full_chunks=full)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
         oracle_step("nvfp4", hs, g, h, gfmt=gfmt, index_base=index_base)
         torch.cuda.synchronize()
         check(f"nvfp4 n={n} t={t}", ds, hs)
@@ -101,12 +101,10 @@ def test_encode_matches_oracle():
     encode_nv_both(np.zeros(64, np.float32))        # no finite nonzero value: st = 1
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
                                                  ("sr", "bf16", True), ("sr", "bf16_sr", True)])
-def test_step_tiles_and_ragged_tail(rounding, sfmt, copy, full):
-    run_nv(5 * 8192 + 7 * 16, 4, 32, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy,
-           full=full)
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+    run_nv(5 * 8192 + 7 * 16, 4, 32, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
 
 
 @pytest.mark.parametrize("n", [16, 48, 1008, 2048 + 16, 4096 + 1024 + 80])

@@ -85,8 +85,7 @@ def check(tag, ds, hs, g_dev, g_host):
     assert_copy_equal(tag, ds, hs)
 
 
-def run_cs(n, steps, seed, hpkw, index_base=0, sfmt="fp32", copy=False, gradf=grad,
-           full=False):
+def run_cs(n, steps, seed, hpkw, index_base=0, sfmt="fp32", copy=False, gradf=grad):
     rng = np.random.default_rng(seed)
     q, s = encode_both(weights(rng, n))
     ds = DevState(FMT, q, n, s, sfmt=sfmt, copy=copy)
@@ -95,7 +94,7 @@ def run_cs(n, steps, seed, hpkw, index_base=0, sfmt="fp32", copy=False, gradf=gr
         g = gradf(rng, n)
         g_dev = to_dev(g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, g_dev, h, index_base=index_base, full_chunks=full)
+        gpu_step(ds, g_dev, h, index_base=index_base)
         oracle_step(FMT, hs, g, h, index_base=index_base)
         torch.cuda.synchronize()
         check(f"{FMT} n={n} t={t}", ds, hs, g_dev, g)
@@ -109,12 +108,10 @@ def test_encode_matches_oracle():
     encode_both(x)
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("rounding,sfmt,copy", [("rne", "fp32", False), ("sr", "fp32", True),
                                                  ("sr", "bf16", True), ("sr", "bf16_sr", True)])
-def test_step_tiles_and_ragged_tail(rounding, sfmt, copy, full):
-    run_cs(5 * 8192 + 7 * 16, 4, 42, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy,
-           full=full)
+def test_step_tiles_and_ragged_tail(rounding, sfmt, copy):
+    run_cs(5 * 8192 + 7 * 16, 4, 42, dict(rounding=rounding, lr_add=1e-2), sfmt=sfmt, copy=copy)
 
 
 @pytest.mark.parametrize("n", [16, 48, 1008, 2048 + 16, 4096 + 1024 + 80])

@@ -80,9 +80,7 @@ def encode_both(wfmt, x, block=False):
 
 
 def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False, sfmt="fp32",
-             copy=False, full=False):
-    """`full`: step in a call large enough for two-sub-tile workgroups (see
-    gpu_parity_util.gpu_step); otherwise the small-call mapping."""
+             copy=False):
     rng = np.random.default_rng(seed)
     x = random_weights(rng, n, wfmt)
     enc = encode_both(wfmt, x, block)
@@ -94,7 +92,7 @@ def run_pair(wfmt, n, steps, seed, hpkw, gfmt="fp32", index_base=0, block=False,
         if gfmt == "bf16":
             g = oracle.encode_array("bf16", g)
         h = hp(step=t, **hpkw)
-        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base, full_chunks=full)
+        gpu_step(ds, to_dev(g), h, gfmt=gfmt, index_base=index_base)
         oracle_step(wfmt, hs, g, h, gfmt=gfmt, index_base=index_base)
         torch.cuda.synchronize()
         w_g, m_g, v_g, ve_g = ds.host()
@@ -130,10 +128,9 @@ def test_fp32_passthrough_unrounded_step_is_bit_exact(bias_correction):
     run_pair("fp32", 3 * 2048 + 77, 6, 11, dict(rounding="rne", bias_correction=bias_correction))
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("n", [1, 7, 8, 9, 127, 1023, 1025, 2047, 2049, 8191, 8193, 65536 + 13])
-def test_ragged_sizes_sr(n, full):
-    run_pair("bf16", n, 3, 100 + n, dict(rounding="sr", seed=77), index_base=12345, full=full)
+def test_ragged_sizes_sr(n):
+    run_pair("bf16", n, 3, 100 + n, dict(rounding="sr", seed=77), index_base=12345)
 
 
 @pytest.mark.parametrize("index_base", [0, 3, 8, 2 ** 33 + 5])
@@ -141,19 +138,16 @@ def test_index_base_keys_the_draws(index_base):
     run_pair("bf16", 4096 + 40, 2, 5, dict(rounding="sr", seed=2 ** 40 + 1), index_base=index_base)
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
 @pytest.mark.parametrize("rounding", ["rne", "sr"])
-def test_fp8_storage(wfmt, rounding, full):
-    run_pair(wfmt, 3 * 8192 + 24, 4, 21, dict(rounding=rounding, lr_add=3e-3, lr_mul=5e-3),
-             full=full)
+def test_fp8_storage(wfmt, rounding):
+    run_pair(wfmt, 3 * 8192 + 24, 4, 21, dict(rounding=rounding, lr_add=3e-3, lr_mul=5e-3))
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("wfmt", ["e4m3", "e5m2"])
 @pytest.mark.parametrize("rounding", ["rne", "sr"])
-def test_block_scaled_fp8(wfmt, rounding, full):
-    run_pair(wfmt, 5 * 8192 + 3 * 128, 4, 31, dict(rounding=rounding), block=True, full=full)
+def test_block_scaled_fp8(wfmt, rounding):
+    run_pair(wfmt, 5 * 8192 + 3 * 128, 4, 31, dict(rounding=rounding), block=True)
 
 
 def test_bf16_gradients():
@@ -166,24 +160,20 @@ def test_bf16_moments(wfmt, n):
     run_pair(wfmt, n, 4, 43 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16", index_base=16)
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("wfmt", ["bf16", "e4m3"])
 @pytest.mark.parametrize("n,base", [(1036, 0), (2047, 8), (4095, 2 ** 33 + 16),
                                     (3 * 2048 + 1024 + 20, 64), (1024 + 20, 8), (516, 0)])
-def test_aligned_ragged_tails_split_lane_pairs(wfmt, n, base, full):
+def test_aligned_ragged_tails_split_lane_pairs(wfmt, n, base):
     """Aligned index bases with a last tile that ends inside a lane pair's
-    group (of sub-tile B in two-sub-tile workgroups, of the only sub-tile in
-    one-sub-tile workgroups): the pair must take the per-element path
+    group of sub-tile A or B: the pair must take the per-element path
     together (the two lanes share Philox blocks)."""
-    run_pair(wfmt, n, 3, 70 + n, dict(rounding="sr", seed=91), index_base=base, full=full)
+    run_pair(wfmt, n, 3, 70 + n, dict(rounding="sr", seed=91), index_base=base)
 
 
-@pytest.mark.parametrize("full", [False, True])
 @pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "fp32"])
 @pytest.mark.parametrize("n,base", [(9, 16), (2047, 16), (3 * 8192 + 24, 16), (5000, 3)])
-def test_bf16_sr_moments(wfmt, n, base, full):
-    run_pair(wfmt, n, 4, 60 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16_sr", index_base=base,
-             full=full)
+def test_bf16_sr_moments(wfmt, n, base):
+    run_pair(wfmt, n, 4, 60 + n, dict(rounding="sr", lr_mul=5e-3), sfmt="bf16_sr", index_base=base)
 
 
 def test_bf16_sr_moments_with_nearest_weights_and_bf16_gradients():

@@ -1,13 +1,14 @@
 """The descriptor-table cache policy of the multi-tensor step, on the host
 (no GPU): the policy header the HIP library compiles is built with g++
-against a fake backend that logs allocations, frees, uploads, event records
-and host waits (tests/table_cache_test.cpp).  Checked: a repeated list
-uploads nothing; recycling takes the least recently used unpinned table and
-waits for that table's last launch before overwriting it; a table used
-while a stream captures a graph is pinned and survives 40 further lists;
-a list first seen during a capture is refused with no allocation, upload or
-wait; tables whose launches are not yet enqueued are never recycled; devices
-keep separate caches."""
+against a fake backend that logs allocations and uploads
+(tests/table_cache_test.cpp).  Checked: a repeated list uploads nothing; a
+table is recycled only by a call on the stream of its latest use (so the
+rewrite is queued behind every launch that read it), the least recently
+used idle table of that stream with enough room; a table used while a
+stream captures a graph is pinned and survives 40 further lists; a list
+first seen during a capture is refused with no allocation or upload;
+tables whose launches are not yet enqueued are never recycled; devices keep
+separate caches; nothing is ever freed or waited for."""
 import os
 import subprocess
 
