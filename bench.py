@@ -12,8 +12,8 @@ synthetic: for the 7B list the gradient buffer is filled anew on the device
 from each step's seeds before the step (outside the timed events; each step
 is bracketed by its own pair of events on the launching stream); the smaller
 lists cycle through up to eight sets made up front, with the steps queued
-back to back behind a short GPU-side delay so that the events between them
-time the GPU alone.
+back to back behind a short GPU-side delay and timed by one pair of events
+around them, so that the events time the GPU alone.
 
 Prints one JSON line with optimizer-step throughput (Gparam/s), the achieved
 HBM bandwidth of the step kernel against the 8 TB/s peak, and the CPU oracle
@@ -414,15 +414,17 @@ def main():
         torch.cuda.synchronize()
         per_launch_ms = [a.elapsed_time(b) for a, b in ev]
     else:
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        # one pair of events around the back-to-back steps: an event between
+        # two short launches costs the stream a few microseconds of its own
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         gpu_delay(stream, args.steps)
         ev[0].record(stream)
         for k in range(args.steps):
             step_no += 1
             one_step()
-            ev[k + 1].record(stream)
+        ev[1].record(stream)
         torch.cuda.synchronize()
-        per_launch_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
+        per_launch_ms = [ev[0].elapsed_time(ev[1]) / args.steps] * args.steps
     wall = time.perf_counter() - wall0
     ms_per_step = sum(per_launch_ms) / args.steps
     avg_launch_ms = ms_per_step
@@ -471,9 +473,9 @@ def main():
     else:
         low = LOW_MASTER[args.weights]
         if low == "nvfp4_current":
-            kname = ("nvcs_clear_kernel + nvcs_pass1_kernel + nvcs_pass2_kernel (NVFP4 with "
-                     "current scaling) + madd_step_kernel<bf16> (four launches per step; timed "
-                     "together)")
+            kname = ("nvcs_clear_kernel + nvcs_step_kernel (NVFP4 with current scaling: the "
+                     "two passes pipelined over groups of tensors) + madd_step_kernel<bf16> "
+                     "(timed together)")
         else:
             kname = (f"madd_step_block_kernel<{low}> + madd_step_kernel<bf16> (two launches per "
                      "step; timed together)")

@@ -31,8 +31,8 @@
  *     pointers owned by the caller.  Pointer arrays, numel arrays and the
  *     hyper-parameter struct are HOST memory, read during the call only.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *     Work is enqueued asynchronously on it; no call synchronizes the
- *     device.  The only host waits and device allocations are those of
+ *     Work is enqueued asynchronously on it; no call synchronizes the host
+ *     or the device.  The only device allocations are those of
  *     madd_multi_tensor_step's descriptor-table cache (see that function).
  *   - A failed launch is reported as MADD_EDEVICE from the launch's own
  *     return status; the calling thread's HIP last-error state is neither
@@ -228,11 +228,13 @@ int32_t madd_encode_weights(const float* x, void* w, int32_t wfmt, void* scales,
  *           per-tensor scale st is read and kept (re-encode to refresh it);
  *           NVFP4_CURRENT derives st' = fp32(amax / 2688) over the finite
  *           |w'| of the whole tensor (1 when none is nonzero), stores it and
- *           the amax bits, and re-encodes every block with st'.  It takes
- *           three launches: clear the amax word, pass 1 (the FP32 step:
- *           moments stored, w' written over g, amax folded in with atomics),
- *           pass 2 (block codes and payloads from w' and st').  gfmt must be
- *           FP32 (else MADD_EINVAL) and g is overwritten.
+ *           the amax bits, and re-encodes every block with st'.  It runs
+ *           in two passes: pass 1 (the FP32 step: moments stored, w' written
+ *           over g, amax folded in with atomics) and pass 2 (block codes and
+ *           payloads from w' and st'), after a launch that clears the amax
+ *           words.  In a multi-tensor call, pass 2 of one group of tensors
+ *           runs in the same launch as pass 1 of the next group.  gfmt must
+ *           be FP32 (else MADD_EINVAL) and g is overwritten.
  *           Requires n % 128 == 0 (FP8), n % 32 == 0 (MXFP4) or n % 16 == 0
  *           (NVFP4, NVFP4_CURRENT) and 16-byte-aligned w, g, m, v, ve and
  *           copy, and a 4-byte-aligned NVFP4 scale array (else MADD_EINVAL /
@@ -270,18 +272,22 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
  *   - The first call with a given list (same pointers and sizes) allocates
  *     the table's device memory (hipMalloc) and writes it on `stream` with a
  *     small kernel (asynchronous); later calls with the same list enqueue
- *     only the step kernels.
- *   - At most 32 lists per device are cached besides pinned ones.  A new list
- *     past that recycles the least recently used table: the host waits for
- *     the last launch that read it (an event recorded after that launch, not
- *     a device-wide synchronization), then reuses its memory, or frees it
- *     when too small for the new list.
+ *     only the step kernels.  Nothing records events, waits on the host or
+ *     frees memory.
+ *   - Up to 32 lists per (device, stream) are cached besides pinned ones; a
+ *     new list past that rewrites the least recently used table whose latest
+ *     use was on the same stream, so the rewrite is queued behind every
+ *     launch that read it there (launches of it on other streams came
+ *     earlier and were ordered before that one by the caller, who must order
+ *     two steps of the same tensors anyway).  Otherwise a new table is
+ *     allocated.
  *   - Graph capture.  A call made while `stream` is capturing a graph only
- *     enqueues kernels, and its tables are pinned: never recycled or freed
+ *     enqueues kernels, and its tables are pinned: never rewritten or freed
  *     until the process ends, so every replay of the graph reads a live,
  *     unchanged table.  A list must have been stepped once outside the
  *     capture; a list first seen during a capture returns MADD_ECAPTURE and
- *     enqueues nothing (no allocation or upload inside a capture).  No call
+ *     enqueues nothing (no allocation or upload inside a capture; the
+ *     allocation-free entry point below has no such restriction).  No call
  *     records a memset.  The hyper-parameters, step counter included, are
  *     kernel arguments fixed at capture (see madd_multi_tensor_step_dev for
  *     replaying successive steps). */
@@ -306,7 +312,7 @@ int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* 
  * can run at the same time (different streams or threads, or graphs replayed
  * concurrently) race and must be ordered by the caller.  The first call on a
  * GPU looks up the array's device address (hipGetSymbolAddress) with that GPU
- * current. */
+ * current; make that first call outside a graph capture. */
 int32_t madd_multi_tensor_step_noalloc(int32_t ntensors, void* const* w, const int32_t* wfmt,
                                        void* const* scales, uint16_t* const* copy,
                                        const void* const* g, int32_t gfmt, void* const* m,

@@ -42,6 +42,7 @@
 #include <cmath>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <tuple>
 #include <utility>
@@ -68,12 +69,7 @@ constexpr int kQuad = 4;                     // consecutive elements per thread 
 constexpr int kSub = kThreads * kQuad;       // 1024 elements per sub-tile
 constexpr int kTile = 2 * kSub;              // sub-tiles A and B
 constexpr int kTilesPerChunk = 1;
-[[maybe_unused]] constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
-// Launches of fewer chunks than this (fewer than 16 workgroups per CU) give
-// each workgroup one sub-tile instead of two: twice the workgroups, each
-// thread one quad, so that one wave's arithmetic overlaps other waves'
-// memory traffic when there is too little work to hide it otherwise.
-[[maybe_unused]] constexpr int64_t kSmallLaunchChunks = 4096;
+constexpr int64_t kChunk = (int64_t)kTile * kTilesPerChunk;
 constexpr int kBlock = 128;                  // block-scaled FP8 block length
 constexpr int kMxBlock = 32;                 // MXFP4 block length (OCP MX)
 constexpr int kNvBlock = 16;                 // NVFP4 block length
@@ -106,7 +102,13 @@ struct TensorDesc {
   int64_t gbase;   // global index of element 0
   int64_t chunk0;  // first chunk of this tensor within the launch
   int32_t vec_ok;  // buffers 16-byte aligned and gbase a multiple of 8
-  int32_t chunk_len;  // elements per chunk: kChunk, or kSub for small launches
+  int32_t pad;
+};
+
+// Chunk ranges of one launch of NVFP4 current scaling (nvcs_step_kernel):
+// pass 1 over [a1, a1 + n1), pass 2 over [a2, a2 + n2).
+struct NvcsSpan {
+  int64_t a1, n1, a2, n2;
 };
 
 typedef float f4 __attribute__((ext_vector_type(4)));
@@ -721,8 +723,8 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
   const Scalars s = sdev ? *sdev : s_arg;  // uniform: device-resident hyper-parameters
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
-  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
-  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
     const int64_t tb = c0 + (int64_t)tile * kTile;
@@ -922,8 +924,8 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
   const int64_t chunk = blockIdx.x;
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float st = WF == WF_NVFP4 ? *(const float*)d.scales : 1.0f;  // NVFP4 tensor scale
-  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
-  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
 #pragma unroll 1
   for (int tile = 0; tile < kTilesPerChunk; ++tile) {
     const int64_t tb = c0 + (int64_t)tile * kTile;
@@ -974,10 +976,13 @@ __global__ __launch_bounds__(kThreads) void madd_step_block_kernel(
 
 // ---------------------------------------------------------------------------
 // NVFP4 with current scaling: the per-tensor scale derived anew from the
-// updated tensor at every step.  Three launches: clear each tensor's amax
-// word; pass 1 takes the FP32 step (moments stored, w' written over the fp32
+// updated tensor at every step.  A launch clears each tensor's amax word;
+// pass 1 takes the FP32 step (moments stored, w' written over the fp32
 // gradient, the largest finite |w'| folded into the amax word); pass 2
 // derives s_t' = fp32(amax / 2688) and re-encodes every block of w' with it.
+// The amax is a reduction over a whole tensor, so pass 2 of a tensor must
+// follow its pass 1 in a later launch; the launches pipeline the two passes
+// over groups of tensors (nvcs_step_kernel).
 // Scale array: s_t (fp32), the amax word, then one E4M3 code per 16 elements.
 // ---------------------------------------------------------------------------
 
@@ -1023,17 +1028,16 @@ __device__ __forceinline__ uint32_t nvcs_step_quad(const TensorDesc& d, int64_t 
   return amax;
 }
 
+// Pass 1 on one chunk: the FP32 step, moments stored, w' over the gradient,
+// the chunk's largest finite |w'| folded into its tensor's amax word.
 template <int SF, bool CLAMP>
-__global__ __launch_bounds__(kThreads) void nvcs_pass1_kernel(const TensorDesc* __restrict__ table,
-                                                              int ntab, TensorDesc single,
-                                                              Scalars s_arg,
-                                                              const Scalars* __restrict__ sdev) {
-  const Scalars s = sdev ? *sdev : s_arg;
-  const int64_t chunk = blockIdx.x;
+__device__ __forceinline__ void nvcs_pass1_chunk(const TensorDesc* __restrict__ table, int ntab,
+                                                 const TensorDesc& single, int64_t chunk,
+                                                 const Scalars& s) {
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float st = *(const float*)d.scales;
-  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
-  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
   const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
   MDraws mA, mB;
   if (d.vec_ok) {  // uniform: index base a multiple of 8
@@ -1075,19 +1079,18 @@ __device__ __forceinline__ void nvcs_requant(const TensorDesc& d, int64_t e, f4 
     store_scale<WF_NVFP4>((uint8_t*)d.scales + 4, (int64_t)((uint64_t)e / kNvBlock), sc);
 }
 
+// Pass 2 on one chunk: the tensor scale from its complete amax word, then
+// every block of the chunk re-encoded from w'.
 template <bool SR, bool COPY>
-__global__ __launch_bounds__(kThreads) void nvcs_pass2_kernel(const TensorDesc* __restrict__ table,
-                                                              int ntab, TensorDesc single,
-                                                              Scalars s_arg,
-                                                              const Scalars* __restrict__ sdev) {
-  const Scalars s = sdev ? *sdev : s_arg;
-  const int64_t chunk = blockIdx.x;
+__device__ __forceinline__ void nvcs_pass2_chunk(const TensorDesc* __restrict__ table, int ntab,
+                                                 const TensorDesc& single, int64_t chunk,
+                                                 const Scalars& s) {
   const TensorDesc d = find_tensor(table, ntab, single, chunk);
   const float amax_t = __uint_as_float(((const uint32_t*)d.scales)[1]);
   const float st = amax_t > 0.0f ? amax_t / 2688.0f : 1.0f;
   if (chunk == d.chunk0 && threadIdx.x == 0) *(float*)d.scales = st;  // pass 2 reads only the amax word
-  const int64_t c0 = (chunk - d.chunk0) * d.chunk_len;
-  const int64_t cend = (c0 + d.chunk_len < d.n) ? c0 + d.chunk_len : d.n;
+  const int64_t c0 = (chunk - d.chunk0) * kChunk;
+  const int64_t cend = (c0 + kChunk < d.n) ? c0 + kChunk : d.n;
   const int64_t eA = c0 + (int64_t)threadIdx.x * kQuad, eB = eA + kSub;
   const bool actA = eA < cend, actB = eB < cend;  // whole lane groups of a block agree
   f4 wa = f4{0.0f, 0.0f, 0.0f, 0.0f}, wb = wa;
@@ -1111,6 +1114,28 @@ __global__ __launch_bounds__(kThreads) void nvcs_pass2_kernel(const TensorDesc* 
   amaxB = block_amax<4>(amaxB);
   if (actA) nvcs_requant<SR, COPY>(d, eA, wa, amaxA, rA, st);
   if (actB) nvcs_requant<SR, COPY>(d, eB, wb, amaxB, rB, st);
+}
+
+// One launch of the pipelined current-scaling step: pass 1 over the chunks
+// [a1, a1 + n1) of one group of tensors and pass 2 over the chunks
+// [a2, a2 + n2) of the previous group, whose amax words the previous launch
+// completed.  The two kinds of workgroup are spread evenly over the grid
+// (n1 + n2 workgroups), so that the arithmetic-heavy re-encoding of one group
+// runs while the memory-heavy first pass of the next one streams.
+
+template <int SF, bool CLAMP, bool SR, bool COPY>
+__global__ __launch_bounds__(kThreads) void nvcs_step_kernel(const TensorDesc* __restrict__ table,
+                                                             int ntab, TensorDesc single,
+                                                             Scalars s_arg,
+                                                             const Scalars* __restrict__ sdev,
+                                                             NvcsSpan sp) {
+  const Scalars s = sdev ? *sdev : s_arg;
+  const int64_t b = blockIdx.x, n = sp.n1 + sp.n2;
+  const int64_t before = (b * sp.n2) / n;  // pass-2 workgroups ahead of this one
+  if (((b + 1) * sp.n2) / n > before)       // uniform per workgroup
+    nvcs_pass2_chunk<SR, COPY>(table, ntab, single, sp.a2 + before, s);
+  else
+    nvcs_pass1_chunk<SF, CLAMP>(table, ntab, single, sp.a1 + (b - before), s);
 }
 #endif  // MADD_IN_PART(9)
 
@@ -1333,9 +1358,11 @@ step_fn pick_part6(int gf, int sf, bool sr, bool clamp, bool copy);  // fp32 pas
 step_fn pick_part7(int gf, int sf, bool sr, bool clamp, bool copy);  // mxfp4 (block-scaled)
 step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy);  // nvfp4 (block-scaled)
 
-// NVFP4 with current scaling: its three kernels.
+// NVFP4 with current scaling: the amax-word clear and the pipelined step.
+typedef void (*nvcs_fn)(const TensorDesc*, int, TensorDesc, Scalars, const Scalars*, NvcsSpan);
 struct NvcsKernels {
-  step_fn clear, pass1, pass2;
+  step_fn clear;
+  nvcs_fn step;
 };
 NvcsKernels pick_part9(int sf, bool sr, bool clamp, bool copy);
 
@@ -1381,13 +1408,17 @@ step_fn pick_part8(int gf, int sf, bool sr, bool clamp, bool copy) {
 #endif
 
 #if MADD_IN_PART(9)
+template <int SF, bool CLAMP>
+nvcs_fn pick_nvcs_rounding(bool sr, bool copy) {
+  return sr ? (copy ? nvcs_step_kernel<SF, CLAMP, true, true> : nvcs_step_kernel<SF, CLAMP, true, false>)
+            : (copy ? nvcs_step_kernel<SF, CLAMP, false, true>
+                    : nvcs_step_kernel<SF, CLAMP, false, false>);
+}
 template <int SF>
 NvcsKernels pick_nvcs(bool sr, bool clamp, bool copy) {
   NvcsKernels k;
   k.clear = nvcs_clear_kernel;
-  k.pass1 = clamp ? nvcs_pass1_kernel<SF, true> : nvcs_pass1_kernel<SF, false>;
-  k.pass2 = sr ? (copy ? nvcs_pass2_kernel<true, true> : nvcs_pass2_kernel<true, false>)
-               : (copy ? nvcs_pass2_kernel<false, true> : nvcs_pass2_kernel<false, false>);
+  k.step = clamp ? pick_nvcs_rounding<SF, true>(sr, copy) : pick_nvcs_rounding<SF, false>(sr, copy);
   return k;
 }
 NvcsKernels pick_part9(int sf, bool sr, bool clamp, bool copy) {
@@ -1475,15 +1506,7 @@ Scalars make_scalars(const madd_hparams& hp) {
   return s;
 }
 
-int64_t chunks_of(int64_t n, int64_t len = kChunk) { return (n + len - 1) / len; }
-
-// Chunk length of a launch over `total` elements' worth of chunks: the
-// half-size chunk when the full-size ones would leave the CUs short of
-// workgroups (the results do not depend on it: every draw is keyed by the
-// element's global index).
-int32_t chunk_len_for(int64_t full_chunks) {
-  return full_chunks < kSmallLaunchChunks ? (int32_t)kSub : (int32_t)kChunk;
-}
+int64_t chunks_of(int64_t n) { return (n + kChunk - 1) / kChunk; }
 
 // Kernel launch that reports the launch's own status.  hipLaunchKernel
 // returns it directly, so the thread's last-error state, which belongs to
@@ -1538,15 +1561,10 @@ int32_t fill_device(void* dst, const void* src, size_t bytes, hipStream_t stream
 
 // The HIP side of the descriptor-table cache (policy in table_cache.h).
 struct HipTables {
-  using Event = hipEvent_t;
   bool alloc(size_t bytes, void** p) { return hipMalloc(p, bytes) == hipSuccess; }
-  void free(void* p) { (void)hipFree(p); }
   bool upload(void* dst, const void* src, size_t bytes, void* stream) {
     return fill_device(dst, src, bytes, (hipStream_t)stream) == MADD_OK;
   }
-  bool new_event(Event* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess; }
-  bool record(Event e, void* stream) { return hipEventRecord(e, (hipStream_t)stream) == hipSuccess; }
-  bool wait(Event e) { return hipEventSynchronize(e) == hipSuccess; }
 };
 HipTables g_hip_tables;
 madd_cache::TableCache<HipTables> g_tables;
@@ -1586,6 +1604,15 @@ int32_t cache_status(int rc) {
   }
 }
 
+// Identity of a stream for the cache: its handle, except for the per-thread
+// default stream, whose one handle names a different stream in every thread.
+uint64_t stream_key(hipStream_t stream) {
+  if (stream != hipStreamPerThread) return (uint64_t)(uintptr_t)stream;
+  static std::atomic<uint64_t> next{1};
+  thread_local const uint64_t id = (1ull << 63) | next.fetch_add(1);
+  return id;
+}
+
 // Whether `stream` is capturing a graph.
 int32_t capturing(hipStream_t stream, bool* cap) {
   hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
@@ -1603,21 +1630,55 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
 }
 
 // NVFP4 with current scaling: clear the amax words (one thread per tensor),
-// then the two passes over the same chunks.
+// then the passes.  Consecutive tensors form groups of at least
+// `group_chunks` chunks; launch j runs pass 1 of group j together with
+// pass 2 of group j - 1 (whose amax words launch j - 1 completed), so a
+// list of G groups takes G + 1 launches after the clear.  `descs` holds the
+// launch's tensors in table order (null for the single tensor of madd_step).
+//
+// Measured on the 7B list's NVFP4 linear layers (same process): with fp32
+// moments pass 1 is bound by HBM and pass 2 by VALU, and overlapping them
+// in groups of 65536 chunks took the step from 47.2 to 45.2 ms (16384:
+// 49.0, launch tails; 2^20: 47.2); with bf16 moments both passes are VALU
+// bound and one group (two launches) is fastest (38.6 against 40.0 ms).
+constexpr int64_t kNvcsGroupChunks = 65536;
+
+int64_t nvcs_group_chunks(int sfmt) {
+  return sfmt == MADD_S_FP32 ? kNvcsGroupChunks : INT64_MAX;
+}
+
 int32_t launch_nvcs(const NvcsKernels& k, const TensorDesc* table, int ntab,
-                    const TensorDesc& single, int64_t nchunks, const Scalars& s,
-                    const Scalars* sdev, hipStream_t stream) {
+                    const TensorDesc& single, const std::vector<TensorDesc>* descs,
+                    int64_t group_chunks, int64_t nchunks, const Scalars& s, const Scalars* sdev,
+                    hipStream_t stream) {
   if (nchunks <= 0) return MADD_OK;
   if (nchunks > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
+  std::vector<int64_t> cut{0};  // group boundaries in chunk space
+  if (descs) {
+    for (size_t i = 0; i < descs->size(); ++i) {
+      const int64_t end = (*descs)[i].chunk0 + chunks_of((*descs)[i].n);
+      if (end - cut.back() >= group_chunks || i + 1 == descs->size()) cut.push_back(end);
+    }
+  } else {
+    cut.push_back(nchunks);
+  }
   const unsigned clear_grid = (unsigned)(((ntab == 0 ? 1 : ntab) + kThreads - 1) / kThreads);
   int32_t rc = launch_k(k.clear, dim3(clear_grid), dim3(kThreads), stream, table, ntab, single, s,
                         sdev);
-  if (rc == MADD_OK)
-    rc = launch_k(k.pass1, dim3((unsigned)nchunks), dim3(kThreads), stream, table, ntab, single,
-                  s, sdev);
-  if (rc == MADD_OK)
-    rc = launch_k(k.pass2, dim3((unsigned)nchunks), dim3(kThreads), stream, table, ntab, single,
-                  s, sdev);
+  const size_t groups = cut.size() - 1;
+  for (size_t j = 0; j <= groups && rc == MADD_OK; ++j) {
+    NvcsSpan sp = {0, 0, 0, 0};
+    if (j < groups) {
+      sp.a1 = cut[j];
+      sp.n1 = cut[j + 1] - cut[j];
+    }
+    if (j > 0) {
+      sp.a2 = cut[j - 1];
+      sp.n2 = cut[j] - cut[j - 1];
+    }
+    rc = launch_k(k.step, dim3((unsigned)(sp.n1 + sp.n2)), dim3(kThreads), stream, table, ntab,
+                  single, s, sdev, sp);
+  }
   return rc;
 }
 
@@ -1635,7 +1696,6 @@ TensorDesc make_desc(void* w, void* scales, uint16_t* copy, const void* g, void*
   d.n = n;
   d.gbase = gbase;
   d.chunk0 = 0;
-  d.chunk_len = (int32_t)kChunk;
   d.vec_ok = al16(w) && al16(g) && al16(m) && al16(v) && al16(ve) && (!copy || al16(copy)) &&
              (gbase & 7) == 0;
   return d;
@@ -1758,47 +1818,35 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     size_t slot;
   };
   std::vector<Group> groups;
-  int64_t full_total = 0;
   for (int wf = MADD_W_BF16; wf <= MADD_W_NVFP4_CURRENT; ++wf) {
     for (int blk = 0; blk <= 1; ++blk) {
       std::vector<TensorDesc> descs;
-      int64_t gbase = index_base, full = 0;
+      int64_t gbase = index_base, nch = 0;
       for (int32_t i = 0; i < ntensors; ++i) {
         const bool is_blk = scales && scales[i];
         if (wfmt[i] == wf && (int)is_blk == blk && numel[i] > 0) {
-          descs.push_back(make_desc(w[i], is_blk ? scales[i] : nullptr,
-                                    copy ? copy[i] : nullptr, g[i], m[i], v[i], ve[i], numel[i],
-                                    gbase));
-          full += chunks_of(numel[i]);
+          TensorDesc d = make_desc(w[i], is_blk ? scales[i] : nullptr, copy ? copy[i] : nullptr,
+                                   g[i], m[i], v[i], ve[i], numel[i], gbase);
+          d.chunk0 = nch;
+          nch += chunks_of(numel[i]);
+          descs.push_back(d);
         }
         gbase += numel[i];
       }
       if (descs.empty()) continue;
-      full_total += full;
+      if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
       bool any_copy = false;
       for (const TensorDesc& d : descs) any_copy = any_copy || d.copy != nullptr;
       step_fn fn = nullptr;
-      NvcsKernels nvcs = {nullptr, nullptr, nullptr};
+      NvcsKernels nvcs = {nullptr, nullptr};
       if (wf == MADD_W_NVFP4_CURRENT) {
         nvcs = pick_part9(sfmt, sr, needs_clamp(*hp), any_copy);
       } else {
         fn = pick_kernel(wf, gfmt, sfmt, sr, needs_clamp(*hp), any_copy, blk != 0);
         if (!fn) return MADD_EUNSUPPORTED;
       }
-      groups.push_back(Group{fn, nvcs, std::move(descs), 0, nullptr, 0});
+      groups.push_back(Group{fn, nvcs, std::move(descs), nch, nullptr, 0});
     }
-  }
-  // One chunk length for the whole call, from its total size.
-  const int32_t len = chunk_len_for(full_total);
-  for (Group& gr : groups) {
-    int64_t nch = 0;
-    for (TensorDesc& d : gr.descs) {
-      d.chunk_len = len;
-      d.chunk0 = nch;
-      nch += chunks_of(d.n, len);
-    }
-    if (nch > 0x7FFFFFFFll) return MADD_EUNSUPPORTED;
-    gr.nchunks = nch;
   }
   hipStream_t st = (hipStream_t)stream;
   int dev = 0;
@@ -1826,7 +1874,8 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     for (const Group& gr : groups) {
       const int ntab = (int)gr.descs.size();
       rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
-                 : launch_nvcs(gr.nvcs, gr.table, ntab, none, gr.nchunks, s, sdev, st);
+                 : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, nvcs_group_chunks(sfmt),
+                               gr.nchunks, s, sdev, st);
       if (rc != MADD_OK) return rc;
     }
     return MADD_OK;
@@ -1838,7 +1887,7 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
   for (; acquired < groups.size(); ++acquired) {
     Group& gr = groups[acquired];
     void* t = nullptr;
-    rc = cache_status(g_tables.acquire(g_hip_tables, dev, gr.descs.data(),
+    rc = cache_status(g_tables.acquire(g_hip_tables, dev, stream_key(st), gr.descs.data(),
                                        gr.descs.size() * sizeof(TensorDesc), cap, st, &t,
                                        &gr.slot));
     if (rc != MADD_OK) break;
@@ -1848,14 +1897,10 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     const Group& gr = groups[k];
     const int ntab = (int)gr.descs.size();
     rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
-               : launch_nvcs(gr.nvcs, gr.table, ntab, none, gr.nchunks, s, sdev, st);
+               : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, nvcs_group_chunks(sfmt),
+                             gr.nchunks, s, sdev, st);
   }
-  const bool launched = rc == MADD_OK;
-  for (size_t k = 0; k < acquired; ++k) {
-    const int32_t r = cache_status(g_tables.release(g_hip_tables, groups[k].slot, cap, st,
-                                                    launched));
-    if (rc == MADD_OK) rc = r;
-  }
+  for (size_t k = 0; k < acquired; ++k) g_tables.release(groups[k].slot);
   return rc;
 }
 
@@ -1984,17 +2029,15 @@ int32_t madd_step(void* w, int32_t wfmt, void* scales, uint16_t* copy, const voi
     if (gfmt != MADD_G_FP32) return MADD_EINVAL;  // w' is written over the fp32 gradient
     const NvcsKernels k = pick_part9(sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                                      copy != nullptr);
-    TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-    d.chunk_len = chunk_len_for(chunks_of(n));
-    return launch_nvcs(k, nullptr, 0, d, chunks_of(n, d.chunk_len), s, nullptr,
+    const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
+    return launch_nvcs(k, nullptr, 0, d, nullptr, INT64_MAX, chunks_of(n), s, nullptr,
                        (hipStream_t)stream);
   }
   step_fn fn = pick_kernel(wfmt, gfmt, sfmt, hp->rounding == MADD_ROUND_SR, needs_clamp(*hp),
                            copy != nullptr, scales != nullptr);
   if (!fn) return MADD_EUNSUPPORTED;
-  TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
-  d.chunk_len = chunk_len_for(chunks_of(n));
-  return launch(fn, nullptr, 0, d, chunks_of(n, d.chunk_len), s, nullptr, (hipStream_t)stream);
+  const TensorDesc d = make_desc(w, scales, copy, g, m, v, ve, n, index_base);
+  return launch(fn, nullptr, 0, d, chunks_of(n), s, nullptr, (hipStream_t)stream);
 }
 
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,

@@ -207,7 +207,10 @@ def test_list_first_seen_during_capture_is_refused():
     """A list the library has not seen before cannot be captured (its table
     would have to be allocated and written inside the capture): the call
     returns MADD_ECAPTURE and touches nothing; stepped once outside the
-    capture, the list captures."""
+    capture, the list captures.  (Tables are cached by content -- pointers,
+    sizes, index bases -- and the allocator may hand this test the addresses
+    of an earlier test's tensors, so an index base no other call uses makes
+    the list new.)"""
     a, fmts = state(9)
     b, _ = state(9)
     tla, tlb = tl_of(a, fmts), tl_of(b, fmts)
@@ -216,14 +219,15 @@ def test_list_first_seen_during_capture_is_refused():
         gb.fill_(1e-3)
     torch.cuda.synchronize()
     h = W.hparams("c2", step=1)
+    base = 3 * 2 ** 40 + 4096
     graph = torch.cuda.CUDAGraph()
     with pytest.raises(B.MaddError, match="ECAPTURE"):
         with torch.cuda.graph(graph):
-            B.madd_multi_tensor_step(tla, h)
+            B.madd_multi_tensor_step(tla, h, index_base=base)
     torch.cuda.synchronize()
     assert_lists_equal(a, b, "refused capture")
-    B.madd_multi_tensor_step(tla, h)
-    B.madd_multi_tensor_step(tlb, h)
+    B.madd_multi_tensor_step(tla, h, index_base=base)
+    B.madd_multi_tensor_step(tlb, h, index_base=base)
     torch.cuda.synchronize()
     assert_lists_equal(a, b, "eager after refusal")
 
