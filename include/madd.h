@@ -369,6 +369,25 @@ int32_t madd_multi_tensor_step_dev(int32_t ntensors, void* const* w, const int32
 int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int64_t n,
                         int64_t index_base, const madd_hparams* hp, void* stream);
 
+/* Gradient of Appendix B's diagnostic loss on sampled entries: the loss is
+ * (1/B) sum over the B sampled entries k of c_i (w_i - w*_i)^4 (i the entry
+ * drawn as sample k, with replacement), whose gradient is
+ *   g_i = ((s_i d_i) d_i) d_i,  d_i = w_i - w*_i,  s_i = (fp32(4/B) cnt_i) c_i,
+ * cnt_i = number of samples equal to i, evaluated in fp32 in this order.
+ * w      : device weight codes of format wfmt (BF16, FP8 E4M3 / E5M2 or FP32;
+ *          4-bit formats are MADD_EINVAL), n elements, decoded exactly.
+ * target, c : device fp32 arrays of n elements (w* and the per-entry scale).
+ * idx    : device int64 array of the B = batch sampled entries (the random
+ *          draws are the caller's); entries outside [0, n) are skipped.
+ * counts : device int32 workspace of n elements (overwritten with cnt).
+ * g      : device fp32 output of n elements.
+ * Three launches on `stream` (clear counts, count with integer atomics, the
+ * gradient); results do not depend on the order of the samples.  Arrays
+ * must not overlap (MADD_EINVAL). */
+int32_t madd_toy_gradient(const void* w, int32_t wfmt, const float* target, const float* c,
+                          const int64_t* idx, int64_t batch, int64_t n, int32_t* counts,
+                          float* g, void* stream);
+
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* madd_status_string(int32_t status);
 

@@ -24,6 +24,8 @@ What each function follows in the paper:
                        step / quantize round trip does.
   * ``step_mx``     -- the same step on MXFP4 storage (E2M1 payloads, one
                        E8M0 scale per 32 elements; OCP's 4-bit block format).
+  * ``toy_gradient`` -- the gradient of Appendix B's sampled quartic loss
+                       (the diagnostic's workload, not the optimizer step).
   * ``encode`` / ``decode`` / ``encode_array`` / ``encode_block`` -- the
                        storage formats' value grids.
   * ``philox`` / ``draw16`` -- the counter-based generator that keys
@@ -317,6 +319,23 @@ def mx_values(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
     el = decode_array("e2m1", unpack_e2m1(q))
     sc = decode_array("e8m0", scales)
     return (el.reshape(-1, 32) * sc[:, None]).ravel()
+
+
+def toy_gradient(w: np.ndarray, target: np.ndarray, c: np.ndarray, idx: np.ndarray,
+                 batch: int) -> np.ndarray:
+    """Gradient of Appendix B's diagnostic loss on sampled entries,
+    (1/B) sum_k c_i (w_i - w*_i)^4 over the B sampled entries idx (with
+    replacement): g_i = (4/B) cnt_i c_i (w_i - w*_i)^3, cnt_i the number of
+    samples equal to i, in fp32 in the order ((s d) d) d with d = w - w* and
+    s = (fp32(4/B) cnt) c.  Plain numpy; pinned by its fp64 derivative and a
+    finite difference of the loss (tests/test_oracle_toy.py)."""
+    w = np.asarray(w, np.float32)
+    n = w.size
+    idx = np.asarray(idx, np.int64)
+    cnt = np.bincount(idx[(idx >= 0) & (idx < n)], minlength=n).astype(np.float32)
+    d = (w - np.asarray(target, np.float32)).astype(np.float32)
+    s = ((np.float32(4.0 / batch) * cnt).astype(np.float32) * np.asarray(c, np.float32)).astype(np.float32)
+    return (((s * d).astype(np.float32) * d).astype(np.float32) * d).astype(np.float32)
 
 
 def plain_step(wfmt: str, w: np.ndarray, g: np.ndarray, hp: dict, gfmt: str = "fp32",

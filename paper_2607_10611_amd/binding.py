@@ -35,7 +35,7 @@ STATUS = {0: "MADD_OK", -1: "MADD_EINVAL", -2: "MADD_EALIGN", -3: "MADD_EUNSUPPO
 
 EXPORTS = ("madd_init_state", "madd_encode_weights", "madd_step", "madd_multi_tensor_step",
            "madd_plain_step", "madd_status_string", "madd_scalars_bytes", "madd_prepare_scalars",
-           "madd_multi_tensor_step_dev", "madd_multi_tensor_step_noalloc")
+           "madd_multi_tensor_step_dev", "madd_multi_tensor_step_noalloc", "madd_toy_gradient")
 
 
 class MaddError(RuntimeError):
@@ -116,6 +116,8 @@ def lib():
         L.madd_multi_tensor_step.restype = I32
         L.madd_multi_tensor_step_noalloc.argtypes = L.madd_multi_tensor_step.argtypes
         L.madd_multi_tensor_step_noalloc.restype = I32
+        L.madd_toy_gradient.argtypes = [P, I32, P, P, P, I64, I64, P, P, P]
+        L.madd_toy_gradient.restype = I32
         L.madd_plain_step.argtypes = [P, I32, P, I32, I64, I64, HP, P]
         L.madd_plain_step.restype = I32
         L.madd_status_string.argtypes = [I32]
@@ -168,6 +170,11 @@ def scale_bytes(wfmt: str, n: int) -> int:
     if wfmt == "nvfp4_current":
         return 8 + n // NV_BLOCK
     return (n // 128) * 2
+
+
+def torch_dtype(name: str):
+    import torch
+    return getattr(torch, name)
 
 
 def _need(what: str, t, nbytes: int):
@@ -269,6 +276,20 @@ def madd_plain_step(w, wfmt: str, g, hp, gfmt: str = "fp32", index_base: int = 0
     _check("madd_plain_step",
            lib().madd_plain_step(_ptr(w), WFMT[wfmt], _ptr(g), GFMT[gfmt], w.numel(),
                                  int(index_base), ctypes.byref(h), _stream(stream)))
+
+
+def madd_toy_gradient(w, wfmt: str, target, c, idx, counts, g, stream=None):
+    """Gradient of Appendix B's sampled quartic loss into g (fp32); idx holds
+    the sampled entries (int64), counts is an int32 workspace of w's size."""
+    n = w.numel()
+    if idx.dtype != torch_dtype("int64") or counts.element_size() != 4:
+        raise ValueError("madd_toy_gradient: idx must be int64 and counts a 4-byte integer array")
+    for name, t, nb in (("target", target, 4 * n), ("c", c, 4 * n), ("counts", counts, 4 * n),
+                        ("g", g, 4 * n), ("idx", idx, 8 * idx.numel())):
+        _need(f"madd_toy_gradient: {name}", t, nb)
+    _check("madd_toy_gradient",
+           lib().madd_toy_gradient(_ptr(w), WFMT[wfmt], _ptr(target), _ptr(c), _ptr(idx),
+                                   idx.numel(), n, _ptr(counts), _ptr(g), _stream(stream)))
 
 
 class TensorList:

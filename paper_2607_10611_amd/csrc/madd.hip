@@ -1223,6 +1223,40 @@ __global__ __launch_bounds__(kThreads) void encode_block_kernel(const float* __r
 }
 
 #if MADD_IN_PART(0)
+// ---------------------------------------------------------------------------
+// Appendix B's diagnostic: the gradient of its sampled quartic loss
+// ---------------------------------------------------------------------------
+
+// counts[i] = number of sampled entries equal to i (entries outside [0, n)
+// are skipped).  Integer atomics: the counts do not depend on their order.
+__global__ __launch_bounds__(kThreads) void toy_count_kernel(const int64_t* __restrict__ idx,
+                                                             int64_t batch, int64_t n,
+                                                             int32_t* __restrict__ counts) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x; k < batch; k += stride) {
+    const int64_t i = idx[k];
+    if (i >= 0 && i < n) atomicAdd(&counts[i], 1);
+  }
+}
+
+// g_i = ((s d) d) d with d = w_i - target_i and s = (fob cnt_i) c_i, fob =
+// fp32(4 / B): the derivative of (1/B) sum_k c_i (w_i - target_i)^4 over the
+// B sampled entries, in this fixed fp32 order.
+template <int WF>
+__global__ __launch_bounds__(kThreads) void toy_grad_kernel(const void* w,
+                                                            const float* __restrict__ target,
+                                                            const float* __restrict__ c,
+                                                            const int32_t* __restrict__ counts,
+                                                            int64_t n, float fob,
+                                                            float* __restrict__ g) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) {
+    const float d = decode<WF>(ld1w<WF>(w, i)) - target[i];
+    const float s = (fob * (float)counts[i]) * c[i];
+    g[i] = ((s * d) * d) * d;
+  }
+}
+
 // One thread per 32-element MXFP4 block.
 __global__ __launch_bounds__(kThreads) void encode_mx_kernel(const float* __restrict__ x,
                                                              uint8_t* q, uint8_t* scales,
@@ -2068,6 +2102,43 @@ int32_t madd_plain_step(void* w, int32_t wfmt, const void* g, int32_t gfmt, int6
   const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
   return launch_k(fn, dim3(grid), dim3(kThreads), (hipStream_t)stream, w, g, n, index_base,
                   (float)hp->lr_add, s);
+}
+
+int32_t madd_toy_gradient(const void* w, int32_t wfmt, const float* target, const float* c,
+                          const int64_t* idx, int64_t batch, int64_t n, int32_t* counts,
+                          float* g, void* stream) {
+  if (n < 0 || n > kMaxN || batch < 0 || batch > kMaxN) return MADD_EINVAL;
+  if (!valid_wfmt(wfmt) || fp4_fmt(wfmt)) return MADD_EINVAL;
+  if (n == 0) return MADD_OK;
+  if (!w || !target || !c || !counts || !g || (batch > 0 && !idx)) return MADD_EINVAL;
+  {
+    const uint64_t u = (uint64_t)n;
+    const void* const p[6] = {w, target, c, counts, g, idx};
+    const uint64_t b[6] = {code_bytes(wfmt, n), 4u * u, 4u * u, 4u * u, 4u * u,
+                           8u * (uint64_t)batch};
+    if (!disjoint(p, b, 6)) return MADD_EINVAL;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t want = (n + kThreads - 1) / kThreads;
+  const dim3 grid((unsigned)(want < 65536 ? want : 65536)), block(kThreads);
+  int32_t rc = launch_k(zero_kernel<uint32_t>, grid, block, st, (uint32_t*)counts, n);
+  if (rc == MADD_OK && batch > 0) {
+    const int64_t wb = (batch + kThreads - 1) / kThreads;
+    rc = launch_k(toy_count_kernel, dim3((unsigned)(wb < 65536 ? wb : 65536)), block, st, idx,
+                  batch, n, counts);
+  }
+  if (rc != MADD_OK) return rc;
+  const float fob = (float)(4.0 / (double)(batch > 0 ? batch : 1));
+  switch (wfmt) {
+    case MADD_W_BF16:
+      return launch_k(toy_grad_kernel<WF_BF16>, grid, block, st, w, target, c, counts, n, fob, g);
+    case MADD_W_FP8_E4M3:
+      return launch_k(toy_grad_kernel<WF_E4M3>, grid, block, st, w, target, c, counts, n, fob, g);
+    case MADD_W_FP8_E5M2:
+      return launch_k(toy_grad_kernel<WF_E5M2>, grid, block, st, w, target, c, counts, n, fob, g);
+    default:
+      return launch_k(toy_grad_kernel<WF_FP32>, grid, block, st, w, target, c, counts, n, fob, g);
+  }
 }
 
 int32_t madd_multi_tensor_step(int32_t ntensors, void* const* w, const int32_t* wfmt,

@@ -3,10 +3,10 @@
 Minimises the sampled quartic loss of one regime (workloads.toy_regime):
 each step draws B entries uniformly with replacement and takes the gradient
 of (1/B) sum_k c_i (w_i - w*_i)^4 over the drawn entries,
-g_i = (4/B) cnt_i c_i (w_i - w*_i)^3, then applies one of the moment-free
-update rules (madd_plain_step) with round-to-nearest BF16 storage.  The
-gradient is workload arithmetic (torch on the device); the update is the
-library's kernel.
+g_i = (4/B) cnt_i c_i (w_i - w*_i)^3 (madd_toy_gradient), then applies one
+of the moment-free update rules (madd_plain_step) with round-to-nearest
+BF16 storage.  Both run as the library's HIP kernels; torch draws the
+sampled entries and holds the buffers.
 
 The paper writes the loss as c ||W - W*||_F^4 evaluated on sampled entries,
 with per-entry c in the mixed regime; the entrywise sampled reading above is
@@ -31,14 +31,6 @@ def rule_hparams(rule: str, lr: float, step: int) -> dict:
     return hp
 
 
-def toy_gradient(w, target, c, counts, batch: int):
-    """g = (4/B) cnt c (w - w*)^3 in fp32, as written (same operation order on
-    any device): ((s * d) * d) * d with s = (4/B) * cnt * c."""
-    d = w - target
-    sc = (4.0 / batch) * counts * c
-    return ((sc * d) * d) * d
-
-
 def run(regime: str, rule: str, lr: float, steps: int = 200, batch: int = W.TOY_N,
         seed: int = 0, device="cuda") -> dict:
     """Run one regime with one rule; returns final weights and summary metrics."""
@@ -54,14 +46,10 @@ def run(regime: str, rule: str, lr: float, steps: int = 200, batch: int = W.TOY_
     gen = torch.Generator(device=dev)
     gen.manual_seed(W.torch_seed(6, 1, seed))
     g = torch.empty(n, dtype=torch.float32, device=dev)
-    four_over_b = torch.tensor(4.0 / batch, dtype=torch.float32, device=dev)
+    counts = torch.empty(n, dtype=torch.int32, device=dev)
     for t in range(1, steps + 1):
-        w = codes.view(torch.bfloat16).float()
         idx = torch.randint(0, n, (batch,), generator=gen, device=dev)
-        cnt = torch.bincount(idx, minlength=n).to(torch.float32)
-        d = w - target
-        sc = (four_over_b * cnt) * cc
-        torch.mul(torch.mul(torch.mul(sc, d), d), d, out=g)
+        B.madd_toy_gradient(codes, "bf16", target, cc, idx, counts, g)
         B.madd_plain_step(codes, "bf16", g, rule_hparams(rule, lr, t))
     w = codes.view(torch.bfloat16).float().cpu().numpy().astype(np.float64)
     return dict(w=w, target=ws.astype(np.float64), w0=w0.astype(np.float64),

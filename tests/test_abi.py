@@ -276,6 +276,23 @@ def test_plain_step_rejects_bad_arguments():
 
 
 @fake_addresses
+def test_toy_gradient_rejects_bad_arguments():
+    lib = B.lib()
+    f = lib.madd_toy_gradient
+    n = 64
+    W_, T_, C_, I_, K_, G_ = (FAKE + k * (1 << 20) for k in range(6))
+    assert f(W_, 0, T_, C_, I_, 10, -1, K_, G_, None) == -1           # n < 0
+    assert f(W_, 0, T_, C_, I_, -1, n, K_, G_, None) == -1            # batch < 0
+    assert f(W_, B.W_MXFP4, T_, C_, I_, 10, n, K_, G_, None) == -1    # 4-bit storage
+    assert f(W_, 9, T_, C_, I_, 10, n, K_, G_, None) == -1            # unknown format
+    assert f(W_, 0, None, C_, I_, 10, n, K_, G_, None) == -1          # null target
+    assert f(W_, 0, T_, C_, None, 10, n, K_, G_, None) == -1          # samples, no idx
+    assert f(W_, 0, T_, C_, I_, 10, n, T_ + 8, G_, None) == -1        # counts inside target
+    assert f(W_, 0, T_, C_, I_, 10, n, K_, W_ + 64, None) == -1       # g overlaps w
+    assert f(None, 0, None, None, None, 0, 0, None, None, None) == 0  # empty
+
+
+@fake_addresses
 def test_init_and_encode_reject_bad_arguments():
     lib = B.lib()
     assert lib.madd_init_state(M_, V_, E_, 0, -1, None) == -1

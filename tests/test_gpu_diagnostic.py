@@ -1,6 +1,8 @@
-"""Appendix B's moment-free rules on the GPU (madd_plain_step): parity with
-the oracle, bit-exact trajectories of the diagnostic regimes, and the
-qualitative outcomes of the paper's diagnostic figure."""
+"""Appendix B's diagnostic on the GPU: the moment-free rules
+(madd_plain_step) and the gradient of the sampled quartic loss
+(madd_toy_gradient) against the oracle, bit-exact trajectories of the
+diagnostic regimes computed entirely on the GPU, and the qualitative
+outcomes of the paper's diagnostic figure."""
 import numpy as np
 import pytest
 import torch
@@ -54,21 +56,53 @@ def test_plain_step_bf16_gradients():
     assert (to_host(wd, np.uint16) == codes).all()
 
 
+@pytest.mark.parametrize("wfmt", ["bf16", "e4m3", "e5m2", "fp32"])
+def test_toy_gradient_kernel_matches_the_oracle(wfmt):
+    """madd_toy_gradient against oracle.toy_gradient bit for bit: entries
+    drawn several times, never drawn, out of range, zero differences."""
+    rng = np.random.default_rng(7)
+    n, batch = 5000, 7000
+    x = rng.normal(0, 2, n).astype(np.float32)
+    if wfmt in ("e4m3", "e5m2"):
+        x = np.clip(x, -448, 448)
+    codes = oracle.encode_array(wfmt, x)
+    w = oracle.decode_array(wfmt, codes).astype(np.float32)
+    target = rng.normal(0, 2, n).astype(np.float32)
+    target[::13] = w[::13]
+    c = (10.0 ** rng.uniform(-7, 8, n)).astype(np.float32)
+    idx = rng.integers(0, n, batch)
+    idx[:5] = [n, -1, n + 7, 3, 3]
+    counts = torch.full((n,), 77, dtype=torch.int32, device="cuda")
+    g = torch.full((n,), 1.0, device="cuda")
+    B.madd_toy_gradient(to_dev(codes), wfmt, to_dev(target), to_dev(c),
+                        torch.from_numpy(idx).cuda(), counts, g)
+    want = oracle.toy_gradient(w, target, c, idx, batch)
+    torch.cuda.synchronize()
+    got = to_host(g)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    ok = (idx >= 0) & (idx < n)
+    assert np.array_equal(to_host(counts), np.bincount(idx[ok], minlength=n))
+
+
 @pytest.mark.parametrize("regime", W.TOY_REGIMES)
 def test_diagnostic_trajectory_bit_exact(regime):
-    """Combined rule, 100 steps: the gradient is computed on the host from the
-    oracle's weights and handed to both sides."""
+    """Combined rule, 100 steps, everything on the GPU (madd_toy_gradient,
+    then madd_plain_step) against the oracle (toy_gradient, plain_step) on the
+    same sampled entries."""
     ws, w0, c = W.toy_regime(regime)
     codes = oracle.encode_array("bf16", w0)
     wd = to_dev(codes)
+    td, cd = to_dev(ws), to_dev(c)
+    g = torch.empty(W.TOY_N, device="cuda")
+    counts = torch.empty(W.TOY_N, dtype=torch.int32, device="cuda")
     rng = np.random.default_rng(1)
     for t in range(1, 101):
-        w = oracle.decode_array("bf16", codes).astype(np.float32)
-        cnt = np.bincount(rng.integers(0, W.TOY_N, W.TOY_N), minlength=W.TOY_N)
-        g = D.toy_gradient(w, ws, c, cnt.astype(np.float32), W.TOY_N).astype(np.float32)
+        idx = rng.integers(0, W.TOY_N, W.TOY_N)
         h = D.rule_hparams("combined", 10.0, t)
-        B.madd_plain_step(wd, "bf16", to_dev(g), h)
-        oracle.plain_step("bf16", codes, g, h)
+        B.madd_toy_gradient(wd, "bf16", td, cd, torch.from_numpy(idx).cuda(), counts, g)
+        B.madd_plain_step(wd, "bf16", g, h)
+        w = oracle.decode_array("bf16", codes).astype(np.float32)
+        oracle.plain_step("bf16", codes, oracle.toy_gradient(w, ws, c, idx, W.TOY_N), h)
     torch.cuda.synchronize()
     assert (to_host(wd, np.uint16) == codes).all()
 
