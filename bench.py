@@ -148,6 +148,8 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
             break
     codes = oracle.encode_array(wfmt, np.concatenate(xs))
     grads = [np.concatenate([g[t] for g in gs]) for t in range(steps)]
+    if sample >= 1 << 27:
+        log(f"oracle inputs ready: {sample:,} parameters, {steps} gradient sets")
     m, v, ve = (np.zeros(sample, np.float32 if sfmt == "fp32" else np.uint16) for _ in range(3))
     bounds = [(sample * k // threads) // 8 * 8 for k in range(threads)] + [sample]
 
@@ -164,6 +166,8 @@ def cpu_baseline(cfg: str, sample: int, steps: int, sfmt: str = "fp32", threads:
             h = W.hparams(cfg, step=done)
             list(ex.map(lambda k: part(k, (done - 1) % steps + 1, h), range(threads)))
             dt = time.perf_counter() - t0
+            if sample >= 1 << 27:
+                log(f"oracle step {done} done ({dt:.1f} s)")
     return {"value": sample * done / dt / 1e9, "unit": "Gparam/s", "cores": threads,
             "kind": "oracle",
             "sample": f"first {sample:,} parameters of the list, {done} steps cycling "
