@@ -570,15 +570,18 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
     args = [t.data_ptr() for t in (w, g, m, v, ve)] + [state_bytes, m.numel(), stream.cuda_stream]
     for _ in range(2):
         assert lib.madd_ceiling_stream(*args) == 0
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    # one pair of events around launches queued behind a GPU-side delay, as
+    # the smaller lists' steps are timed: an event recorded after every launch
+    # would add microseconds of stream time to each microsecond-scale probe
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
     gpu_delay(stream, steps)
     ev[0].record(stream)
-    for k in range(steps):
+    for _ in range(steps):
         assert lib.madd_ceiling_stream(*args) == 0
-        ev[k + 1].record(stream)
+    ev[1].record(stream)
     torch.cuda.synchronize()
-    ms = ev[0].elapsed_time(ev[-1]) / steps
+    ms = ev[0].elapsed_time(ev[1]) / steps
     gbs = alg_bytes / (ms / 1e3) / 1e9
     out = {"kernel": "madd_ceiling_stream (same buffers and bytes, no arithmetic)",
            "avg_launch_ms": round(ms, 4), "achieved": round(gbs, 1), "unit": "GB/s",
