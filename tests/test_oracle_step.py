@@ -545,8 +545,8 @@ def test_plain_rules_on_appendix_b_regimes():
         rng = np.random.default_rng(0)
         for t in range(1, steps + 1):
             w = oracle.decode_array("bf16", codes).astype(np.float32)
-            cnt = np.bincount(rng.integers(0, W.TOY_N, W.TOY_N), minlength=W.TOY_N)
-            g = D.toy_gradient(w, ws, c, cnt.astype(np.float32), W.TOY_N).astype(np.float32)
+            idx = rng.integers(0, W.TOY_N, W.TOY_N)
+            g = oracle.toy_gradient(w, ws, c, idx, W.TOY_N)
             oracle.plain_step("bf16", codes, g, D.rule_hparams(rule, lr, t))
         return oracle.decode_array("bf16", codes), ws, w0
 
