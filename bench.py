@@ -349,7 +349,6 @@ def main():
     grads = args.grads or ("regen" if nparam * 4 > (8 << 30) else "cycle")
     nsets = 1 if grads == "regen" else max(1, min(8, args.steps))
     gsets = [flat(torch.float32) for _ in range(nsets)]
-    gbuf = gsets[0][0]
     st_dt = torch.float32 if args.states == "fp32" else torch.int16
     mbuf, ms = flat(st_dt)
     vbuf, vs = flat(st_dt)
@@ -447,7 +446,7 @@ def main():
 
     ceiling = None
     if not args.no_ceiling and args.weights == "list" and wfmt == "bf16":
-        ceiling = stream_ceiling(wbuf[lo:hi], gbuf[lo:hi], mbuf[lo:hi], vbuf[lo:hi],
+        ceiling = stream_ceiling(wbuf[lo:hi], [gb[lo:hi] for gb, _ in gsets], mbuf[lo:hi], vbuf[lo:hi],
                                  vebuf[lo:hi], 4 if args.states == "fp32" else 2, args.steps,
                                  stream, alg_bytes, achieved)
         log(f"streaming ceiling: {ceiling['achieved']:.1f} GB/s; the step reaches "
@@ -554,9 +553,10 @@ def gpu_delay(stream, steps: int):
     assert lib.madd_probe_delay(min(sleeps, 1 << 20), stream.cuda_stream) == 0
 
 
-def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_gbs) -> dict:
+def stream_ceiling(w, gs, m, v, ve, state_bytes, steps, stream, alg_bytes, step_gbs) -> dict:
     """Time the streaming-ceiling probe (libmadd_probes.so) on the step's own
-    buffers: the same bytes and access pattern without the arithmetic."""
+    buffers: the same bytes and access pattern without the arithmetic, cycling
+    through the gradient sets `gs` in the order the timed steps used them."""
     import ctypes
 
     import torch
@@ -567,9 +567,10 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
     lib.madd_ceiling_stream.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int32, ctypes.c_int64,
                                                                 ctypes.c_void_p]
     lib.madd_ceiling_stream.restype = ctypes.c_int32
-    args = [t.data_ptr() for t in (w, g, m, v, ve)] + [state_bytes, m.numel(), stream.cuda_stream]
-    for _ in range(2):
-        assert lib.madd_ceiling_stream(*args) == 0
+    args = [[t.data_ptr() for t in (w, g, m, v, ve)] + [state_bytes, m.numel(), stream.cuda_stream]
+            for g in gs]
+    for k in range(2 * len(gs)):
+        assert lib.madd_ceiling_stream(*args[k % len(gs)]) == 0
     # one pair of events around launches queued behind a GPU-side delay, as
     # the smaller lists' steps are timed: an event recorded after every launch
     # would add microseconds of stream time to each microsecond-scale probe
@@ -577,8 +578,8 @@ def stream_ceiling(w, g, m, v, ve, state_bytes, steps, stream, alg_bytes, step_g
     torch.cuda.synchronize()
     gpu_delay(stream, steps)
     ev[0].record(stream)
-    for _ in range(steps):
-        assert lib.madd_ceiling_stream(*args) == 0
+    for k in range(steps):
+        assert lib.madd_ceiling_stream(*args[k % len(gs)]) == 0
     ev[1].record(stream)
     torch.cuda.synchronize()
     ms = ev[0].elapsed_time(ev[1]) / steps
