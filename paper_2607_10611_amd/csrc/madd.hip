@@ -1672,10 +1672,14 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
 //
 // Measured on the 7B list's NVFP4 linear layers (same process): with fp32
 // moments pass 1 is bound by HBM and pass 2 by VALU, and overlapping them
-// in groups of 65536 chunks took the step from 47.2 to 45.2 ms (16384:
-// 49.0, launch tails; 2^20: 47.2); with bf16 moments both passes are VALU
-// bound and one group (two launches) is fastest (38.6 against 40.0 ms).
-constexpr int64_t kNvcsGroupChunks = 65536;
+// takes the step from 47.2 ms (one group) to 43.8 ms with groups of at
+// least 40960 chunks (two groups per transformer layer; 36864-49152: within
+// 0.2 ms; 57344 and 65536: 45.2-45.5; 16384: 49.0, launch tails).  Keeping
+// w' in the Infinity Cache between the passes (temporal stores and loads,
+// pass 2 reading its group newest first) gained at most 0.3% more.  With
+// bf16 moments both passes are VALU bound and one group (two launches) is
+// fastest (38.6 against 40.0 ms).
+constexpr int64_t kNvcsGroupChunks = 40960;
 
 int64_t nvcs_group_chunks(int sfmt) {
   return sfmt == MADD_S_FP32 ? kNvcsGroupChunks : INT64_MAX;
