@@ -1677,13 +1677,9 @@ int32_t launch(step_fn fn, const TensorDesc* table, int ntab, const TensorDesc& 
 // 0.2 ms; 57344 and 65536: 45.2-45.5; 16384: 49.0, launch tails).  Keeping
 // w' in the Infinity Cache between the passes (temporal stores and loads,
 // pass 2 reading its group newest first) gained at most 0.3% more.  With
-// bf16 moments both passes are VALU bound and one group (two launches) is
-// fastest (38.6 against 40.0 ms).
+// bf16 moments both passes are VALU bound, and the same groups take the
+// step from 39.3 ms (one group) to 38.8 ms (65536: 40.9; 98304: 43.7).
 constexpr int64_t kNvcsGroupChunks = 40960;
-
-int64_t nvcs_group_chunks(int sfmt) {
-  return sfmt == MADD_S_FP32 ? kNvcsGroupChunks : INT64_MAX;
-}
 
 int32_t launch_nvcs(const NvcsKernels& k, const TensorDesc* table, int ntab,
                     const TensorDesc& single, const std::vector<TensorDesc>* descs,
@@ -1912,7 +1908,7 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     for (const Group& gr : groups) {
       const int ntab = (int)gr.descs.size();
       rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
-                 : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, nvcs_group_chunks(sfmt),
+                 : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, kNvcsGroupChunks,
                                gr.nchunks, s, sdev, st);
       if (rc != MADD_OK) return rc;
     }
@@ -1935,7 +1931,7 @@ static int32_t multi_tensor_step(int32_t ntensors, void* const* w, const int32_t
     const Group& gr = groups[k];
     const int ntab = (int)gr.descs.size();
     rc = gr.fn ? launch(gr.fn, gr.table, ntab, none, gr.nchunks, s, sdev, st)
-               : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, nvcs_group_chunks(sfmt),
+               : launch_nvcs(gr.nvcs, gr.table, ntab, none, &gr.descs, kNvcsGroupChunks,
                              gr.nchunks, s, sdev, st);
   }
   for (size_t k = 0; k < acquired; ++k) g_tables.release(groups[k].slot);
