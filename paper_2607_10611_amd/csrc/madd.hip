@@ -742,9 +742,14 @@ __global__ __launch_bounds__(kThreads, (kStepWaves<SF, COPY>)) void madd_step_ke
     const uint64_t gpair = (uint64_t)(d.gbase + tb) + 8u * (threadIdx.x >> 1);
     Quad<WF> qa, qb;
     MDraws mA, mB;
-    if (fullA && fullB) {
-      // Both sub-tiles whole (every tile but a tensor's last): loads grouped
-      // by array, so a wave's two requests to one array are adjacent spans.
+    if (tb + kTile <= cend) {  // uniform
+      // The whole tile lies in the tensor (every tile but a tensor's last).
+      // A uniform branch keeps this path straight-line, so the compiler waits
+      // for sub-tile A's loads alone before A's arithmetic and B's arithmetic
+      // does not wait for A's stores (1024x1024 step 7.60 -> 7.51 us, 7B list
+      // 34.38 -> 34.26 ms, same process; the same split of the block-scaled
+      // kernel made it 7-10% slower).  Loads grouped by array, so a wave's
+      // two requests to one array are adjacent spans.
       qa.w.load(d.w, eA);
       qb.w.load(d.w, eB);
       qa.g = ld4g<GF>(d.g, eA);
