@@ -18,8 +18,9 @@
 // owns one chunk.  A chunk is made of tiles of 2048 elements, each split into
 // two sub-tiles of 1024; thread t handles the four consecutive elements
 // [4t, 4t+4) of both sub-tiles, so every load and store instruction of a
-// wave covers one contiguous span (1 KiB for fp32 arrays) and all ten loads
-// of a tile are in flight before any arithmetic.  A workgroup finds its
+// wave covers one contiguous span (1 KiB for fp32 arrays); a tile's loads
+// are issued together, and in whole tiles the arithmetic of sub-tile A waits
+// only for A's loads.  A workgroup finds its
 // tensor by a binary search over the descriptor table (uniform, scalar
 // loads).  Loads and stores of the streamed arrays are non-temporal global
 // accesses: nothing is reused within a step.
